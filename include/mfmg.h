@@ -1,0 +1,214 @@
+/*
+ * mfmg.h -- C ABI of the MixFlow-MG meta-gradient library for MI355X (gfx950).
+ *
+ * The library computes the truncated-BPTT meta-gradient dV/deta of the bilevel
+ * problem (Section 2.1, eq. bilevel_opt_problem and eq. bptt_bilevel):
+ *
+ *   (theta_{i+1}, upsilon_{i+1}) = Upsilon(dL(theta_i, eta, x_i)/dtheta_i,
+ *                                          theta_i, upsilon_i, eta),  i = 0..T-1
+ *   V = V(theta_T, val)
+ *
+ * with the inner gradient an explicit argument of the update (Section 3,
+ * eq. reparam).  The reverse sweep follows the one-step recurrence of
+ * Section 3 (eq. bptt_recur) seeded by eq. dVdmeta; every Hessian-vector and
+ * mixed-derivative product it needs is formed forward-over-reverse
+ * (Section 2.2; Section 3, eq. vhp_to_hvp and eq. vmp_to_mvp): a tangent on
+ * theta rides through the inner gradient computation.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ *  - Pointers marked (dev) are device memory on the current HIP device, owned
+ *    by the caller.  Pointers marked (host) are host memory.
+ *  - The library never allocates or frees device memory inside a call.  All
+ *    scratch comes from the caller's workspace `ws` of `ws_bytes` bytes, whose
+ *    required size mfmg_query_sizes reports.  `ws` must be 256-byte aligned.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *    asynchronously on it; outputs are valid once the stream has reached the
+ *    end of the call.
+ *  - All arguments are validated on the host before anything is enqueued.  On
+ *    any status other than MFMG_OK nothing has been enqueued and no output has
+ *    been written; mfmg_last_error_message() describes the failure.  Errors of
+ *    the device execution itself surface at the caller's next synchronisation.
+ *  - Inputs are never modified; outputs are fully overwritten.
+ *  - Calls on the same workspace must not overlap in time; distinct
+ *    workspaces may be used concurrently on distinct streams.
+ *
+ * Parameter layout (flat float32 arrays)
+ * --------------------------------------
+ *  MLP: for each layer l = 0..n_layers-1, W_l row-major [widths[l]][widths[l+1]]
+ *  followed by b_l [widths[l+1]] when has_bias.  Linear regression is the
+ *  one-layer, bias-free, identity-activation MLP with squared loss.
+ *  opt_state (Adam): [m | v], each n_theta floats in the theta layout.
+ *  eta, by meta-parameter kind:
+ *   MFMG_META_LOGLR_PER_PARAM      n_theta log learning rates, theta layout;
+ *                                  update theta' = theta - exp(eta) * g.
+ *   MFMG_META_LOGLR_PER_LAYER_WD   n_layers log learning rates then one raw
+ *                                  decoupled weight decay omega (Adam).
+ *   MFMG_META_EXAMPLE_WEIGHT_LOGITS [T][rows] logits; example n of inner step
+ *                                  t has loss weight sigmoid(eta[t][n]).
+ *  The inner loss is L = (1/N) sum_n alpha_n l_n over the N rows of a batch,
+ *  alpha_n = 1 unless the loss is weighted; the outer loss V is the unweighted
+ *  mean over the validation rows.  l_n is softmax cross-entropy (CE) or the
+ *  squared error sum_j (z_nj - y_nj)^2 (MSE).
+ *
+ * Batches (mfmg_batch)
+ * --------------------
+ *  x (dev) float32 [rows][widths[0]] row-major; y (dev) int32 class labels
+ *  [rows] for CE or float32 targets [rows][widths[n_layers]] for MSE.
+ */
+#ifndef MFMG_H_
+#define MFMG_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MFMG_OK = 0,
+  MFMG_ERR_INVALID_ARGUMENT = 1, /* a null/misaligned pointer, a bad size or shape */
+  MFMG_ERR_UNSUPPORTED = 2,      /* a valid combination this build does not implement */
+  MFMG_ERR_WORKSPACE = 3,        /* ws_bytes smaller than mfmg_query_sizes reports */
+  MFMG_ERR_HIP = 4               /* a HIP runtime call failed while enqueueing */
+} mfmg_status;
+
+enum { MFMG_KIND_MLP = 0, MFMG_KIND_TRANSFORMER = 1 };
+enum { MFMG_ACT_TANH = 0, MFMG_ACT_GELU = 1, MFMG_ACT_RELU = 2, MFMG_ACT_NONE = 3 };
+enum { MFMG_LOSS_MSE = 0, MFMG_LOSS_CE = 1 };
+enum { MFMG_OPT_SGD = 0, MFMG_OPT_ADAM = 1 };
+enum {
+  MFMG_META_LOGLR_PER_PARAM = 0,
+  MFMG_META_LOGLR_PER_LAYER_WD = 1,
+  MFMG_META_EXAMPLE_WEIGHT_LOGITS = 2,
+  MFMG_META_TOKEN_WEIGHT_MLP = 3
+};
+/* FP32: float32 GEMM operands.  BF16: bfloat16 GEMM operands (round to nearest
+ * even) with float32 accumulation; parameters, optimiser state, adjoints and
+ * all elementwise arithmetic stay float32 in both modes. */
+enum { MFMG_PREC_FP32 = 0, MFMG_PREC_BF16 = 1 };
+
+#define MFMG_MAX_LAYERS 16
+
+/* Problem description.  Fields a kind does not use are ignored. */
+typedef struct {
+  int kind;                            /* MFMG_KIND_* */
+  int n_layers;                        /* MLP: number of weight matrices, 1..MFMG_MAX_LAYERS */
+  int widths[MFMG_MAX_LAYERS + 1];     /* MLP: widths[0] inputs .. widths[n_layers] outputs */
+  int act;                             /* hidden activation, MFMG_ACT_* */
+  int loss;                            /* MFMG_LOSS_* */
+  int optimizer;                       /* MFMG_OPT_* */
+  int meta;                            /* MFMG_META_* */
+  int precision;                       /* MFMG_PREC_* */
+  int has_bias;                        /* MLP: 0 or 1 */
+  int rows;                            /* rows of every training batch */
+  int val_rows;                        /* rows of the validation batch */
+  float sgd_lr;                        /* fixed inner learning rate (weighted-loss metas) */
+  float adam_b1, adam_b2, adam_eps;    /* Adam constants */
+  /* transformer fields (reserved) */
+  int d_model, n_heads, d_ff, vocab, seq, n_blocks, meta_hidden;
+  float ln_eps, rope_base;
+} mfmg_problem_desc;
+
+typedef struct mfmg_problem* mfmg_problem_t;
+
+/* Sizes, in elements (n_*) and bytes (*_bytes). */
+typedef struct {
+  size_t n_theta;              /* floats in theta */
+  size_t n_opt_state;          /* floats in opt_state (0 for SGD) */
+  size_t n_eta;                /* floats in eta (depends on T for EXAMPLE_WEIGHT_LOGITS) */
+  size_t workspace_bytes;      /* workspace mfmg_meta_grad needs at this T */
+  size_t static_bytes;         /* part of it that lives through the whole call
+                                  (theta checkpoints, adjoints, tangents) */
+  size_t dynamic_bytes;        /* part of it reused by every inner step
+                                  (one step's activations); independent of T */
+  size_t step_workspace_bytes; /* workspace mfmg_inner_step / mfmg_hvp_fwd_over_rev need */
+} mfmg_sizes;
+
+typedef struct {
+  const void* x;  /* (dev) see "Batches" above */
+  const void* y;  /* (dev) see "Batches" above */
+  int64_t rows;   /* must equal desc.rows (training) or desc.val_rows (validation) */
+} mfmg_batch;
+
+/* Validates `desc` and creates an immutable problem handle.  The handle holds
+ * host memory only and may be shared by threads.  INVALID_ARGUMENT for a bad
+ * description, UNSUPPORTED for a valid one this build does not implement. */
+mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* out);
+
+/* Releases a handle (NULL is ignored). */
+void mfmg_problem_destroy(mfmg_problem_t problem);
+
+/* Host-only size query for T inner steps (T >= 1).  No device work. */
+mfmg_status mfmg_query_sizes(mfmg_problem_t problem, int T, mfmg_sizes* out);
+
+/* One inner update (Section 2.1, eq. bptt_bilevel; Section 3, eq. reparam):
+ * g = dL(theta, eta, batch)/dtheta, then (theta_next, opt_state_next) =
+ * Upsilon(g, theta, opt_state, eta) with Adam's bias correction taken at update
+ * count step_index + 1.  step_index (0-based) also selects the loss weights of
+ * EXAMPLE_WEIGHT_LOGITS.
+ *   theta (dev, n_theta), opt_state (dev, n_opt_state; NULL = zeros; must be
+ *   NULL-or-valid for Adam, ignored for SGD), eta (dev, n_eta),
+ *   theta_next (dev, n_theta), opt_state_next (dev, n_opt_state; required for
+ *   Adam, ignored for SGD), grad_out (dev, n_theta, nullable), loss_out (dev,
+ *   1 float, nullable: L of this batch).
+ *   ws: at least step_workspace_bytes.  Outputs must not alias inputs. */
+mfmg_status mfmg_inner_step(mfmg_problem_t problem, const float* theta, const float* opt_state,
+                            const float* eta, const mfmg_batch* batch, int step_index,
+                            float* theta_next, float* opt_state_next, float* grad_out,
+                            float* loss_out, void* ws, size_t ws_bytes, void* stream);
+
+/* One forward-over-reverse pass (Section 2.2; Section 3, eq. vhp_to_hvp and
+ * eq. vmp_to_mvp; the JVP-of-gradient rule of the fwdrev_grad transformation,
+ * Section 3.1): with the tangent v on theta,
+ *   grad_out = dL/dtheta                                   (dev, n_theta, nullable)
+ *   hvp_out  = (d^2 L / dtheta^2) v                        (dev, n_theta)
+ *   mvp_out  = (d^2 L / dalpha_n dtheta) v, one float per loss row n
+ *              (= (1/N) <grad l_n, v>)                     (dev, rows floats, nullable)
+ * at theta (dev, n_theta) on one batch; eta and step_index select the loss
+ * weights alpha as in mfmg_inner_step.  v (dev, n_theta).
+ * ws: at least step_workspace_bytes. */
+mfmg_status mfmg_hvp_fwd_over_rev(mfmg_problem_t problem, const float* theta, const float* eta,
+                                  const mfmg_batch* batch, int step_index, const float* v,
+                                  float* grad_out, float* hvp_out, float* mvp_out, void* ws,
+                                  size_t ws_bytes, void* stream);
+
+/* The meta-gradient dV/deta through T inner steps (Algorithm 2, mixed-mode
+ * truncated BPTT), with per-inner-step checkpointing of theta_t (Section 4):
+ * the forward unroll stores theta_t (and Adam's state and inner gradients,
+ * Section 4 "saving inner gradients"); the reverse sweep i = T-1..0 recomputes
+ * step i from its checkpoint with a tangent, accumulating d eta.
+ *   theta0 (dev, n_theta), opt_state0 (dev, n_opt_state or NULL = zeros),
+ *   eta (dev, n_eta at this T), train_batches (host array of T descriptors
+ *   whose x/y are dev), val_batch (host descriptor, dev x/y),
+ *   d_eta_out (dev, n_eta), val_loss_out (dev, 1 float, nullable: V),
+ *   peak_bytes_out (host, nullable): bytes of device memory the call touches
+ *   at its peak: caller-visible inputs and outputs plus the workspace it uses.
+ * ws: at least workspace_bytes of mfmg_query_sizes(problem, T). */
+mfmg_status mfmg_meta_grad(mfmg_problem_t problem, const float* theta0, const float* opt_state0,
+                           const float* eta, const mfmg_batch* train_batches, int T,
+                           const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
+                           size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Static string naming a status. */
+const char* mfmg_status_string(mfmg_status status);
+
+/* Thread-local description of the last non-OK status returned on this thread. */
+const char* mfmg_last_error_message(void);
+
+/* Kernel timing instrumentation.  While enabled, every launch of the kernel
+ * classes below is bracketed by HIP events on its stream; mfmg_timing_read
+ * (after the caller has synchronised the stream) returns the number of
+ * launches and their summed duration, then clears that class.  Classes:
+ *   0 forward GEMM, 1 backward-data GEMM, 2 backward-weight GEMM (with update),
+ *   3 dual forward GEMM, 4 dual backward-data GEMM, 5 dual backward-weight GEMM
+ *   (with reverse accumulation), 6 loss head, 7 other elementwise kernels. */
+#define MFMG_NUM_KERNEL_CLASSES 8
+mfmg_status mfmg_timing_enable(int enable);
+mfmg_status mfmg_timing_read(int kernel_class, int* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MFMG_H_ */

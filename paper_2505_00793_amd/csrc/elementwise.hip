@@ -1,0 +1,491 @@
+// Elementwise and reduction kernels of the meta-gradient path (gfx950).
+//
+// All are HBM- or latency-bound: 64-lane wavefront reductions, coalesced
+// row-major traffic, LDS-staged transposes where a second layout is written.
+#include "kernels.h"
+#include "param_epi.h"
+
+namespace mfmg {
+
+namespace {
+
+inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+// ------------------------------------------------------------------------------------
+// float32 [rows][cols] -> operand copies in both layouts, through a 64x64 LDS tile.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ src, int rows,
+                                                      int cols, int lds, T* dst, int ldd, T* dstT,
+                                                      int lddT) {
+  __shared__ float tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    float v = 0.0f;
+    if (r < rows && c < cols) {
+      v = src[(long)r * lds + c];
+      if (dst) dst[(long)r * ldd + c] = Elem<T>::from_float(v);
+    }
+    tile[i][tx] = v;
+  }
+  if (!dstT) return;
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) dstT[(long)c * lddT + r] = Elem<T>::from_float(tile[tx][i]);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Bias entries: column sums of dZ (and its tangent) over the batch rows, read
+// from the transposed copies (one wavefront per column, contiguous reads),
+// then the per-parameter epilogue.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) bias_kernel(const T* __restrict__ dZT,
+                                                   const T* __restrict__ dZdT, int ld, int rows,
+                                                   ParamArgs<T> P) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= P.nout) return;
+  float g = 0.0f, hv = 0.0f;
+  for (int r = lane; r < rows; r += 64) {
+    g += Elem<T>::to_float(dZT[(long)n * ld + r]);
+    if (dZdT) hv += Elem<T>::to_float(dZdT[(long)n * ld + r]);
+  }
+  g = wave_sum(g);
+  hv = wave_sum(hv);
+  if (lane == 0) {
+    const float cv = param_elem(P, P.b_off + n, g, hv);
+    if (P.outb) P.outb[n] = cv;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Loss head, one wavefront per row.  Softmax cross-entropy:
+//   p = softmax(z), l = logsumexp(z) - z_y, dL/dz = (alpha/N)(p - e_y);
+// with the tangent zd of z (forward mode):
+//   ldot = <p - e_y, zd>,  d(dL/dz) = (alpha/N) p (zd - <p, zd>).
+// Squared error: l = |z - t|^2, dL/dz = (2 alpha/N)(z - t), ldot = 2<z - t, zd>,
+// d(dL/dz) = (2 alpha/N) zd.  ldot/N is the mixed product
+// (d^2 L / d alpha_n d theta) v of Section 3 (eq. vmp_to_mvp) for loss weights.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.rows) return;
+  const int C = a.C;
+  const float* z = a.Z + (long)row * C;
+  const float* zd = a.dual ? a.Zd + (long)row * C : nullptr;
+  float w = 1.0f;
+  if (a.alpha_logits) w = 1.0f / (1.0f + expf(-a.alpha_logits[row]));
+  const float scale = w * a.inv_n;
+  float loss = 0.0f, ldot = 0.0f;
+  if (a.loss == 1) {
+    float mx = -INFINITY;
+    for (int c = lane; c < C; c += 64) mx = fmaxf(mx, z[c]);
+    mx = wave_max(mx);
+    float se = 0.0f;
+    for (int c = lane; c < C; c += 64) se += expf(z[c] - mx);
+    se = wave_sum(se);
+    const float lse = mx + logf(se);
+    int y = a.labels[row];
+    if (y < 0 || y >= C) {  // invalid label: NaN loss, no target term
+      y = -1;
+      loss = NAN;
+    } else {
+      loss = lse - z[y];
+    }
+    float s = 0.0f;
+    if (a.dual) {
+      for (int c = lane; c < C; c += 64) s += expf(z[c] - lse) * zd[c];
+      s = wave_sum(s);
+      ldot = y >= 0 ? s - zd[y] : NAN;
+    }
+    for (int c = lane; c < C; c += 64) {
+      const float p = expf(z[c] - lse);
+      const float d = scale * (p - (c == y ? 1.0f : 0.0f));
+      a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
+      a.dT[(long)c * a.ldT + row] = Elem<T>::from_float(d);
+      if (a.dual) {
+        const float dd = scale * p * (zd[c] - s);
+        a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
+        a.ddT[(long)c * a.ldT + row] = Elem<T>::from_float(dd);
+      }
+    }
+  } else {
+    const float* t = a.targets + (long)row * C;
+    for (int c = lane; c < C; c += 64) {
+      const float r = z[c] - t[c];
+      loss += r * r;
+      const float d = 2.0f * scale * r;
+      a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
+      a.dT[(long)c * a.ldT + row] = Elem<T>::from_float(d);
+      if (a.dual) {
+        ldot += 2.0f * r * zd[c];
+        const float dd = 2.0f * scale * zd[c];
+        a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
+        a.ddT[(long)c * a.ldT + row] = Elem<T>::from_float(dd);
+      }
+    }
+    loss = wave_sum(loss);
+    ldot = wave_sum(ldot);
+  }
+  if (lane == 0) {
+    if (a.loss_rows) a.loss_rows[row] = loss;
+    if (a.mvp_rows) a.mvp_rows[row] = ldot * a.inv_n;
+    if (a.deta_rows) a.deta_rows[row] = w * (1.0f - w) * ldot * a.inv_n;
+  }
+}
+
+// Deterministic single-workgroup weighted sum.
+__global__ void __launch_bounds__(256) loss_reduce_kernel(const float* __restrict__ l,
+                                                          const float* __restrict__ alpha_logits,
+                                                          int rows, float inv_n, float* out) {
+  __shared__ float red[256];
+  float s = 0.0f;
+  for (int r = threadIdx.x; r < rows; r += 256) {
+    float w = alpha_logits ? 1.0f / (1.0f + expf(-alpha_logits[r])) : 1.0f;
+    s += w * l[r];
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = red[0] * inv_n;
+}
+
+// ------------------------------------------------------------------------------------
+// Adam, reverse step i before the dual pass.  With the step's recomputed
+// (m', v') from (m_i, v_i, g_i), t = i + 1, k1 = 1 - b1^t, k2 = 1 - b2^t,
+// D = sqrt(v'/k2) + eps, u = (m'/k1)/D, and incoming adjoints (tb, mb', vb'):
+//   ub        = -lr tb                                (adjoint of u)
+//   mb_tot    = mb' + ub / (k1 D)
+//   vb_tot    = vb' - ub (m'/k1) / (D^2 2 sqrt(v'/k2) k2)   (0 where v' = 0)
+//   v_g       = (1-b1) mb_tot + 2 (1-b2) g vb_tot     (tangent for the dual pass,
+//                                                      the normal VJP of eq. vhp_to_hvp)
+//   mb_i      = b1 mb_tot,  vb_i = b2 vb_tot
+//   tb_i      = tb (1 - lr omega) + H v_g             (H v_g added by the dual pass)
+//   d eta_l  += sum_layer -lr tb (u + omega theta)    (d lr / d eta_l = lr)
+//   d omega  += sum_all   -lr tb theta
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpArgs<T> a, float* partial) {
+  __shared__ float red0[256], red1[256];
+  const long nW = (long)a.nin * a.nout;
+  const long ntot = nW + (a.b_off >= 0 ? a.nout : 0);
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  float pe = 0.0f, po = 0.0f;
+  if (e < ntot) {
+    const bool isb = e >= nW;
+    const long idx = isb ? a.b_off + (e - nW) : a.w_off + e;
+    const float g = a.g[idx], m = a.m[idx], v = a.v[idx], th = a.theta[idx];
+    const float m1 = a.b1 * m + (1.0f - a.b1) * g;
+    const float v1 = a.b2 * v + (1.0f - a.b2) * g * g;
+    const float s = sqrtf(v1 / a.k2);
+    const float D = s + a.eps;
+    const float mh = m1 / a.k1;
+    const float u = mh / D;
+    const float lam = expf(a.eta[a.layer]);
+    const float om = a.eta[a.n_layers];
+    const float tb = a.thetabar[idx];
+    const float ub = -lam * tb;
+    const float mb = (a.first ? 0.0f : a.mbar[idx]) + ub / (a.k1 * D);
+    const float vbt = (a.first ? 0.0f : a.vbar[idx]) +
+                      (v1 > 0.0f ? -ub * mh / (D * D) / (2.0f * s * a.k2) : 0.0f);
+    const float vg = (1.0f - a.b1) * mb + 2.0f * (1.0f - a.b2) * g * vbt;
+    a.mbar[idx] = a.b1 * mb;
+    a.vbar[idx] = a.b2 * vbt;
+    a.thetabar[idx] = tb * (1.0f - lam * om);
+    pe = -lam * tb * (u + om * th);
+    po = -lam * tb * th;
+    if (isb) {
+      a.vb[e - nW] = vg;
+    } else {
+      const long mm = e / a.nout, nn = e % a.nout;
+      a.vW[mm * a.ldW + nn] = Elem<T>::from_float(vg);
+      a.vWT[nn * a.ldWT + mm] = Elem<T>::from_float(vg);
+    }
+  }
+  red0[threadIdx.x] = pe;
+  red1[threadIdx.x] = po;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      red0[threadIdx.x] += red0[threadIdx.x + o];
+      red1[threadIdx.x] += red1[threadIdx.x + o];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    partial[2 * blockIdx.x] = red0[0];
+    partial[2 * blockIdx.x + 1] = red1[0];
+  }
+}
+
+struct Offsets {
+  int off[MFMG_MAX_LAYERS + 1];
+};
+
+__global__ void adam_reduce_kernel(const float* __restrict__ partial, Offsets o, int n_layers,
+                                   int first, float* d_eta) {
+  __shared__ float red[256];
+  float tot_om = 0.0f;
+  for (int l = 0; l < n_layers; ++l) {
+    float s = 0.0f, so = 0.0f;
+    for (int b = o.off[l] + threadIdx.x; b < o.off[l + 1]; b += 256) {
+      s += partial[2 * b];
+      so += partial[2 * b + 1];
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+      if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) d_eta[l] = (first ? 0.0f : d_eta[l]) + red[0];
+    __syncthreads();
+    red[threadIdx.x] = so;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+      if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+      __syncthreads();
+    }
+    tot_om += red[0];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) d_eta[n_layers] = (first ? 0.0f : d_eta[n_layers]) + tot_om;
+}
+
+// ------------------------------------------------------------------------------------
+// Linear regression meta-gradient in one workgroup: squared loss
+// L = (1/N)|X theta - y|^2, SGD theta' = theta - exp(eta) g, V on the
+// validation batch.  Forward unroll with theta_t checkpoints, then the
+// reverse sweep with the dual pass (r, rdot) = (X theta - y, X v):
+// g = (2/N) X^T r, H v = (2/N) X^T rdot.
+// ------------------------------------------------------------------------------------
+constexpr int LR_MAXD = 256;
+constexpr int LR_MAXR = 1024;
+constexpr int LR_MAXT = 64;
+
+struct LinregArgs {
+  const float* theta0;
+  const float* eta;
+  const float* xs[LR_MAXT];  // device pointers of the T training batches
+  const float* ys[LR_MAXT];
+  int T, rows, d, vrows;
+  const float* vx;
+  const float* vy;
+  float* d_eta;
+  float* val_loss;
+  float* ckpt;  // (T + 1) x d
+};
+
+__global__ void __launch_bounds__(256) linreg_kernel(LinregArgs a) {
+  __shared__ float th[LR_MAXD], tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD], vv[LR_MAXD];
+  __shared__ float r[LR_MAXR], rd[LR_MAXR];
+  __shared__ float red[256];
+  const int tid = threadIdx.x, d = a.d;
+  for (int j = tid; j < d; j += 256) {
+    th[j] = a.theta0[j];
+    lam[j] = expf(a.eta[j]);
+    eb[j] = 0.0f;
+    a.ckpt[j] = th[j];
+  }
+  __syncthreads();
+  // forward unroll
+  for (int t = 0; t < a.T; ++t) {
+    const float* X = a.xs[t];
+    const float* y = a.ys[t];
+    const float inv = 2.0f / a.rows;
+    for (int n = tid; n < a.rows; n += 256) {
+      float s = -y[n];
+      for (int j = 0; j < d; ++j) s += X[(long)n * d + j] * th[j];
+      r[n] = s;
+    }
+    __syncthreads();
+    for (int j = tid; j < d; j += 256) {
+      float g = 0.0f;
+      for (int n = 0; n < a.rows; ++n) g += X[(long)n * d + j] * r[n];
+      th[j] -= lam[j] * inv * g;
+      a.ckpt[(long)(t + 1) * d + j] = th[j];
+    }
+    __syncthreads();
+  }
+  // validation loss and its gradient (the seed of the reverse sweep)
+  {
+    const float inv = 2.0f / a.vrows;
+    float ls = 0.0f;
+    for (int n = tid; n < a.vrows; n += 256) {
+      float s = -a.vy[n];
+      for (int j = 0; j < d; ++j) s += a.vx[(long)n * d + j] * th[j];
+      r[n] = s;
+      ls += s * s;
+    }
+    red[tid] = ls;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+      if (tid < o) red[tid] += red[tid + o];
+      __syncthreads();
+    }
+    if (tid == 0 && a.val_loss) *a.val_loss = red[0] / a.vrows;
+    for (int j = tid; j < d; j += 256) {
+      float g = 0.0f;
+      for (int n = 0; n < a.vrows; ++n) g += a.vx[(long)n * d + j] * r[n];
+      tb[j] = inv * g;
+    }
+    __syncthreads();
+  }
+  // reverse sweep
+  for (int i = a.T - 1; i >= 0; --i) {
+    const float* X = a.xs[i];
+    const float* y = a.ys[i];
+    const float inv = 2.0f / a.rows;
+    for (int j = tid; j < d; j += 256) {
+      th[j] = a.ckpt[(long)i * d + j];
+      vv[j] = -lam[j] * tb[j];
+    }
+    __syncthreads();
+    for (int n = tid; n < a.rows; n += 256) {
+      float s = -y[n], sd = 0.0f;
+      for (int j = 0; j < d; ++j) {
+        const float x = X[(long)n * d + j];
+        s += x * th[j];
+        sd += x * vv[j];
+      }
+      r[n] = s;
+      rd[n] = sd;
+    }
+    __syncthreads();
+    for (int j = tid; j < d; j += 256) {
+      float g = 0.0f, hv = 0.0f;
+      for (int n = 0; n < a.rows; ++n) {
+        const float x = X[(long)n * d + j];
+        g += x * r[n];
+        hv += x * rd[n];
+      }
+      eb[j] += -lam[j] * inv * g * tb[j];
+      tb[j] += inv * hv;
+    }
+    __syncthreads();
+  }
+  for (int j = tid; j < d; j += 256) a.d_eta[j] = eb[j];
+}
+
+__global__ void fill_kernel(float* p, long n, float v) {
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) p[i] = v;
+}
+
+__global__ void copy_kernel(const float* __restrict__ src, float* __restrict__ dst, long n) {
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    dst[i] = src[i];
+}
+
+}  // namespace
+
+hipError_t fill(float* p, long n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_kernel, dim3(min(cdiv(n, 256), 4096)), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t copy(const float* src, float* dst, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_kernel, dim3(min(cdiv(n, 256), 4096)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
+                          T* dstT, int lddT, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  dim3 grid(cdiv(cols, 64), cdiv(rows, 64));
+  hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
+                     dstT, lddT);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t bias_reduce(const T* dZT, const T* dZdT, int ld, int rows, const ParamArgs<T>& P,
+                       hipStream_t s) {
+  if (P.nout <= 0) return hipSuccess;
+  hipLaunchKernelGGL(bias_kernel<T>, dim3(cdiv(P.nout, 4)), dim3(256), 0, s, dZT, dZdT, ld, rows,
+                     P);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
+  hipLaunchKernelGGL(loss_kernel<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t loss_reduce(const float* loss_rows, const float* alpha_logits, int rows, float inv_n,
+                       float* loss_out, hipStream_t s) {
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, loss_rows, alpha_logits, rows,
+                     inv_n, loss_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks_used, hipStream_t s) {
+  const long ntot = (long)a.nin * a.nout + (a.b_off >= 0 ? a.nout : 0);
+  const int blocks = cdiv(ntot, 256);
+  *blocks_used = blocks;
+  hipLaunchKernelGGL(adam_vjp_kernel<T>, dim3(blocks), dim3(256), 0, s, a, a.partial);
+  return hipGetLastError();
+}
+
+hipError_t adam_reduce(const float* partial, const int* block_offsets, int n_layers, int first,
+                       float* d_eta, hipStream_t s) {
+  Offsets o;
+  for (int l = 0; l <= n_layers; ++l) o.off[l] = block_offsets[l];
+  hipLaunchKernelGGL(adam_reduce_kernel, dim3(1), dim3(256), 0, s, partial, o, n_layers, first,
+                     d_eta);
+  return hipGetLastError();
+}
+
+bool linreg_fits(int T, int rows, int vrows, int d) {
+  return T >= 1 && T <= LR_MAXT && d >= 1 && d <= LR_MAXD && rows >= 1 && rows <= LR_MAXR &&
+         vrows >= 1 && vrows <= LR_MAXR;
+}
+
+hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* const* xs,
+                            const float* const* ys, int T, int rows, int d, const float* vx,
+                            const float* vy, int vrows, float* d_eta, float* val_loss,
+                            float* scratch, hipStream_t s) {
+  LinregArgs a;
+  a.theta0 = theta0;
+  a.eta = eta;
+  for (int t = 0; t < LR_MAXT; ++t) {
+    a.xs[t] = t < T ? xs[t] : nullptr;
+    a.ys[t] = t < T ? ys[t] : nullptr;
+  }
+  a.T = T;
+  a.rows = rows;
+  a.d = d;
+  a.vrows = vrows;
+  a.vx = vx;
+  a.vy = vy;
+  a.d_eta = d_eta;
+  a.val_loss = val_loss;
+  a.ckpt = scratch;
+  hipLaunchKernelGGL(linreg_kernel, dim3(1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template hipError_t convert_matrix<bf16_t>(const float*, int, int, int, bf16_t*, int, bf16_t*, int, hipStream_t);
+template hipError_t convert_matrix<float>(const float*, int, int, int, float*, int, float*, int, hipStream_t);
+template hipError_t bias_reduce<bf16_t>(const bf16_t*, const bf16_t*, int, int, const ParamArgs<bf16_t>&, hipStream_t);
+template hipError_t bias_reduce<float>(const float*, const float*, int, int, const ParamArgs<float>&, hipStream_t);
+template hipError_t loss_head<bf16_t>(const LossArgs<bf16_t>&, hipStream_t);
+template hipError_t loss_head<float>(const LossArgs<float>&, hipStream_t);
+template hipError_t adam_vjp<bf16_t>(const AdamVjpArgs<bf16_t>&, int*, hipStream_t);
+template hipError_t adam_vjp<float>(const AdamVjpArgs<float>&, int*, hipStream_t);
+
+}  // namespace mfmg

@@ -1,0 +1,188 @@
+// Internal interfaces between the C ABI front end (api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+#include "mfmg.h"
+
+namespace mfmg {
+
+// ------------------------------------------------------------------------------------
+// Dual NT GEMM: every operand is stored with its contraction index contiguous.
+//   C1[m][n] = sum_k A[m][k] B[n][k]                      (flag G_C1)
+//   C2[m][n] = sum_k Ad[m][k] B[n][k] + A[m][k] Bd[n][k]  (flags G_AD, G_BD)
+// (A, Ad): M x K with leading dimension lda; (B, Bd): N x K with ldb.  Leading
+// dimensions are multiples of 16 bytes and base pointers are 16-byte aligned.
+// ------------------------------------------------------------------------------------
+enum GemmFlags { G_C1 = 1, G_AD = 2, G_BD = 4 };
+
+template <typename T>
+struct GemmOperands {
+  const T* A;
+  const T* Ad;
+  const T* B;
+  const T* Bd;
+  int lda, ldb;
+  int M, N, K;
+};
+
+// Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
+// ad = act'(z) zd.  Hidden layers store z (and zd) in float32 for the
+// backward and a (ad) as operands in both layouts; the output layer stores the
+// logits z (and zd) only.
+template <typename T>
+struct EpiActFwd {
+  const float* bias;     // [N] or null
+  const float* bias_d;   // [N] or null (tangent of the bias)
+  int act, last, dual;
+  int M, N;
+  float* Z;              // [M][N]
+  float* Zd;             // [M][N] (dual)
+  T* Ao;  T* AoT;        // [M][ldA], [N][ldAT]
+  T* Ado; T* AdoT;       // (dual)
+  int ldA, ldAT;
+};
+
+// Backward-data of one layer: C1 = dA of the previous layer's output, C2 its
+// tangent.  dz = dA * act'(z), dzd = dAd * act'(z) + dA * act''(z) * zd, stored
+// as operands in both layouts.
+template <typename T>
+struct EpiActBwd {
+  const float* Zp;       // [M][N] pre-activations of the previous layer
+  const float* Zdp;      // [M][N] their tangents (dual)
+  int act, dual;
+  int M, N;
+  T* dZ;  T* dZT;        // [M][ld], [N][ldT]
+  T* dZd; T* dZdT;
+  int ld, ldT;
+};
+
+// What the per-parameter epilogue does with (g, hv) = (C1, C2) of a
+// backward-weight GEMM (and of the bias reduction).
+enum ParamMode {
+  P_UPD_SGD_PP = 0,     // theta' = theta - exp(eta) g
+  P_UPD_SGD_FIXED = 1,  // theta' = theta - lr g
+  P_UPD_ADAM = 2,       // Adam with bias correction, per-layer lr, decoupled decay
+  P_SEED_SGD_PP = 3,    // tb = g (= dV/dtheta_T); v = -exp(eta) tb
+  P_SEED_SGD_FIXED = 4, // tb = g; v = -lr tb
+  P_SEED_ADAM = 5,      // tb = g
+  P_REV_SGD_PP = 6,     // eb (+)= -exp(eta) g tb; tb += hv; v = -exp(eta) tb
+  P_REV_SGD_FIXED = 7,  // tb += hv; v = -lr tb
+  P_REV_ADAM = 8,       // tb += hv
+  P_HVP = 9             // grad_out = g; hvp_out = hv
+};
+
+template <typename T>
+struct ParamArgs {
+  int mode;
+  int layer, n_layers;
+  int nin, nout;
+  long w_off, b_off;       // offsets of W_l and b_l in the flat theta layout
+  // update
+  const float* theta;      // theta_t
+  float* theta_next;
+  const float* eta;
+  float lr;
+  const float* m_in; const float* v_in;
+  float* m_out; float* v_out; float* g_save;
+  float b1, b2, eps, k1, k2;  // k1 = 1 - b1^t, k2 = 1 - b2^t
+  float* grad_out;
+  // reverse
+  float* thetabar;
+  float* etabar;
+  int first;
+  float* hvp_out;
+  // operand copies written by the epilogue (new theta for P_UPD_*, the next
+  // tangent for P_SEED_SGD_* and P_REV_SGD_*); each may be null
+  T* outW; T* outWT; float* outb;
+  int ldW, ldWT;
+};
+
+template <typename T>
+struct LossArgs {
+  int loss;                 // 0 MSE, 1 CE
+  int rows, C, dual;
+  float inv_n;
+  const float* Z;           // [rows][C] outputs
+  const float* Zd;          // [rows][C] their tangents (dual)
+  const int* labels;        // CE
+  const float* targets;     // MSE [rows][C]
+  const float* alpha_logits;  // per-row weight logits, or null (weights 1)
+  T* d; T* dT;              // dL/dz in both layouts [rows][ld], [C][ldT]
+  T* dd; T* ddT;            // its tangent (dual)
+  int ld, ldT;
+  float* loss_rows;         // l_n (unweighted), or null
+  float* mvp_rows;          // (1/N) ldot_n, or null
+  float* deta_rows;         // sigmoid'(eta_n) (1/N) ldot_n, or null
+};
+
+template <typename T>
+hipError_t gemm_act_fwd(const GemmOperands<T>& op, int flags, const EpiActFwd<T>& epi,
+                        hipStream_t s);
+template <typename T>
+hipError_t gemm_act_bwd(const GemmOperands<T>& op, int flags, const EpiActBwd<T>& epi,
+                        hipStream_t s);
+template <typename T>
+hipError_t gemm_param(const GemmOperands<T>& op, int flags, const ParamArgs<T>& P,
+                      hipStream_t s);
+
+// float32 matrix [rows][cols] (leading dim lds) -> operand copies dst [rows][ldd]
+// and dstT [cols][lddT] (either may be null).
+template <typename T>
+hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
+                          T* dstT, int lddT, hipStream_t s);
+
+// Column sums over rows of dZT [nout][ld] (and dZdT) -> per-parameter epilogue
+// on the bias entries of layer P.layer.
+template <typename T>
+hipError_t bias_reduce(const T* dZT, const T* dZdT, int ld, int rows, const ParamArgs<T>& P,
+                       hipStream_t s);
+
+template <typename T>
+hipError_t loss_head(const LossArgs<T>& a, hipStream_t s);
+
+// loss_out = (1/N) sum_n alpha_n l_n (alpha from logits, or 1).
+hipError_t loss_reduce(const float* loss_rows, const float* alpha_logits, int rows, float inv_n,
+                       float* loss_out, hipStream_t s);
+
+// Adam's reverse step before the dual pass (see adam_vjp in elementwise.hip).
+template <typename T>
+struct AdamVjpArgs {
+  int layer, n_layers, nin, nout;
+  long w_off, b_off;
+  int first;                     // adjoints of m and v are zero (i = T-1)
+  float b1, b2, eps, k1, k2;
+  const float* eta;
+  const float* theta; const float* m; const float* v; const float* g;   // step i state
+  float* thetabar; float* mbar; float* vbar;                            // in/out
+  T* vW; T* vWT; float* vb; int ldW, ldWT;                              // tangent out
+  float* partial;                // [blocks][2]: (eta_l partial, omega partial)
+};
+template <typename T>
+hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks_used, hipStream_t s);
+
+// d_eta[layer] (+)= sum partial[l][.][0]; d_eta[L] (+)= sum of all partial[.][1].
+hipError_t adam_reduce(const float* partial, const int* block_offsets, int n_layers, int first,
+                       float* d_eta, hipStream_t s);
+
+// Linear regression, SGD with per-parameter log learning rates, squared loss:
+// the whole meta-gradient in one workgroup.  xs, ys: host arrays of T device
+// pointers; scratch: (T + 1) * d floats of device memory.
+hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* const* xs,
+                            const float* const* ys, int T, int rows, int d, const float* vx,
+                            const float* vy, int vrows, float* d_eta, float* val_loss,
+                            float* scratch, hipStream_t s);
+bool linreg_fits(int T, int rows, int vrows, int d);
+
+// Fill / copy float arrays with kernels (no memset or memcpy nodes, so the
+// calls stay safe inside captured HIP graphs).
+hipError_t fill(float* p, long n, float v, hipStream_t s);
+hipError_t copy(const float* src, float* dst, long n, hipStream_t s);
+
+// Kernel timing (api.hip).
+void timing_begin(int cls, hipStream_t s);
+void timing_end(int cls, hipStream_t s);
+
+}  // namespace mfmg

@@ -1,0 +1,53 @@
+"""Shared test helpers: workload config -> ABI description, device upload, error metrics."""
+from __future__ import annotations
+
+import numpy as np
+
+import workloads as W
+
+FP32_TOL = 1e-4   # float32 GEMM operands
+BF16_TOL = 2e-2   # bfloat16 GEMM operands, against the oracle's bf16-emulation mode
+
+
+def desc_of(cfg: W.Config):
+    from paper_2505_00793_amd import _lib as M
+    return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
+                       meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
+                       rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
+                       adam_b1=cfg.adam_b1, adam_b2=cfg.adam_b2, adam_eps=cfg.adam_eps)
+
+
+def tol_of(cfg: W.Config) -> float:
+    return BF16_TOL if cfg.precision == W.PREC_BF16 else FP32_TOL
+
+
+def relerr(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64).ravel()
+    b = np.asarray(b, dtype=np.float64).ravel()
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def eta_groups(cfg: W.Config):
+    """Index groups over which the normwise error of d eta is taken: each
+    per-layer log-lr and the weight decay separately; otherwise all of eta."""
+    n = W.n_eta(cfg)
+    if cfg.meta == W.META_LOGLR_PER_LAYER_WD:
+        return [np.array([i]) for i in range(n)]
+    return [np.arange(n)]
+
+
+def group_errors(cfg, got, ref):
+    return [relerr(np.asarray(got)[g], np.asarray(ref)[g]) for g in eta_groups(cfg)]
+
+
+def to_device(inp: dict, device="cuda"):
+    import torch
+
+    def t(a):
+        return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+    return {
+        "theta0": t(inp["theta0"]), "eta": t(inp["eta"]), "opt_state0": t(inp["opt_state0"]),
+        "xs": [t(x) for x in inp["train_x"]], "ys": [t(y) for y in inp["train_y"]],
+        "vx": t(inp["val_x"]), "vy": t(inp["val_y"]),
+    }

@@ -1,0 +1,130 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, validates descriptions and arguments on the host, and
+reports sizes.  No call here reaches a kernel launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import workloads as W
+from helpers import desc_of
+
+M = pytest.importorskip("paper_2505_00793_amd._lib")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(M.LIB_PATH):
+        pytest.skip("libmfmg.so not built")
+    return M.lib()
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "mfmg.h")).read()
+    return sorted(set(re.findall(r"^(?:mfmg_status|void|const char\*)\s+(mfmg_\w+)\(", src, re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    declared = header_functions()
+    assert len(declared) >= 9
+    for name in declared:
+        assert hasattr(L, name), name
+    assert sorted(M.EXPORTED) == declared
+
+
+def test_status_strings(L):
+    for s in range(5):
+        assert L.mfmg_status_string(s).decode().startswith("MFMG_")
+
+
+@pytest.mark.parametrize("cfg", [W.C1, W.C2, W.C3, W.C5], ids=lambda c: c.name)
+def test_sizes_match_layout(L, cfg):
+    p = M.Problem(desc_of(cfg))
+    s = p.mfmg_query_sizes(cfg.T)
+    assert s.n_theta == W.n_theta(cfg)
+    assert s.n_eta == W.n_eta(cfg)
+    assert s.n_opt_state == W.n_opt_state(cfg)
+    assert s.workspace_bytes == s.static_bytes + s.dynamic_bytes or s.dynamic_bytes == 0
+
+
+def test_static_memory_grows_only_with_checkpoints(L):
+    """Workspace per extra inner step = one checkpoint of theta's GEMM operands
+    (bf16, two layouts: 4 bytes per weight + 4 per bias, up to 256-byte
+    alignment); the dynamic part does not depend on T."""
+    cfg = W.C5
+    p = M.Problem(desc_of(cfg))
+    sizes = {T: p.mfmg_query_sizes(T) for T in W.C5_TS}
+    n_w = sum(cfg.widths[l] * cfg.widths[l + 1] for l in range(cfg.n_layers))
+    n_b = sum(cfg.widths[1:])
+    per_step = 4 * n_w + 4 * n_b
+    dyn = {s.dynamic_bytes for s in sizes.values()}
+    assert len(dyn) == 1
+    for a, b in zip(W.C5_TS, W.C5_TS[1:]):
+        slope = (sizes[b].static_bytes - sizes[a].static_bytes) / (b - a)
+        assert abs(slope - per_step) <= 3 * 256 * cfg.n_layers
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("n_layers", 0, M.ERR_INVALID_ARGUMENT if M else 1),
+    ("act", 9, 1), ("loss", 5, 1), ("precision", 3, 1), ("rows", 0, 1),
+    ("kind", 1, 2), ("meta", 3, 2), ("optimizer", 1, 2),
+])
+def test_create_rejects_bad_descriptions(L, field, value, status):
+    d = desc_of(W.C2)
+    setattr(d, field, value)
+    h = ctypes.c_void_p()
+    st = L.mfmg_problem_create(ctypes.byref(d), ctypes.byref(h))
+    assert st == status
+    assert not h.value
+    assert len(L.mfmg_last_error_message()) > 0
+
+
+FAKE = 0x7f0000000000  # never dereferenced: every call below fails validation first
+
+
+def _meta_call(L, p, T, rows=None, ws_bytes=None, ws=FAKE, x=FAKE, d_eta=FAKE):
+    cfg_rows = p.desc.rows
+    b = (M.mfmg_batch * max(T, 1))(*[M.mfmg_batch(x, FAKE, rows or cfg_rows) for _ in range(max(T, 1))])
+    vb = M.mfmg_batch(FAKE, FAKE, p.desc.val_rows)
+    need = p.mfmg_query_sizes(max(T, 1)).workspace_bytes
+    peak = ctypes.c_size_t(0)
+    return L.mfmg_meta_grad(p.handle, ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), b, T,
+                            ctypes.byref(vb), ctypes.c_void_p(d_eta) if d_eta else None, None,
+                            ctypes.byref(peak), ctypes.c_void_p(ws) if ws else None,
+                            need if ws_bytes is None else ws_bytes, None)
+
+
+def test_meta_grad_argument_errors(L):
+    p = M.Problem(desc_of(W.C2))
+    assert _meta_call(L, p, 0) == M.ERR_INVALID_ARGUMENT
+    assert _meta_call(L, p, 2, rows=W.C2.rows + 1) == M.ERR_INVALID_ARGUMENT
+    assert _meta_call(L, p, 2, ws_bytes=100) == M.ERR_WORKSPACE
+    assert b"workspace" in L.mfmg_last_error_message()
+    assert _meta_call(L, p, 2, ws=FAKE + 8) == M.ERR_INVALID_ARGUMENT
+    assert _meta_call(L, p, 2, ws=0) == M.ERR_INVALID_ARGUMENT
+    assert _meta_call(L, p, 2, d_eta=0) == M.ERR_INVALID_ARGUMENT
+    assert _meta_call(L, p, 2, x=0) == M.ERR_INVALID_ARGUMENT
+
+
+def test_step_argument_errors(L):
+    p = M.Problem(desc_of(W.C3))
+    b = M.mfmg_batch(FAKE, FAKE, W.C3.rows)
+    need = p.mfmg_query_sizes(1).step_workspace_bytes
+    # Adam without opt_state_next
+    st = L.mfmg_inner_step(p.handle, FAKE, None, FAKE, ctypes.byref(b), 0, FAKE, None, None, None,
+                           FAKE, need, None)
+    assert st == M.ERR_INVALID_ARGUMENT
+    st = L.mfmg_hvp_fwd_over_rev(p.handle, FAKE, FAKE, ctypes.byref(b), 0, FAKE, None, FAKE, None,
+                                 FAKE, need - 1, None)
+    assert st == M.ERR_WORKSPACE
+    st = L.mfmg_hvp_fwd_over_rev(p.handle, FAKE, FAKE, ctypes.byref(b), -1, FAKE, None, FAKE, None,
+                                 FAKE, need, None)
+    assert st == M.ERR_INVALID_ARGUMENT
+
+
+def test_timing_read_validates(L):
+    n, ms = ctypes.c_int(), ctypes.c_double()
+    assert L.mfmg_timing_read(99, ctypes.byref(n), ctypes.byref(ms)) == M.ERR_INVALID_ARGUMENT

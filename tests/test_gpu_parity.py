@@ -1,0 +1,186 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Float32-operand problems are gated at 1e-4, bf16-operand problems at 2e-2
+(normwise relative error per eta group), the latter against the oracle's
+bf16-operand emulation.  Sizes span several GEMM tiles and ragged tails.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import desc_of, eta_groups, group_errors, relerr, to_device, tol_of
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_00793_amd import _lib
+    _lib.lib()  # fails loudly when the library is missing
+
+
+def M():
+    from paper_2505_00793_amd import _lib
+    return _lib
+
+
+def _sig(x):
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+def step_alpha(cfg, eta, step):
+    if cfg.meta == W.META_EXAMPLE_WEIGHT_LOGITS:
+        return _sig(eta.astype(np.float64).reshape(-1, cfg.rows)[step])
+    return None
+
+
+def run_meta(cfg, inp):
+    P = M().Problem(desc_of(cfg))
+    dev = to_device(inp)
+    d = torch.full((W.n_eta(cfg),), float("nan"), device="cuda")
+    vl = torch.full((1,), float("nan"), device="cuda")
+    peak = P.mfmg_meta_grad(dev["theta0"], dev["opt_state0"], dev["eta"], dev["xs"], dev["ys"],
+                            dev["vx"], dev["vy"], d, vl)
+    torch.cuda.synchronize()
+    return d.cpu().numpy().astype(np.float64), float(vl.item()), peak
+
+
+META_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small",
+              "c3_small", "c1_linreg", "c2_mlp_tanh_lossweights"]
+
+
+def cfg_of(name):
+    return W.SMALL.get(name) or W.CONFIGS[name]
+
+
+@pytest.mark.parametrize("name", META_CASES)
+def test_meta_grad_parity(name):
+    cfg = cfg_of(name)
+    inp = W.make_inputs(cfg)
+    print(f"\n[meta_grad] {name} T={cfg.T}", flush=True)
+    got, V, peak = run_meta(cfg, inp)
+    bf16 = cfg.precision == W.PREC_BF16
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=bf16)
+    errs = group_errors(cfg, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]}  V {V:.6f} ref {Vref:.6f}", flush=True)
+    if bf16:
+        ref64, _ = oracle.meta_grad_checkpointed(cfg, inp)
+        print(f"  distance of the bf16 result to the fp64 oracle: "
+              f"{['%.2e' % e for e in group_errors(cfg, got, ref64)]}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+    assert peak > 0
+
+
+INNER_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_small", "c3_small"]
+
+
+@pytest.mark.parametrize("name", INNER_CASES)
+def test_inner_step_parity(name):
+    cfg = cfg_of(name)
+    inp = W.make_inputs(cfg)
+    step = 1
+    n = W.n_theta(cfg)
+    theta = inp["theta0"] + 0.01 * W.random_direction(n, 11)
+    opt = None
+    if cfg.optimizer == W.OPT_ADAM:
+        m = 0.01 * W.random_direction(n, 12)
+        v = (0.01 * W.random_direction(n, 13)) ** 2
+        opt = np.concatenate([m, v]).astype(np.float32)
+    x, y = inp["train_x"][step], inp["train_y"][step]
+    bf16 = cfg.precision == W.PREC_BF16
+    print(f"\n[inner_step] {name}", flush=True)
+    th1_ref, opt1_ref, g_ref, L_ref = oracle.inner_step(
+        cfg, theta, opt, inp["eta"], x, y, step, alpha=step_alpha(cfg, inp["eta"], step), bf16=bf16)
+    P = M().Problem(desc_of(cfg))
+    c = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    th1 = torch.empty(n, device="cuda")
+    g = torch.empty(n, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    opt1 = torch.empty(2 * n, device="cuda") if opt is not None else None
+    P.mfmg_inner_step(c(theta), c(opt) if opt is not None else None, c(inp["eta"]), c(x), c(y),
+                      step, th1, opt1, g, loss)
+    torch.cuda.synchronize()
+    tol = tol_of(cfg)
+    e_g = relerr(g.cpu().numpy(), g_ref)
+    e_up = relerr(th1.cpu().numpy() - theta, th1_ref - theta)
+    print(f"  grad {e_g:.2e} update {e_up:.2e} loss {loss.item():.6f} ref {L_ref:.6f}", flush=True)
+    assert e_g <= tol and e_up <= (tol if cfg.optimizer == W.OPT_SGD else 5 * tol)
+    assert abs(loss.item() - L_ref) <= tol * abs(L_ref)
+    if opt is not None:
+        assert relerr(opt1.cpu().numpy()[:n], opt1_ref[:n]) <= tol
+        assert relerr(opt1.cpu().numpy()[n:], opt1_ref[n:]) <= tol
+
+
+HVP_CASES = ["c1_small", "c2_small", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c3_small"]
+
+
+@pytest.mark.parametrize("name", HVP_CASES)
+def test_hvp_parity(name):
+    cfg = cfg_of(name)
+    inp = W.make_inputs(cfg)
+    n = W.n_theta(cfg)
+    step = 0
+    theta = inp["theta0"]
+    v = W.random_direction(n, 21)
+    x, y = inp["train_x"][step], inp["train_y"][step]
+    bf16 = cfg.precision == W.PREC_BF16
+    alpha = step_alpha(cfg, inp["eta"], step)
+    print(f"\n[hvp] {name}", flush=True)
+    hv_ref = oracle.hvp_rev_rev(cfg, theta, x, y, v, alpha=alpha, bf16=bf16)
+    mv_ref = oracle.mvp_rev_rev(cfg, theta, x, y, v, alpha=alpha, bf16=bf16)
+    g_ref, _ = oracle.grad_and_loss(cfg, theta, x, y, alpha=alpha, bf16=bf16)
+    P = M().Problem(desc_of(cfg))
+    c = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    g = torch.empty(n, device="cuda")
+    hv = torch.empty(n, device="cuda")
+    mv = torch.empty(cfg.rows, device="cuda")
+    P.mfmg_hvp_fwd_over_rev(c(theta), c(inp["eta"]), c(x), c(y), step, c(v), g, hv, mv)
+    torch.cuda.synchronize()
+    e = (relerr(g.cpu().numpy(), g_ref), relerr(hv.cpu().numpy(), hv_ref),
+         relerr(mv.cpu().numpy(), mv_ref))
+    print(f"  grad {e[0]:.2e} hvp {e[1]:.2e} mvp {e[2]:.2e}", flush=True)
+    assert max(e) <= tol_of(cfg)
+
+
+def test_hvp_symmetry_full_size_c5():
+    """u.(H v) == v.(H u) on the full 8 x 4096 ReLU network (a property that holds at
+    any size), both products from the GPU's forward-over-reverse pass."""
+    cfg = W.C5
+    inp = W.make_inputs(cfg, T=1)
+    n = W.n_theta(cfg)
+    P = M().Problem(desc_of(cfg))
+    c = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    th, eta = c(inp["theta0"]), c(inp["eta"])
+    x, y = c(inp["train_x"][0]), c(inp["train_y"][0])
+    u = c(W.random_direction(n, 31))
+    v = c(W.random_direction(n, 32))
+    hu = torch.empty(n, device="cuda")
+    hv = torch.empty(n, device="cuda")
+    ws = P.workspace(P.mfmg_query_sizes(1).step_workspace_bytes)
+    print("\n[hvp symmetry] c5 full size", flush=True)
+    P.mfmg_hvp_fwd_over_rev(th, eta, x, y, 0, v, None, hv, None, ws=ws)
+    P.mfmg_hvp_fwd_over_rev(th, eta, x, y, 0, u, None, hu, None, ws=ws)
+    torch.cuda.synchronize()
+    uhv = float(torch.dot(u.double(), hv.double()))
+    vhu = float(torch.dot(v.double(), hu.double()))
+    scale = float(u.double().norm() * hv.double().norm())
+    print(f"  u.Hv {uhv:.6e}  v.Hu {vhu:.6e}", flush=True)
+    assert abs(uhv - vhu) <= 2e-2 * max(abs(uhv), 1e-3 * scale)
+
+
+def test_meta_grad_deterministic_and_workspace_reuse():
+    cfg = W.SMALL["c5_small"]
+    inp = W.make_inputs(cfg)
+    other = W.SMALL["c2_small"]
+    inp2 = W.make_inputs(other)
+    a, Va, _ = run_meta(cfg, inp)
+    run_meta(other, inp2)
+    b, Vb, _ = run_meta(cfg, inp)
+    assert np.array_equal(a, b) and Va == Vb
