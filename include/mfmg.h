@@ -26,10 +26,14 @@
  *    asynchronously on it; outputs are valid once the stream has reached the
  *    end of the call.
  *  - All arguments are validated on the host before anything is enqueued.  On
- *    any status other than MFMG_OK nothing has been enqueued and no output has
- *    been written; mfmg_last_error_message() describes the failure.  Errors of
- *    the device execution itself surface at the caller's next synchronisation.
+ *    MFMG_ERR_INVALID_ARGUMENT, MFMG_ERR_UNSUPPORTED and MFMG_ERR_WORKSPACE
+ *    nothing has been enqueued and no output has been written;
+ *    mfmg_last_error_message() describes the failure.  MFMG_ERR_HIP means a
+ *    launch failed part-way: outputs are undefined.  Errors of the device
+ *    execution itself surface at the caller's next synchronisation.
  *  - Inputs are never modified; outputs are fully overwritten.
+ *  - Arrays in the theta, opt_state or eta layout (and v, grad_out, hvp_out,
+ *    d_eta_out) must be 16-byte aligned; batch arrays 4-byte aligned.
  *  - Calls on the same workspace must not overlap in time; distinct
  *    workspaces may be used concurrently on distinct streams.
  *

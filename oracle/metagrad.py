@@ -88,10 +88,43 @@ def unroll(cfg: Config, inputs: dict, bf16: bool = False):
             th1, op1 = upsilon(cfg, g, th.detach(), opts[-1], I.eta, i)
         thetas.append(th1)
         opts.append(op1)
-        losses.append(float(L))
+        losses.append(float(L.detach()))
     with torch.no_grad():
         V = float(outer_loss(cfg, thetas[-1], I.vx, I.vy, bf16))
     return thetas, opts, losses, V
+
+
+def reverse_step(cfg: Config, I: "_Inputs", i: int, theta_i, opt_i, thbar, obar, bf16: bool):
+    """One step of the reverse sweep: rebuild inner step i from (theta_i, opt_i)
+    and back-propagate <thbar, theta_{i+1}> + <obar, opt_{i+1}> into
+    (theta_i, opt_i, eta).  Returns (bar theta_i, bar opt_i, d eta contribution)."""
+    th = theta_i.clone().requires_grad_(True)
+    op = None if opt_i is None else opt_i.clone().requires_grad_(True)
+    et = I.eta.clone().requires_grad_(True)
+    alpha = alpha_of(cfg, et, i, I.xs[i], I.emb0)
+    L = inner_loss(cfg, th, alpha, I.xs[i], I.ys[i], bf16)
+    (g,) = torch.autograd.grad(L, th, create_graph=True)
+    th1, op1 = upsilon(cfg, g, th, op, et, i)
+    s = (thbar * th1).sum()
+    wrt = [th, et]
+    if op is not None:
+        s = s + (obar * op1).sum()
+        wrt.append(op)
+    grads = torch.autograd.grad(s, wrt, allow_unused=True)
+    new_thbar = grads[0] if grads[0] is not None else torch.zeros_like(th)
+    d_eta = grads[1] if grads[1] is not None else torch.zeros_like(et)
+    new_obar = None
+    if op is not None:
+        new_obar = grads[2] if grads[2] is not None else torch.zeros_like(op)
+    return new_thbar, new_obar, d_eta
+
+
+def seed(cfg: Config, I: "_Inputs", theta_T, bf16: bool):
+    """(V, dV/dtheta_T) at the end of the unroll."""
+    thT = theta_T.clone().requires_grad_(True)
+    V = outer_loss(cfg, thT, I.vx, I.vy, bf16)
+    (thbar,) = torch.autograd.grad(V, thT)
+    return V, thbar
 
 
 def meta_grad_checkpointed(cfg: Config, inputs: dict, bf16: bool = False
@@ -99,31 +132,13 @@ def meta_grad_checkpointed(cfg: Config, inputs: dict, bf16: bool = False
     """Same quantity as ``meta_grad``, one inner step's graph at a time."""
     I = _Inputs(cfg, inputs)
     thetas, opts, _, _ = unroll(cfg, inputs, bf16)
-    thT = thetas[-1].clone().requires_grad_(True)
-    V = outer_loss(cfg, thT, I.vx, I.vy, bf16)
-    (thbar,) = torch.autograd.grad(V, thT)
+    V, thbar = seed(cfg, I, thetas[-1], bf16)
     obar = None if opts[-1] is None else torch.zeros_like(opts[-1])
     etabar = torch.zeros_like(I.eta)
     for i in reversed(range(I.T)):
-        th = thetas[i].clone().requires_grad_(True)
-        op = None if opts[i] is None else opts[i].clone().requires_grad_(True)
-        et = I.eta.clone().requires_grad_(True)
-        alpha = alpha_of(cfg, et, i, I.xs[i], I.emb0)
-        L = inner_loss(cfg, th, alpha, I.xs[i], I.ys[i], bf16)
-        (g,) = torch.autograd.grad(L, th, create_graph=True)
-        th1, op1 = upsilon(cfg, g, th, op, et, i)
-        s = (thbar * th1).sum()
-        wrt = [th, et]
-        if op is not None:
-            s = s + (obar * op1).sum()
-            wrt.append(op)
-        grads = torch.autograd.grad(s, wrt, allow_unused=True)
-        thbar = grads[0] if grads[0] is not None else torch.zeros_like(th)
-        if grads[1] is not None:
-            etabar = etabar + grads[1]
-        if op is not None:
-            obar = grads[2] if grads[2] is not None else torch.zeros_like(op)
-    return etabar.numpy(), float(V)
+        thbar, obar, d = reverse_step(cfg, I, i, thetas[i], opts[i], thbar, obar, bf16)
+        etabar = etabar + d
+    return etabar.numpy(), float(V.detach())
 
 
 # ---------------------------------------------------------------------------------------

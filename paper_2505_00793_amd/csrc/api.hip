@@ -19,6 +19,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <new>
 #include <string>
@@ -687,6 +688,13 @@ mfmg_status check_batch(const mfmg_problem* p, const mfmg_batch* b, int rows, co
   return MFMG_OK;
 }
 
+mfmg_status check_align16(std::initializer_list<const void*> ptrs) {
+  for (const void* q : ptrs)
+    if (q && !aligned(q, 16))
+      return fail(MFMG_ERR_INVALID_ARGUMENT, "parameter-shaped arrays must be 16-byte aligned");
+  return MFMG_OK;
+}
+
 mfmg_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (ws_bytes < need)
     return fail(MFMG_ERR_WORKSPACE, "workspace of %zu bytes, %zu required", ws_bytes, need);
@@ -876,6 +884,7 @@ mfmg_status mfmg_inner_step(mfmg_problem_t p, const float* theta, const float* o
     return fail(MFMG_ERR_INVALID_ARGUMENT, "batch rows %lld, expected %d", (long long)batch->rows,
                 p->d.rows);
   TRY(check_batch(p, batch, p->d.rows, "batch", 0));
+  TRY(check_align16({theta, opt_state, eta, theta_next, opt_state_next, grad_out}));
   TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->bf16())
@@ -894,6 +903,7 @@ mfmg_status mfmg_hvp_fwd_over_rev(mfmg_problem_t p, const float* theta, const fl
     return fail(MFMG_ERR_INVALID_ARGUMENT, "null theta, eta, v or hvp_out");
   if (step_index < 0) return fail(MFMG_ERR_INVALID_ARGUMENT, "negative step_index");
   TRY(check_batch(p, batch, p->d.rows, "batch", 0));
+  TRY(check_align16({theta, eta, v, grad_out, hvp_out}));
   TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->bf16())
@@ -914,6 +924,7 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
   if (!train_batches) return fail(MFMG_ERR_INVALID_ARGUMENT, "null train_batches");
   for (int t = 0; t < T; ++t) TRY(check_batch(p, &train_batches[t], p->d.rows, "train_batches", t));
   TRY(check_batch(p, val_batch, p->d.val_rows, "val_batch", 0));
+  TRY(check_align16({theta0, opt_state0, eta, d_eta_out}));
   size_t st = 0, dy = 0;
   const size_t need = meta_ws_bytes(p, T, &st, &dy);
   TRY(check_ws(ws, ws_bytes, need));

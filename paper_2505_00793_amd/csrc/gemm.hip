@@ -59,16 +59,135 @@ __device__ __forceinline__ uint4 load_chunk(const T* __restrict__ src, int gr, i
   return u.v;
 }
 
+// ------------------------------------------------------------------------------------
+// Epilogues.  row(m, n, cnt, c1, c2, t1, t2): cnt (1..4) consecutive columns
+// n.. of row m; writes the row-major outputs and returns in t1/t2 the values
+// of the outputs also stored transposed.  trans(k, n, m, cnt, v): stores cnt
+// consecutive rows m.. of column n into transposed output k.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void store_row4(T* p, long off, int cnt, const float* v) {
+  if (cnt == 4 && (off & 3) == 0) {
+    store4(p + off, v[0], v[1], v[2], v[3]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (k < cnt) p[off + k] = Elem<T>::from_float(v[k]);
+  }
+}
+
+template <typename T>
+struct ActFwdOp {
+  EpiActFwd<T> e;
+  int M, N;
+  __device__ int n_trans() const { return e.last ? 0 : (e.dual ? 2 : 1); }
+  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
+                                      float* t1, float* t2) const {
+    const bool vec = cnt == 4 && (e.N & 3) == 0;
+    float b[4] = {0.f, 0.f, 0.f, 0.f}, bd[4] = {0.f, 0.f, 0.f, 0.f};
+    if (e.bias) ld4(e.bias, n, cnt, cnt == 4, b);
+    if (e.dual && e.bias_d) ld4(e.bias_d, n, cnt, cnt == 4, bd);
+    float z[4], zd[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      z[k] = c1[k] + b[k];
+      zd[k] = c2[k] + bd[k];
+    }
+    st4(e.Z, (long)m * e.N + n, cnt, vec, z);
+    if (e.dual) st4(e.Zd, (long)m * e.N + n, cnt, vec, zd);
+    if (e.last) return;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      t1[k] = act_f(e.act, z[k]);
+      if (e.dual) {
+        float d1, d2;
+        act_d12(e.act, z[k], d1, d2);
+        t2[k] = d1 * zd[k];
+      }
+    }
+    store_row4(e.Ao, (long)m * e.ldA + n, cnt, t1);
+    if (e.dual) store_row4(e.Ado, (long)m * e.ldA + n, cnt, t2);
+  }
+  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+    store_row4(k == 0 ? e.AoT : e.AdoT, (long)n * e.ldAT + m, cnt, v);
+  }
+};
+
+template <typename T>
+struct ActBwdOp {
+  EpiActBwd<T> e;
+  int M, N;
+  __device__ int n_trans() const { return e.dual ? 2 : 1; }
+  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
+                                      float* t1, float* t2) const {
+    const bool vec = cnt == 4 && (e.N & 3) == 0;
+    float z[4], zd[4] = {0.f, 0.f, 0.f, 0.f};
+    ld4(e.Zp, (long)m * e.N + n, cnt, vec, z);
+    if (e.dual) ld4(e.Zdp, (long)m * e.N + n, cnt, vec, zd);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float d1, d2;
+      act_d12(e.act, z[k], d1, d2);
+      t1[k] = c1[k] * d1;
+      t2[k] = e.dual ? c2[k] * d1 + c1[k] * d2 * zd[k] : 0.0f;
+    }
+    store_row4(e.dZ, (long)m * e.ld + n, cnt, t1);
+    if (e.dual) store_row4(e.dZd, (long)m * e.ld + n, cnt, t2);
+  }
+  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+    store_row4(k == 0 ? e.dZT : e.dZdT, (long)n * e.ldT + m, cnt, v);
+  }
+};
+
+template <typename T>
+struct ParamOp {
+  ParamArgs<T> P;
+  int M, N;
+  __device__ int n_trans() const { return P.outWT ? 1 : 0; }
+  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
+                                      float* t1, float* t2) const {
+    param_apply(P, P.w_off + (long)m * P.nout + n, cnt, c1, c2, t1);
+    if (P.outW) store_row4(P.outW, (long)m * P.ldW + n, cnt, t1);
+  }
+  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+    store_row4(P.outWT, (long)n * P.ldWT + m, cnt, v);
+  }
+};
+
+// Staged epilogue geometry: the accumulator tile goes to LDS one wave-row
+// (BM/2 rows) at a time, then all 256 threads walk it in row-major order with
+// 16-byte global accesses, and (for outputs that are also needed in the
+// transposed layout) a second walk writes contiguous runs of the transpose.
+template <int BN>
+struct Stage {
+  static constexpr int SLD = BN + 4;  // padded LDS row stride, floats
+};
+
+template <typename T, int FLAGS, int BM, int BN>
+struct Smem {
+  static constexpr int VE = Elem<T>::VE;
+  static constexpr int LDL = BK + VE;
+  static constexpr int NAS = (FLAGS & G_AD) ? 2 : 1;
+  static constexpr int NBS = (FLAGS & G_BD) ? 2 : 1;
+  static constexpr int STAGE = (NAS * BM + NBS * BN) * LDL;  // elements
+  static constexpr int NS = (FLAGS & (G_AD | G_BD)) ? 2 : 1;  // staged accumulators
+  static constexpr int PIPE_BYTES = 2 * STAGE * (int)sizeof(T);
+  static constexpr int EPI_BYTES = NS * (BM / 2) * Stage<BN>::SLD * 4;
+  static constexpr int BYTES = PIPE_BYTES > EPI_BYTES ? PIPE_BYTES : EPI_BYTES;
+};
+
 template <typename T, int FLAGS, int BM, int BN, class Epi>
 __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
+  typedef Smem<T, FLAGS, BM, BN> SM;
   constexpr int VE = Elem<T>::VE;
-  constexpr int LDL = BK + VE;  // padded LDS row, in elements
+  constexpr int LDL = SM::LDL;
   constexpr bool HC1 = (FLAGS & G_C1) != 0;
   constexpr bool HAD = (FLAGS & G_AD) != 0;
   constexpr bool HBD = (FLAGS & G_BD) != 0;
-  constexpr int NAS = HAD ? 2 : 1;
-  constexpr int NBS = HBD ? 2 : 1;
-  constexpr int STAGE = (NAS * BM + NBS * BN) * LDL;
+  constexpr bool HC2 = HAD || HBD;
+  constexpr int NAS = SM::NAS;
+  constexpr int NBS = SM::NBS;
+  constexpr int STAGE = SM::STAGE;
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int TM = WTM / 16, TN = WTN / 16;
   constexpr int CPR = BK / VE;           // 16-byte chunks per tile row
@@ -78,7 +197,8 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   static_assert(ACH >= 1 && BCH >= 1 && (BM * CPR) % 256 == 0 && (BN * CPR) % 256 == 0, "tile");
   typedef typename Frag<T>::type frag_t;
 
-  __shared__ __attribute__((aligned(16))) T smem[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) char smem_raw[SM::BYTES];
+  T* smem = reinterpret_cast<T*>(smem_raw);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -192,128 +312,79 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
     __syncthreads();
   }
 
+  // ---- staged epilogue ----
   // C layout of a 16x16 MFMA tile: lane holds rows 4*(lane/16) + 0..3 of
   // column lane%16.
+  constexpr int SLD = Stage<BN>::SLD;
+  constexpr int RP = WTM;               // rows per pass
+  float* S1 = reinterpret_cast<float*>(smem_raw);
+  float* S2 = S1 + RP * SLD;
+  const int nT = epi.n_trans();
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int pass = 0; pass < 2; ++pass) {
+    if (wm == pass) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int mr = m0 + wm * WTM + i * 16 + (lane >> 4) * 4;
-      const int nc = n0 + wn * WTN + j * 16 + (lane & 15);
-      epi(mr, nc, acc1[i][j], acc2[i][j]);
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int c = wn * WTN + j * 16 + (lane & 15);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int rl = i * 16 + (lane >> 4) * 4 + r;
+            S1[rl * SLD + c] = HC1 ? acc1[i][j][r] : 0.0f;
+            if constexpr (HC2) S2[rl * SLD + c] = acc2[i][j][r];
+          }
+        }
     }
-}
-
-// ------------------------------------------------------------------------------------
-// Epilogues
-// ------------------------------------------------------------------------------------
-template <typename T>
-struct ActFwdOp {
-  EpiActFwd<T> e;
-  __device__ __forceinline__ void operator()(int m0, int n, const f32x4& c1, const f32x4& c2) const {
-    if (n >= e.N) return;
-    const float b = e.bias ? e.bias[n] : 0.0f;
-    const float bd = (e.dual && e.bias_d) ? e.bias_d[n] : 0.0f;
-    float a[4], ad[4];
+    __syncthreads();
+    {
+      constexpr int TPR = BN / 4;        // threads per row, 4 columns each
+      constexpr int RPI = 256 / TPR;     // rows per iteration
+      const int c = (tid % TPR) * 4;
+      const int n = n0 + c;
+      for (int rr = tid / TPR; rr < RP; rr += RPI) {
+        const int m = m0 + pass * RP + rr;
+        if (m < epi.M && n < epi.N) {
+          float c1[4], c2[4], t1[4], t2[4];
+          const float4 x1 = *reinterpret_cast<const float4*>(S1 + rr * SLD + c);
+          c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
+          if constexpr (HC2) {
+            const float4 x2 = *reinterpret_cast<const float4*>(S2 + rr * SLD + c);
+            c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
+          } else {
+            c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
+          }
+          epi.row(m, n, min(4, epi.N - n), c1, c2, t1, t2);
+          if (nT > 0) *reinterpret_cast<float4*>(S1 + rr * SLD + c) = make_float4(t1[0], t1[1], t1[2], t1[3]);
+          if (nT > 1) *reinterpret_cast<float4*>(S2 + rr * SLD + c) = make_float4(t2[0], t2[1], t2[2], t2[3]);
+        }
+      }
+    }
+    if (nT > 0) {
+      __syncthreads();
+      constexpr int TPC = RP / 4;        // threads per transposed row, 4 rows of C each
+      constexpr int CPI = 256 / TPC;
+      const int r4 = (tid % TPC) * 4;
+      const int m = m0 + pass * RP + r4;
+      for (int cc = tid / TPC; cc < BN; cc += CPI) {
+        const int n = n0 + cc;
+        if (n < epi.N && m < epi.M) {
+          const int cnt = min(4, epi.M - m);
+          float v[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + r;
-      const float z = c1[r] + b;
-      const float zd = c2[r] + bd;
-      a[r] = 0.0f;
-      ad[r] = 0.0f;
-      if (m < e.M) {
-        e.Z[(long)m * e.N + n] = z;
-        if (e.dual) e.Zd[(long)m * e.N + n] = zd;
-        if (!e.last) {
-          a[r] = act_f(e.act, z);
-          e.Ao[(long)m * e.ldA + n] = Elem<T>::from_float(a[r]);
-          if (e.dual) {
-            float d1, d2;
-            act_d12(e.act, z, d1, d2);
-            ad[r] = d1 * zd;
-            e.Ado[(long)m * e.ldA + n] = Elem<T>::from_float(ad[r]);
+          for (int k = 0; k < 4; ++k) v[k] = S1[(r4 + k) * SLD + cc];
+          epi.trans(0, n, m, cnt, v);
+          if (nT > 1) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = S2[(r4 + k) * SLD + cc];
+            epi.trans(1, n, m, cnt, v);
           }
         }
       }
     }
-    if (e.last) return;
-    if (m0 + 3 < e.M) {
-      store4(e.AoT + (long)n * e.ldAT + m0, a[0], a[1], a[2], a[3]);
-      if (e.dual) store4(e.AdoT + (long)n * e.ldAT + m0, ad[0], ad[1], ad[2], ad[3]);
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (m0 + r < e.M) {
-          e.AoT[(long)n * e.ldAT + m0 + r] = Elem<T>::from_float(a[r]);
-          if (e.dual) e.AdoT[(long)n * e.ldAT + m0 + r] = Elem<T>::from_float(ad[r]);
-        }
-    }
+    __syncthreads();
   }
-};
-
-template <typename T>
-struct ActBwdOp {
-  EpiActBwd<T> e;
-  __device__ __forceinline__ void operator()(int m0, int n, const f32x4& c1, const f32x4& c2) const {
-    if (n >= e.N) return;
-    float dz[4], dzd[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + r;
-      dz[r] = 0.0f;
-      dzd[r] = 0.0f;
-      if (m < e.M) {
-        float d1, d2;
-        act_d12(e.act, e.Zp[(long)m * e.N + n], d1, d2);
-        dz[r] = c1[r] * d1;
-        e.dZ[(long)m * e.ld + n] = Elem<T>::from_float(dz[r]);
-        if (e.dual) {
-          dzd[r] = c2[r] * d1 + c1[r] * d2 * e.Zdp[(long)m * e.N + n];
-          e.dZd[(long)m * e.ld + n] = Elem<T>::from_float(dzd[r]);
-        }
-      }
-    }
-    if (m0 + 3 < e.M) {
-      store4(e.dZT + (long)n * e.ldT + m0, dz[0], dz[1], dz[2], dz[3]);
-      if (e.dual) store4(e.dZdT + (long)n * e.ldT + m0, dzd[0], dzd[1], dzd[2], dzd[3]);
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (m0 + r < e.M) {
-          e.dZT[(long)n * e.ldT + m0 + r] = Elem<T>::from_float(dz[r]);
-          if (e.dual) e.dZdT[(long)n * e.ldT + m0 + r] = Elem<T>::from_float(dzd[r]);
-        }
-    }
-  }
-};
-
-template <typename T>
-struct ParamOp {
-  ParamArgs<T> P;
-  __device__ __forceinline__ void operator()(int m0, int n, const f32x4& c1, const f32x4& c2) const {
-    if (n >= P.nout) return;
-    float cv[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + r;
-      cv[r] = 0.0f;
-      if (m < P.nin) {
-        const long idx = P.w_off + (long)m * P.nout + n;
-        cv[r] = param_elem(P, idx, c1[r], c2[r]);
-        if (P.outW) P.outW[(long)m * P.ldW + n] = Elem<T>::from_float(cv[r]);
-      }
-    }
-    if (!P.outWT) return;
-    if (m0 + 3 < P.nin) {
-      store4(P.outWT + (long)n * P.ldWT + m0, cv[0], cv[1], cv[2], cv[3]);
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (m0 + r < P.nin) P.outWT[(long)n * P.ldWT + m0 + r] = Elem<T>::from_float(cv[r]);
-    }
-  }
-};
+}
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
@@ -351,17 +422,17 @@ hipError_t dispatch(const GemmOperands<T>& op, int flags, const Epi& epi, hipStr
 template <typename T>
 hipError_t gemm_act_fwd(const GemmOperands<T>& op, int flags, const EpiActFwd<T>& epi,
                         hipStream_t s) {
-  return dispatch(op, flags, ActFwdOp<T>{epi}, s);
+  return dispatch(op, flags, ActFwdOp<T>{epi, epi.M, epi.N}, s);
 }
 template <typename T>
 hipError_t gemm_act_bwd(const GemmOperands<T>& op, int flags, const EpiActBwd<T>& epi,
                         hipStream_t s) {
-  return dispatch(op, flags, ActBwdOp<T>{epi}, s);
+  return dispatch(op, flags, ActBwdOp<T>{epi, epi.M, epi.N}, s);
 }
 template <typename T>
 hipError_t gemm_param(const GemmOperands<T>& op, int flags, const ParamArgs<T>& P,
                       hipStream_t s) {
-  return dispatch(op, flags, ParamOp<T>{P}, s);
+  return dispatch(op, flags, ParamOp<T>{P, P.nin, P.nout}, s);
 }
 
 template hipError_t gemm_act_fwd<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiActFwd<bf16_t>&, hipStream_t);
