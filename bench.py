@@ -32,7 +32,8 @@ PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0
 
 KERNEL_CLASSES = ["fwd_gemm", "bwd_data_gemm", "bwd_weight_gemm_update", "dual_fwd_gemm",
-                  "dual_bwd_data_gemm", "dual_bwd_weight_gemm_reverse", "loss_head", "elementwise"]
+                  "dual_bwd_data_gemm", "dual_bwd_weight_gemm_reverse_first_layer", "loss_head",
+                  "elementwise", "dual_bwd_weight_gemm_reverse"]
 
 
 def log(msg):
@@ -53,7 +54,12 @@ def algorithmic_flops(cfg: W.Config, T: int):
             f[1] += (T * R + Rv) * u                     # backward-data
             f[4] += T * R * u * 3                        # dual backward-data
         f[3] += T * R * u * (3 if l > 0 else 2)          # dual forward
-        f[5] += T * R * u * ((2 if l > 0 else 1) if adam else (3 if l > 0 else 2))
+        if adam:                                         # tangent products only
+            f[5] += T * R * u * (2 if l > 0 else 1)
+        elif l > 0:                                      # G and G' = H v, three products
+            f[8] += T * R * u * 3
+        else:                                            # layer 0: A' = 0, two products
+            f[5] += T * R * u * 2
     return f
 
 
@@ -165,9 +171,12 @@ def main():
     log(f"[bench] {ms:.2f} ms per meta-gradient (wall {wall / args.steps * 1e3:.2f} ms)")
     dom = max((k for k in kern if kern[k]["tflops"]), key=lambda k: kern[k]["ms_per_step"])
     achieved = kern[dom]["tflops"]
+    c = KERNEL_CLASSES.index(dom)
+    per_launch = flops[c] / kern[dom]["launches_per_step"]
     roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None}
+            "traffic": None, "gflop_per_launch": round(per_launch / 1e9, 3),
+            "us_per_launch": round(kern[dom]["ms_per_step"] / kern[dom]["launches_per_step"] * 1e3, 2)}
     finite = bool(torch.isfinite(d_eta).all().item())
 
     sweep = {}

@@ -207,8 +207,11 @@ const char* mfmg_last_error_message(void);
  * launches and their summed duration, then clears that class.  Classes:
  *   0 forward GEMM, 1 backward-data GEMM, 2 backward-weight GEMM (with update),
  *   3 dual forward GEMM, 4 dual backward-data GEMM, 5 dual backward-weight GEMM
- *   (with reverse accumulation), 6 loss head, 7 other elementwise kernels. */
-#define MFMG_NUM_KERNEL_CLASSES 8
+ *   (with reverse accumulation) computing fewer than three products (first
+ *   layer, or no primal gradient), 6 loss head, 7 other elementwise kernels,
+ *   8 dual backward-weight GEMM computing all three products G = A^T dZ and
+ *   G' = A'^T dZ + A^T dZ' (hidden layers).  Timing covers MLP problems. */
+#define MFMG_NUM_KERNEL_CLASSES 9
 mfmg_status mfmg_timing_enable(int enable);
 mfmg_status mfmg_timing_read(int kernel_class, int* launches, double* total_ms);
 

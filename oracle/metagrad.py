@@ -26,13 +26,29 @@ from .models import alpha_of, inner_loss, outer_loss, unpack
 from .optim import upsilon
 
 F64 = torch.float64
+_FLOAT = [F64]  # working precision of the oracle: float64 (float32 only to measure spreads)
 
 
-def _t(a, dtype=F64):
+class working_precision:
+    """Context manager that runs the same oracle code in another float dtype.
+    The oracle is float64; float32 runs measure how far float32 arithmetic
+    alone moves a result (the noise floor a float32 GPU result is held to)."""
+
+    def __init__(self, dtype):
+        self.dtype = dtype
+
+    def __enter__(self):
+        _FLOAT.append(self.dtype)
+
+    def __exit__(self, *exc):
+        _FLOAT.pop()
+
+
+def _t(a, dtype=None):
     if a is None:
         return None
     t = torch.from_numpy(np.ascontiguousarray(a))
-    return t.to(dtype) if t.dtype.is_floating_point else t.long()
+    return t.to(dtype or _FLOAT[-1]) if t.dtype.is_floating_point else t.long()
 
 
 class _Inputs:
@@ -138,7 +154,7 @@ def meta_grad_checkpointed(cfg: Config, inputs: dict, bf16: bool = False
     for i in reversed(range(I.T)):
         thbar, obar, d = reverse_step(cfg, I, i, thetas[i], opts[i], thbar, obar, bf16)
         etabar = etabar + d
-    return etabar.numpy(), float(V.detach())
+    return etabar.double().numpy(), float(V.detach())
 
 
 # ---------------------------------------------------------------------------------------

@@ -55,6 +55,24 @@ class _RoundedMM(torch.autograd.Function):
         return ga, gb
 
 
+class _RoundedMM32(torch.autograd.Function):
+    """As _RoundedMM, but the product of the rounded operands is accumulated in
+    float32 (a second, equally valid bf16-operand implementation; the spread
+    between the two measures how far rounding alone moves a result)."""
+
+    @staticmethod
+    def forward(ctx, a, b):
+        ctx.save_for_backward(a, b)
+        return (bf16_round(a).float() @ bf16_round(b).float()).to(F64)
+
+    @staticmethod
+    def backward(ctx, g):
+        a, b = ctx.saved_tensors
+        ga = _RoundedMM32.apply(g, b.transpose(-2, -1)) if ctx.needs_input_grad[0] else None
+        gb = _RoundedMM32.apply(a.transpose(-2, -1), g) if ctx.needs_input_grad[1] else None
+        return ga, gb
+
+
 class _RoundedBMM(torch.autograd.Function):
     """Batched version: leading dims equal on both sides."""
 
@@ -71,8 +89,32 @@ class _RoundedBMM(torch.autograd.Function):
         return ga, gb
 
 
-def mm(a: torch.Tensor, b: torch.Tensor, bf16: bool) -> torch.Tensor:
-    """2-D matrix product, with bf16 operands when ``bf16``."""
+class _MM32(torch.autograd.Function):
+    """Float32 product of the (unrounded) operands; its VJP uses the same op.  A
+    float32-GEMM implementation of the same method, for measuring how far
+    float32 accumulation alone moves a result."""
+
+    @staticmethod
+    def forward(ctx, a, b):
+        ctx.save_for_backward(a, b)
+        return (a.float() @ b.float()).to(F64)
+
+    @staticmethod
+    def backward(ctx, g):
+        a, b = ctx.saved_tensors
+        ga = _MM32.apply(g, b.transpose(-2, -1)) if ctx.needs_input_grad[0] else None
+        gb = _MM32.apply(a.transpose(-2, -1), g) if ctx.needs_input_grad[1] else None
+        return ga, gb
+
+
+def mm(a: torch.Tensor, b: torch.Tensor, bf16) -> torch.Tensor:
+    """2-D matrix product.  ``bf16``: False = float64; True = bf16 operands;
+    "acc32" = bf16 operands with float32 accumulation; "fp32" = float32
+    operands and accumulation."""
+    if bf16 == "acc32":
+        return _RoundedMM32.apply(a, b)
+    if bf16 == "fp32":
+        return _MM32.apply(a, b)
     return _RoundedMM.apply(a, b) if bf16 else a @ b
 
 
@@ -94,8 +136,8 @@ class _BiasAdd(torch.autograd.Function):
         return g, _RoundST.apply(g).sum(0)
 
 
-def bias_add(z: torch.Tensor, b: torch.Tensor, bf16: bool) -> torch.Tensor:
-    return _BiasAdd.apply(z, b) if bf16 else z + b
+def bias_add(z: torch.Tensor, b: torch.Tensor, bf16) -> torch.Tensor:
+    return _BiasAdd.apply(z, b) if (bf16 and bf16 != "fp32") else z + b
 
 
 def gelu(z: torch.Tensor) -> torch.Tensor:

@@ -27,6 +27,7 @@
 
 #include "kernels.h"
 #include "mfmg.h"
+#include "tf_engine.h"
 
 using namespace mfmg;
 
@@ -69,6 +70,7 @@ struct Carver {
 
 struct mfmg_problem {
   mfmg_problem_desc d;
+  bool tf;  // transformer kind (tf_engine)
   int L;
   int w[MFMG_MAX_LAYERS + 1];
   long w_off[MFMG_MAX_LAYERS];
@@ -394,7 +396,7 @@ struct Eng {
         op.N = nout;
         op.K = R;
         const int flags = (need_c1 ? G_C1 : 0) | (dual ? (G_BD | (l > 0 ? G_AD : 0)) : 0);
-        TimingScope ts(dual ? 5 : 2, s);
+        TimingScope ts(dual ? (flags == (G_C1 | G_AD | G_BD) ? 8 : 5) : 2, s);
         HIPCHK(gemm_param<T>(op, flags, P, s));
       }
       if (p->d.has_bias) {
@@ -666,6 +668,7 @@ mfmg_status run_hvp(const mfmg_problem* p, const float* theta, const float* eta,
 // Validation helpers
 // ------------------------------------------------------------------------------------
 long n_eta_of(const mfmg_problem* p, int T) {
+  if (p->tf) return tf_n_eta(p->d);
   switch (p->d.meta) {
     case MFMG_META_LOGLR_PER_PARAM: return p->n_theta;
     case MFMG_META_LOGLR_PER_LAYER_WD: return p->L + 1;
@@ -679,11 +682,12 @@ bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(pt
 mfmg_status check_batch(const mfmg_problem* p, const mfmg_batch* b, int rows, const char* what,
                         int idx) {
   if (!b) return fail(MFMG_ERR_INVALID_ARGUMENT, "%s[%d]: null batch", what, idx);
-  if (!b->x || !b->y) return fail(MFMG_ERR_INVALID_ARGUMENT, "%s[%d]: null x or y", what, idx);
+  if (!b->x || (!b->y && !p->tf))
+    return fail(MFMG_ERR_INVALID_ARGUMENT, "%s[%d]: null x or y", what, idx);
   if (b->rows != rows)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "%s[%d]: rows %lld, expected %d", what, idx,
                 (long long)b->rows, rows);
-  if (!aligned(b->x, 4) || !aligned(b->y, 4))
+  if (!aligned(b->x, 4) || (b->y && !aligned(b->y, 4)))
     return fail(MFMG_ERR_INVALID_ARGUMENT, "%s[%d]: x/y not 4-byte aligned", what, idx);
   return MFMG_OK;
 }
@@ -776,8 +780,18 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
   if (!desc || !out) return fail(MFMG_ERR_INVALID_ARGUMENT, "null desc or out");
   *out = nullptr;
   const mfmg_problem_desc& d = *desc;
-  if (d.kind == MFMG_KIND_TRANSFORMER)
-    return fail(MFMG_ERR_UNSUPPORTED, "transformer problems are not implemented in this build");
+  if (d.kind == MFMG_KIND_TRANSFORMER) {
+    if (const char* msg = tf_validate(d)) return fail(MFMG_ERR_UNSUPPORTED, "%s", msg);
+    mfmg_problem* p = new (std::nothrow) mfmg_problem;
+    if (!p) return fail(MFMG_ERR_INVALID_ARGUMENT, "out of host memory");
+    std::memset(p, 0, sizeof(*p));
+    p->d = d;
+    p->tf = true;
+    p->VE = d.precision == MFMG_PREC_BF16 ? 8 : 4;
+    p->n_theta = tf_n_theta(d);
+    *out = p;
+    return MFMG_OK;
+  }
   if (d.kind != MFMG_KIND_MLP) return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown kind %d", d.kind);
   if (d.n_layers < 1 || d.n_layers > MFMG_MAX_LAYERS)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "n_layers %d outside [1, %d]", d.n_layers,
@@ -828,6 +842,7 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
   mfmg_problem* p = new (std::nothrow) mfmg_problem;
   if (!p) return fail(MFMG_ERR_INVALID_ARGUMENT, "out of host memory");
   p->d = d;
+  p->tf = false;
   p->L = d.n_layers;
   p->VE = d.precision == MFMG_PREC_BF16 ? 8 : 4;
   long off = 0;
@@ -862,6 +877,13 @@ mfmg_status mfmg_query_sizes(mfmg_problem_t p, int T, mfmg_sizes* out) {
   out->n_opt_state = p->adam() ? 2 * p->n_theta : 0;
   out->n_eta = n_eta_of(p, T);
   size_t st = 0, dy = 0;
+  if (p->tf) {
+    out->workspace_bytes = tf_meta_ws(p->d, T, &st, &dy);
+    out->static_bytes = st;
+    out->dynamic_bytes = dy;
+    out->step_workspace_bytes = tf_step_ws(p->d);
+    return MFMG_OK;
+  }
   out->workspace_bytes = meta_ws_bytes(p, T, &st, &dy);
   out->static_bytes = st;
   out->dynamic_bytes = dy;
@@ -885,8 +907,13 @@ mfmg_status mfmg_inner_step(mfmg_problem_t p, const float* theta, const float* o
                 p->d.rows);
   TRY(check_batch(p, batch, p->d.rows, "batch", 0));
   TRY(check_align16({theta, opt_state, eta, theta_next, opt_state_next, grad_out}));
-  TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (p->tf) {
+    TRY(check_ws(ws, ws_bytes, tf_step_ws(p->d)));
+    HIPCHK(tf_run_inner(p->d, theta, eta, batch, theta_next, grad_out, loss_out, (char*)ws, s));
+    return MFMG_OK;
+  }
+  TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   if (p->bf16())
     return run_inner_step<bf16_t>(p, theta, opt_state, eta, batch, step_index, theta_next,
                                   opt_state_next, grad_out, loss_out, (char*)ws, s);
@@ -904,8 +931,13 @@ mfmg_status mfmg_hvp_fwd_over_rev(mfmg_problem_t p, const float* theta, const fl
   if (step_index < 0) return fail(MFMG_ERR_INVALID_ARGUMENT, "negative step_index");
   TRY(check_batch(p, batch, p->d.rows, "batch", 0));
   TRY(check_align16({theta, eta, v, grad_out, hvp_out}));
-  TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (p->tf) {
+    TRY(check_ws(ws, ws_bytes, tf_step_ws(p->d)));
+    HIPCHK(tf_run_hvp(p->d, theta, eta, batch, v, grad_out, hvp_out, mvp_out, (char*)ws, s));
+    return MFMG_OK;
+  }
+  TRY(check_ws(ws, ws_bytes, step_ws_bytes(p)));
   if (p->bf16())
     return run_hvp<bf16_t>(p, theta, eta, batch, step_index, v, grad_out, hvp_out, mvp_out,
                            (char*)ws, s);
@@ -926,9 +958,20 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
   TRY(check_batch(p, val_batch, p->d.val_rows, "val_batch", 0));
   TRY(check_align16({theta0, opt_state0, eta, d_eta_out}));
   size_t st = 0, dy = 0;
-  const size_t need = meta_ws_bytes(p, T, &st, &dy);
+  const size_t need = p->tf ? tf_meta_ws(p->d, T, &st, &dy) : meta_ws_bytes(p, T, &st, &dy);
   TRY(check_ws(ws, ws_bytes, need));
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (p->tf) {
+    if (peak_bytes_out) {
+      const long n_eta = tf_n_eta(p->d);
+      size_t b = need + 4 * (size_t)p->n_theta + 8 * (size_t)n_eta + (val_loss_out ? 4 : 0);
+      b += (size_t)(T * p->d.rows + p->d.val_rows) * (p->d.seq + 1) * 4;
+      *peak_bytes_out = b;
+    }
+    HIPCHK(tf_run_meta(p->d, theta0, eta, train_batches, T, val_batch, d_eta_out, val_loss_out,
+                       (char*)ws, s));
+    return MFMG_OK;
+  }
   if (peak_bytes_out) {
     const long n_eta = n_eta_of(p, T);
     const size_t ybytes = 4 * (size_t)(p->d.loss == MFMG_LOSS_CE ? 1 : p->w[p->L]);

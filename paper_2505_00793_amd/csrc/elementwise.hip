@@ -17,9 +17,13 @@ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 template <typename T>
 __global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ src, int rows,
                                                       int cols, int lds, T* dst, int ldd, T* dstT,
-                                                      int lddT) {
+                                                      int lddT, long s_src, long s_dst,
+                                                      long s_dstT) {
   __shared__ float tile[64][65];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  src += blockIdx.z * s_src;
+  if (dst) dst += blockIdx.z * s_dst;
+  if (dstT) dstT += blockIdx.z * s_dstT;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tx;
@@ -402,11 +406,12 @@ hipError_t copy(const float* src, float* dst, long n, hipStream_t s) {
 
 template <typename T>
 hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
-                          T* dstT, int lddT, hipStream_t s) {
-  if (rows <= 0 || cols <= 0) return hipSuccess;
-  dim3 grid(cdiv(cols, 64), cdiv(rows, 64));
+                          T* dstT, int lddT, hipStream_t s, int batch, long s_src, long s_dst,
+                          long s_dstT) {
+  if (rows <= 0 || cols <= 0 || batch <= 0) return hipSuccess;
+  dim3 grid(cdiv(cols, 64), cdiv(rows, 64), batch);
   hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
-                     dstT, lddT);
+                     dstT, lddT, s_src, s_dst, s_dstT);
   return hipGetLastError();
 }
 
@@ -479,8 +484,8 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   return hipGetLastError();
 }
 
-template hipError_t convert_matrix<bf16_t>(const float*, int, int, int, bf16_t*, int, bf16_t*, int, hipStream_t);
-template hipError_t convert_matrix<float>(const float*, int, int, int, float*, int, float*, int, hipStream_t);
+template hipError_t convert_matrix<bf16_t>(const float*, int, int, int, bf16_t*, int, bf16_t*, int, hipStream_t, int, long, long, long);
+template hipError_t convert_matrix<float>(const float*, int, int, int, float*, int, float*, int, hipStream_t, int, long, long, long);
 template hipError_t bias_reduce<bf16_t>(const bf16_t*, const bf16_t*, int, int, const ParamArgs<bf16_t>&, hipStream_t);
 template hipError_t bias_reduce<float>(const float*, const float*, int, int, const ParamArgs<float>&, hipStream_t);
 template hipError_t loss_head<bf16_t>(const LossArgs<bf16_t>&, hipStream_t);

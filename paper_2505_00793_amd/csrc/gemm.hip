@@ -24,7 +24,6 @@ namespace mfmg {
 
 namespace {
 
-constexpr int BK = 32;
 
 __device__ __forceinline__ void mma(f32x4& acc, const bf16x8& a, const bf16x8& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
@@ -81,8 +80,8 @@ struct ActFwdOp {
   EpiActFwd<T> e;
   int M, N;
   __device__ int n_trans() const { return e.last ? 0 : (e.dual ? 2 : 1); }
-  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
-                                      float* t1, float* t2) const {
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
     const bool vec = cnt == 4 && (e.N & 3) == 0;
     float b[4] = {0.f, 0.f, 0.f, 0.f}, bd[4] = {0.f, 0.f, 0.f, 0.f};
     if (e.bias) ld4(e.bias, n, cnt, cnt == 4, b);
@@ -108,7 +107,8 @@ struct ActFwdOp {
     store_row4(e.Ao, (long)m * e.ldA + n, cnt, t1);
     if (e.dual) store_row4(e.Ado, (long)m * e.ldA + n, cnt, t2);
   }
-  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+  __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
+                                        const float* v) const {
     store_row4(k == 0 ? e.AoT : e.AdoT, (long)n * e.ldAT + m, cnt, v);
   }
 };
@@ -118,8 +118,8 @@ struct ActBwdOp {
   EpiActBwd<T> e;
   int M, N;
   __device__ int n_trans() const { return e.dual ? 2 : 1; }
-  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
-                                      float* t1, float* t2) const {
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
     const bool vec = cnt == 4 && (e.N & 3) == 0;
     float z[4], zd[4] = {0.f, 0.f, 0.f, 0.f};
     ld4(e.Zp, (long)m * e.N + n, cnt, vec, z);
@@ -134,7 +134,8 @@ struct ActBwdOp {
     store_row4(e.dZ, (long)m * e.ld + n, cnt, t1);
     if (e.dual) store_row4(e.dZd, (long)m * e.ld + n, cnt, t2);
   }
-  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+  __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
+                                        const float* v) const {
     store_row4(k == 0 ? e.dZT : e.dZdT, (long)n * e.ldT + m, cnt, v);
   }
 };
@@ -144,13 +145,112 @@ struct ParamOp {
   ParamArgs<T> P;
   int M, N;
   __device__ int n_trans() const { return P.outWT ? 1 : 0; }
-  __device__ __forceinline__ void row(int m, int n, int cnt, const float* c1, const float* c2,
-                                      float* t1, float* t2) const {
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
     param_apply(P, P.w_off + (long)m * P.nout + n, cnt, c1, c2, t1);
     if (P.outW) store_row4(P.outW, (long)m * P.ldW + n, cnt, t1);
   }
-  __device__ __forceinline__ void trans(int k, int n, int m, int cnt, const float* v) const {
+  __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
+                                        const float* v) const {
     store_row4(P.outWT, (long)n * P.ldWT + m, cnt, v);
+  }
+};
+
+struct StoreOp {
+  EpiStore e;
+  int M, N;
+  __device__ int n_trans() const { return 0; }
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
+    const long off = bz * e.sC + (long)m * e.ldc + n;
+    const bool vec = cnt == 4 && (off & 3) == 0;
+    float v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = e.scale * c1[k];
+    st4(e.C, off, cnt, vec, v);
+    if (e.dual) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = e.scale * c2[k];
+      st4(e.Cd, off, cnt, vec, v);
+    }
+  }
+  __device__ __forceinline__ void trans(int, int, int, int, int, const float*) const {}
+};
+
+struct ResidOp {
+  EpiResid e;
+  int M, N;
+  __device__ int n_trans() const { return 0; }
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
+    const long off = (long)m * e.N + n;
+    const bool vec = cnt == 4 && (e.N & 3) == 0;
+    float h[4];
+    ld4(e.H, off, cnt, vec, h);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) h[k] += c1[k];
+    st4(e.Ho, off, cnt, vec, h);
+    if (e.dual) {
+      ld4(e.Hd, off, cnt, vec, h);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) h[k] += c2[k];
+      st4(e.Hdo, off, cnt, vec, h);
+    }
+  }
+  __device__ __forceinline__ void trans(int, int, int, int, int, const float*) const {}
+};
+
+template <typename T>
+struct HeadMergeOp {
+  EpiHeadMerge<T> e;
+  int M, N;
+  __device__ int n_trans() const { return e.dual ? 2 : 1; }
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
+    const long r = (long)(bz / e.heads) * e.seq + m;
+    const int c = (bz % e.heads) * e.dh + n;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      t1[k] = c1[k];
+      t2[k] = c2[k];
+    }
+    store_row4(e.O, r * e.ldO + c, cnt, t1);
+    if (e.dual) store_row4(e.Od, r * e.ldO + c, cnt, t2);
+  }
+  __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
+                                        const float* v) const {
+    const long r = (long)(bz / e.heads) * e.seq + m;
+    const long c = (bz % e.heads) * e.dh + n;
+    store_row4(k == 0 ? e.OT : e.OdT, c * e.ldOT + r, cnt, v);
+  }
+};
+
+template <typename T>
+struct HeadSplitOp {
+  EpiHeadSplit<T> e;
+  int M, N;
+  __device__ int n_trans() const { return e.dual ? 2 : 1; }
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
+    const int b = m / e.seq, s = m % e.seq;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      t1[k] = c1[k];
+      t2[k] = c2[k];
+    }
+    // cnt columns n.. lie in one head (dh is a multiple of 4)
+    const int h = n / e.dh, j = n % e.dh;
+    const long off = ((long)(b * e.heads + h) * e.seq + s) * e.ldh + j;
+    store_row4(e.Oh, off, cnt, t1);
+    if (e.dual) store_row4(e.Odh, off, cnt, t2);
+  }
+  __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
+                                        const float* v) const {
+    // cnt rows m.. lie in one sequence (seq is a multiple of 4)
+    const int b = m / e.seq, s = m % e.seq;
+    const int h = n / e.dh, j = n % e.dh;
+    const long off = ((long)(b * e.heads + h) * e.dh + j) * e.ldhT + s;
+    store_row4(k == 0 ? e.OhT : e.OdhT, off, cnt, v);
   }
 };
 
@@ -163,7 +263,7 @@ struct Stage {
   static constexpr int SLD = BN + 4;  // padded LDS row stride, floats
 };
 
-template <typename T, int FLAGS, int BM, int BN>
+template <typename T, int FLAGS, int BM, int BN, int BK>
 struct Smem {
   static constexpr int VE = Elem<T>::VE;
   static constexpr int LDL = BK + VE;
@@ -176,9 +276,9 @@ struct Smem {
   static constexpr int BYTES = PIPE_BYTES > EPI_BYTES ? PIPE_BYTES : EPI_BYTES;
 };
 
-template <typename T, int FLAGS, int BM, int BN, class Epi>
+template <typename T, int FLAGS, int BM, int BN, int BK, class Epi>
 __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
-  typedef Smem<T, FLAGS, BM, BN> SM;
+  typedef Smem<T, FLAGS, BM, BN, BK> SM;
   constexpr int VE = Elem<T>::VE;
   constexpr int LDL = SM::LDL;
   constexpr bool HC1 = (FLAGS & G_C1) != 0;
@@ -221,6 +321,13 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   const int tm = first_m + within % gsz;
   const int tn = within / gsz;
   const int m0 = tm * BM, n0 = tn * BN;
+  const int bz = blockIdx.y;
+  if (bz > 0) {
+    op.A += bz * op.sA;
+    if (op.Ad) op.Ad += bz * op.sA;
+    op.B += bz * op.sB;
+    if (op.Bd) op.Bd += bz * op.sB;
+  }
 
   uint4 ra[NAS][ACH], rb[NBS][BCH];
 
@@ -354,7 +461,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
           } else {
             c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
           }
-          epi.row(m, n, min(4, epi.N - n), c1, c2, t1, t2);
+          epi.row(bz, m, n, min(4, epi.N - n), c1, c2, t1, t2);
           if (nT > 0) *reinterpret_cast<float4*>(S1 + rr * SLD + c) = make_float4(t1[0], t1[1], t1[2], t1[3]);
           if (nT > 1) *reinterpret_cast<float4*>(S2 + rr * SLD + c) = make_float4(t2[0], t2[1], t2[2], t2[3]);
         }
@@ -373,11 +480,11 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
           float v[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) v[k] = S1[(r4 + k) * SLD + cc];
-          epi.trans(0, n, m, cnt, v);
+          epi.trans(0, bz, n, m, cnt, v);
           if (nT > 1) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) v[k] = S2[(r4 + k) * SLD + cc];
-            epi.trans(1, n, m, cnt, v);
+            epi.trans(1, bz, n, m, cnt, v);
           }
         }
       }
@@ -388,10 +495,37 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// k depth per LDS stage: 64 keeps more MFMA work in flight per prefetch; the dual
+// backward-weight kernels (short k = batch rows, heavy epilogue) use 32 so that
+// their double-buffered tiles stay at 80 KB of LDS.
+template <int FLAGS, class Epi>
+struct KDepth {
+  static constexpr int value = 64;
+};
+template <typename T> struct ParamOp;
+template <typename T>
+struct KDepth<G_C1 | G_AD | G_BD, ParamOp<T>> {
+  static constexpr int value = 32;
+};
+template <typename T>
+struct KDepth<G_AD | G_BD, ParamOp<T>> {
+  static constexpr int value = 32;
+};
+template <typename T>
+struct KDepth<G_C1 | G_BD, ParamOp<T>> {
+  static constexpr int value = 32;
+};
+template <typename T>
+struct KDepth<G_BD, ParamOp<T>> {
+  static constexpr int value = 32;
+};
+
 template <typename T, int FLAGS, int BM, int BN, class Epi>
 hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   const int tiles = cdiv(op.M, BM) * cdiv(op.N, BN);
-  hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, Epi>), dim3(tiles), dim3(256), 0, s, op, epi);
+  constexpr int BK = KDepth<FLAGS, Epi>::value;
+  hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi>), dim3(tiles, op.batch), dim3(256), 0, s,
+                     op, epi);
   return hipGetLastError();
 }
 
@@ -400,7 +534,8 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
   if (op.M <= 0 || op.N <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2) {
     // 128 x 128 tiles once they alone fill most of the 256 compute units.
-    if (cdiv(op.M, 128) * cdiv(op.N, 128) >= 192) return launch<T, FLAGS, 128, 128>(op, epi, s);
+    if (cdiv(op.M, 128) * cdiv(op.N, 128) * op.batch >= 192)
+      return launch<T, FLAGS, 128, 128>(op, epi, s);
   }
   return launch<T, FLAGS, 64, 64>(op, epi, s);
 }
@@ -435,6 +570,33 @@ hipError_t gemm_param(const GemmOperands<T>& op, int flags, const ParamArgs<T>& 
   return dispatch(op, flags, ParamOp<T>{P, P.nin, P.nout}, s);
 }
 
+template <typename T>
+hipError_t gemm_store(const GemmOperands<T>& op, int flags, const EpiStore& e, hipStream_t s) {
+  return dispatch(op, flags, StoreOp{e, e.M, e.N}, s);
+}
+template <typename T>
+hipError_t gemm_resid(const GemmOperands<T>& op, int flags, const EpiResid& e, hipStream_t s) {
+  return dispatch(op, flags, ResidOp{e, e.M, e.N}, s);
+}
+template <typename T>
+hipError_t gemm_head_merge(const GemmOperands<T>& op, int flags, const EpiHeadMerge<T>& e,
+                           hipStream_t s) {
+  return dispatch(op, flags, HeadMergeOp<T>{e, e.M, e.N}, s);
+}
+template <typename T>
+hipError_t gemm_head_split(const GemmOperands<T>& op, int flags, const EpiHeadSplit<T>& e,
+                           hipStream_t s) {
+  return dispatch(op, flags, HeadSplitOp<T>{e, e.M, e.N}, s);
+}
+
+template hipError_t gemm_store<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiStore&, hipStream_t);
+template hipError_t gemm_store<float>(const GemmOperands<float>&, int, const EpiStore&, hipStream_t);
+template hipError_t gemm_resid<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiResid&, hipStream_t);
+template hipError_t gemm_resid<float>(const GemmOperands<float>&, int, const EpiResid&, hipStream_t);
+template hipError_t gemm_head_merge<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiHeadMerge<bf16_t>&, hipStream_t);
+template hipError_t gemm_head_merge<float>(const GemmOperands<float>&, int, const EpiHeadMerge<float>&, hipStream_t);
+template hipError_t gemm_head_split<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiHeadSplit<bf16_t>&, hipStream_t);
+template hipError_t gemm_head_split<float>(const GemmOperands<float>&, int, const EpiHeadSplit<float>&, hipStream_t);
 template hipError_t gemm_act_fwd<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiActFwd<bf16_t>&, hipStream_t);
 template hipError_t gemm_act_fwd<float>(const GemmOperands<float>&, int, const EpiActFwd<float>&, hipStream_t);
 template hipError_t gemm_act_bwd<bf16_t>(const GemmOperands<bf16_t>&, int, const EpiActBwd<bf16_t>&, hipStream_t);

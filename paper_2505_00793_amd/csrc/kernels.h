@@ -26,6 +26,8 @@ struct GemmOperands {
   const T* Bd;
   int lda, ldb;
   int M, N, K;
+  int batch = 1;      // independent products (grid.y); operand z starts at A + z * sA
+  long sA = 0, sB = 0;
 };
 
 // Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
@@ -61,6 +63,46 @@ struct EpiActBwd {
 
 // What the per-parameter epilogue does with (g, hv) = (C1, C2) of a
 // backward-weight GEMM (and of the bias reduction).
+// Plain float32 store of scale * C1 (and scale * C2): C[z * sC + m * ldc + n].
+struct EpiStore {
+  float* C;
+  float* Cd;
+  int ldc;
+  long sC;
+  float scale;
+  int M, N, dual;
+};
+
+// Residual stream update: Ho = H + C1, Hdo = Hd + C2 (float32 [M][N]).
+struct EpiResid {
+  const float* H;
+  const float* Hd;
+  float* Ho;
+  float* Hdo;
+  int M, N, dual;
+};
+
+// Attention output of head z = b * heads + h (rows = query positions s,
+// columns = head dims j) written as operands in token-major layout:
+// O[(b * seq + s) * ldO + h * dh + j] and the transpose OT[(h * dh + j) * ldOT + b * seq + s].
+template <typename T>
+struct EpiHeadMerge {
+  T* O; T* OT; T* Od; T* OdT;
+  int ldO, ldOT;
+  int seq, heads, dh;
+  int M, N, dual;
+};
+
+// The inverse: a token-major [tokens][heads * dh] result written per head,
+// Oh[((b * heads + h) * seq + s) * ldh + j] and OhT[((b * heads + h) * dh + j) * ldhT + s].
+template <typename T>
+struct EpiHeadSplit {
+  T* Oh; T* OhT; T* Odh; T* OdhT;
+  int ldh, ldhT;
+  int seq, heads, dh;
+  int M, N, dual;
+};
+
 enum ParamMode {
   P_UPD_SGD_PP = 0,     // theta' = theta - exp(eta) g
   P_UPD_SGD_FIXED = 1,  // theta' = theta - lr g
@@ -71,7 +113,8 @@ enum ParamMode {
   P_REV_SGD_PP = 6,     // eb (+)= -exp(eta) g tb; tb += hv; v = -exp(eta) tb
   P_REV_SGD_FIXED = 7,  // tb += hv; v = -lr tb
   P_REV_ADAM = 8,       // tb += hv
-  P_HVP = 9             // grad_out = g; hvp_out = hv
+  P_HVP = 9,            // grad_out = g; hvp_out = hv
+  P_STORE_G = 10        // grad_out = g
 };
 
 template <typename T>
@@ -127,12 +170,23 @@ hipError_t gemm_act_bwd(const GemmOperands<T>& op, int flags, const EpiActBwd<T>
 template <typename T>
 hipError_t gemm_param(const GemmOperands<T>& op, int flags, const ParamArgs<T>& P,
                       hipStream_t s);
+template <typename T>
+hipError_t gemm_store(const GemmOperands<T>& op, int flags, const EpiStore& e, hipStream_t s);
+template <typename T>
+hipError_t gemm_resid(const GemmOperands<T>& op, int flags, const EpiResid& e, hipStream_t s);
+template <typename T>
+hipError_t gemm_head_merge(const GemmOperands<T>& op, int flags, const EpiHeadMerge<T>& e,
+                           hipStream_t s);
+template <typename T>
+hipError_t gemm_head_split(const GemmOperands<T>& op, int flags, const EpiHeadSplit<T>& e,
+                           hipStream_t s);
 
 // float32 matrix [rows][cols] (leading dim lds) -> operand copies dst [rows][ldd]
 // and dstT [cols][lddT] (either may be null).
 template <typename T>
 hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
-                          T* dstT, int lddT, hipStream_t s);
+                          T* dstT, int lddT, hipStream_t s, int batch = 1, long s_src = 0,
+                          long s_dst = 0, long s_dstT = 0);
 
 // Column sums over rows of dZT [nout][ld] (and dZdT) -> per-parameter epilogue
 // on the bias entries of layer P.layer.

@@ -132,6 +132,12 @@ __device__ __forceinline__ void param_apply(const ParamArgs<T>& P, long idx, int
       for (int k = 0; k < 4; ++k) cv[k] = 0.0f;
       return;
     }
+    case P_STORE_G: {
+      st4(P.grad_out, idx, cnt, vec, g);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cv[k] = 0.0f;
+      return;
+    }
   }
 }
 

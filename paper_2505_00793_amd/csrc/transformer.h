@@ -1,0 +1,89 @@
+// Interfaces of the decoder-block dual kernels (transformer.hip).
+#pragma once
+
+#include "kernels.h"
+
+namespace mfmg {
+
+constexpr int LN_ROWS_PER_WAVE = 8;
+constexpr int LN_MAX_D = 1024;
+constexpr int TOKEN_SORT_MAX = 8192;
+constexpr int META_ROWS_PER_BLOCK = 128;
+constexpr int META_MAX_HIDDEN = 256;
+
+struct LnArgs {
+  const float* x;  const float* xd;          // [N][d] input (and tangent)
+  const float* g;  const float* b;           // gain, bias [d]
+  const float* gd; const float* bd;          // their tangents
+  float* y;  float* yd;                      // [N][d] output (and tangent)
+  float* xh; float* xhd;                     // normalised input (and tangent), saved
+  float* rstd; float* c;                     // [N] 1/sigma and mean(xh xd), saved
+  int N, d, dual;
+  float eps;
+};
+
+struct LnBwdArgs {
+  const float* dy; const float* dyd;         // [N][d] cotangent of y (and tangent)
+  const float* xh; const float* xhd;
+  const float* rstd; const float* c;
+  const float* g;  const float* gd;
+  const float* dh_in; const float* dhd_in;   // residual-stream gradient entering
+  float* dh_out; float* dhd_out;             // dh_in + dx (may alias dh_in)
+  float* partial;                            // [ln_bwd_parts(N)][4][d]
+  int N, d, dual;
+};
+
+struct RopeArgs {
+  const float* qkv; const float* qkvd;       // split: [N][3d] in
+  float* Q; float* K; float* V;              // per-head [B*H][S][dh]
+  float* Qd; float* Kd; float* Vd;
+  float* qkv_out; float* qkvd_out;           // merge: [N][3d] out
+  const float* cs; const float* sn;          // [S][dh/2]
+  int N, S, H, dh, dual;
+};
+
+struct SoftmaxArgs {
+  const float* Sc; const float* Scd;         // scores (scaled) [rows][S]
+  float* P; float* Pd;                       // probabilities (and tangent)
+  const float* dP; const float* dPd;         // backward: cotangent of P
+  float* dS; float* dSd;                     // backward: scale * cotangent of the scores
+  long rows;
+  int S, dual;
+  float scale;
+};
+
+struct EmbedGradArgs {
+  const float* dh; const float* dhd;         // [N][d] gradient at the embedding output
+  const int* perm; const int* run_len; const int* tok2run;
+  long emb_off;
+  float* outE;                               // operand copy of the new rows (fp32 [V][d]) or null
+  int V, d;
+};
+
+hipError_t split_tokens(const int* tok, int B, int S, int V, int* ids, int* labels,
+                        hipStream_t s);
+hipError_t gather_rows(const int* ids, int N, int d, const float* E, const float* Ed, float* h,
+                       float* hd, hipStream_t s);
+hipError_t ln_fwd(const LnArgs& a, hipStream_t s);
+int ln_bwd_parts(int N);
+template <typename T>
+hipError_t ln_bwd(const LnBwdArgs& a, long g_off, long b_off, const ParamArgs<T>& P,
+                  float* out_g, float* out_b, hipStream_t s);
+hipError_t rope_table(int S, int dh, double base, float* cs, float* sn, hipStream_t s);
+hipError_t rope_split(const RopeArgs& a, hipStream_t s);
+hipError_t rope_merge(const RopeArgs& a, hipStream_t s);
+hipError_t softmax_fwd(const SoftmaxArgs& a, hipStream_t s);
+hipError_t softmax_bwd(const SoftmaxArgs& a, hipStream_t s);
+bool sort_tokens_fits(int N);
+hipError_t sort_tokens(const int* ids, int N, int V, int* perm, int* run_start, int* run_len,
+                       int* tok2run, hipStream_t s);
+template <typename T>
+hipError_t embed_grad(const EmbedGradArgs& a, const ParamArgs<T>& P, hipStream_t s);
+hipError_t meta_out(const float* hid, int rows, int hdim, const float* w2, const float* b2,
+                    float* u, hipStream_t s);
+int meta_vjp_parts(int rows);
+hipError_t meta_vjp(const float* hid, const float* ubar, int rows, int hdim, const float* w2,
+                    float* dhid, float* partial, float* d_w2, float* d_b1, float* d_b2,
+                    hipStream_t s);
+
+}  // namespace mfmg

@@ -1,0 +1,570 @@
+// Decoder-block dual kernels (gfx950): token gather, LayerNorm, RoPE head
+// split/merge, causal softmax, embedding scatter and the loss-weighting
+// meta-model, each with the tangent carried alongside (forward-over-reverse,
+// Section 2.2; the transformer workloads of Section 5).  Matrix products go
+// through gemm_nt; these kernels are the elementwise/row-wise pieces.
+//
+// Layouts: token rows n = b * seq + s; residual stream and LayerNorm values
+// float32 [tokens][d]; per-head tensors float32 [batch * heads][seq][dh];
+// attention scores/probabilities float32 [batch * heads][seq][seq].
+#include "kernels.h"
+#include "param_epi.h"
+#include "transformer.h"
+
+namespace mfmg {
+
+namespace {
+
+inline int cdivl(long a, long b) { return (int)((a + b - 1) / b); }
+
+// ------------------------------------------------------------------------------------
+// Tokens: input ids and next-token labels from [batch][seq + 1] sequences.
+// Out-of-range ids gather a zero row; out-of-range labels make the loss NaN.
+// ------------------------------------------------------------------------------------
+__global__ void split_tokens_kernel(const int* __restrict__ tok, int B, int S, int V, int* ids,
+                                    int* labels) {
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= B * S) return;
+  const int b = n / S, s = n % S;
+  const int a = tok[b * (S + 1) + s];
+  const int y = tok[b * (S + 1) + s + 1];
+  ids[n] = (a >= 0 && a < V) ? a : -1;
+  labels[n] = (y >= 0 && y < V) ? y : -1;
+}
+
+// h[n] = E[ids[n]] (and the tangent rows).
+__global__ void gather_rows_kernel(const int* __restrict__ ids, int N, int d,
+                                   const float* __restrict__ E, const float* __restrict__ Ed,
+                                   float* h, float* hd) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (long)N * d) return;
+  const int n = (int)(e / d), j = (int)(e % d);
+  const int v = ids[n];
+  h[e] = v >= 0 ? E[(long)v * d + j] : 0.0f;
+  if (hd) hd[e] = v >= 0 ? Ed[(long)v * d + j] : 0.0f;
+}
+
+// ------------------------------------------------------------------------------------
+// LayerNorm forward, one wavefront per row: xh = (x - mean) rstd,
+// y = g xh + b.  Tangent: xhd = rstd (xd - mean(xd) - xh mean(xh xd)),
+// yd = g xhd + gd xh + bd.  Saves xh, rstd, c = mean(xh xd) and xhd for the
+// backward.
+// ------------------------------------------------------------------------------------
+constexpr int LN_MAXPL = 16;  // d <= 64 * 16
+
+__global__ void __launch_bounds__(256) ln_fwd_kernel(LnArgs a) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.N) return;
+  const int d = a.d;
+  const float* x = a.x + (long)row * d;
+  float xv[LN_MAXPL], xdv[LN_MAXPL];
+  float s = 0.f;
+  int cnt = 0;
+  for (int j = lane, k = 0; j < d; j += 64, ++k) {
+    xv[k] = x[j];
+    s += xv[k];
+    cnt = k + 1;
+  }
+  const float mean = wave_sum(s) / d;
+  float v = 0.f;
+  for (int k = 0; k < cnt; ++k) {
+    xv[k] -= mean;
+    v += xv[k] * xv[k];
+  }
+  const float rstd = rsqrtf(wave_sum(v) / d + a.eps);
+  for (int k = 0; k < cnt; ++k) xv[k] *= rstd;  // xh
+  float c = 0.f, md = 0.f;
+  if (a.dual) {
+    const float* xd = a.xd + (long)row * d;
+    for (int j = lane, k = 0; j < d; j += 64, ++k) {
+      xdv[k] = xd[j];
+      md += xdv[k];
+      c += xv[k] * xdv[k];
+    }
+    md = wave_sum(md) / d;
+    c = wave_sum(c) / d;
+  }
+  for (int j = lane, k = 0; j < d; j += 64, ++k) {
+    const long o = (long)row * d + j;
+    a.xh[o] = xv[k];
+    a.y[o] = a.g[j] * xv[k] + a.b[j];
+    if (a.dual) {
+      const float xhd = rstd * (xdv[k] - md - xv[k] * c);
+      a.xhd[o] = xhd;
+      a.yd[o] = a.g[j] * xhd + a.gd[j] * xv[k] + a.bd[j];
+    }
+  }
+  if (lane == 0) {
+    a.rstd[row] = rstd;
+    if (a.dual) a.c[row] = c;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// LayerNorm backward, one wavefront per row, with the residual add:
+//   q = g dy, A = q - mean(q) - xh mean(xh q), dx = rstd A, dh_out = dh_in + dx.
+// Tangent (w.r.t. x through xh and rstd, g and dy): with rstd' = -rstd^2 c,
+//   qd = gd dy + g dyd,
+//   Ad = qd - mean(qd) - xhd mean(xh q) - xh (mean(xhd q) + mean(xh qd)),
+//   dxd = rstd' A + rstd Ad.
+// Per-block partial column sums of dy xh, dy and their tangents
+// (dyd xh + dy xhd, dyd) feed the parameter epilogue of g and b.
+// ------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) ln_bwd_kernel(LnBwdArgs a) {
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int d = a.d;
+  // each block: 4 waves x LN_ROWS rows; partial sums per block in a.partial
+  float pg[LN_MAXPL], pb[LN_MAXPL], pgd[LN_MAXPL], pbd[LN_MAXPL];
+  int cnt = 0;
+  for (int j = lane, k = 0; j < d; j += 64, ++k) {
+    pg[k] = pb[k] = pgd[k] = pbd[k] = 0.f;
+    cnt = k + 1;
+  }
+  for (int rr = 0; rr < LN_ROWS_PER_WAVE; ++rr) {
+    const int row = (blockIdx.x * 4 + wave) * LN_ROWS_PER_WAVE + rr;
+    if (row >= a.N) break;
+    const long base = (long)row * d;
+    const float rstd = a.rstd[row];
+    float xh[LN_MAXPL], dy[LN_MAXPL], q[LN_MAXPL];
+    float mq = 0.f, mxq = 0.f;
+    for (int j = lane, k = 0; j < d; j += 64, ++k) {
+      xh[k] = a.xh[base + j];
+      dy[k] = a.dy[base + j];
+      q[k] = a.g[j] * dy[k];
+      mq += q[k];
+      mxq += xh[k] * q[k];
+    }
+    mq = wave_sum(mq) / d;
+    mxq = wave_sum(mxq) / d;
+    float xhd[LN_MAXPL], dyd[LN_MAXPL], qd[LN_MAXPL];
+    float mqd = 0.f, mxdq = 0.f, mxqd = 0.f;
+    if (a.dual) {
+      for (int j = lane, k = 0; j < d; j += 64, ++k) {
+        xhd[k] = a.xhd[base + j];
+        dyd[k] = a.dyd[base + j];
+        qd[k] = a.gd[j] * dy[k] + a.g[j] * dyd[k];
+        mqd += qd[k];
+        mxdq += xhd[k] * q[k];
+        mxqd += xh[k] * qd[k];
+      }
+      mqd = wave_sum(mqd) / d;
+      mxdq = wave_sum(mxdq) / d;
+      mxqd = wave_sum(mxqd) / d;
+    }
+    const float rstdd = a.dual ? -rstd * rstd * a.c[row] : 0.f;
+    for (int j = lane, k = 0; j < d; j += 64, ++k) {
+      const float A = q[k] - mq - xh[k] * mxq;
+      a.dh_out[base + j] = (a.dh_in ? a.dh_in[base + j] : 0.f) + rstd * A;
+      pg[k] += dy[k] * xh[k];
+      pb[k] += dy[k];
+      if (a.dual) {
+        const float Ad = qd[k] - mqd - xhd[k] * mxq - xh[k] * (mxdq + mxqd);
+        a.dhd_out[base + j] = (a.dhd_in ? a.dhd_in[base + j] : 0.f) + rstdd * A + rstd * Ad;
+        pgd[k] += dyd[k] * xh[k] + dy[k] * xhd[k];
+        pbd[k] += dyd[k];
+      }
+    }
+  }
+  // partial[(block * 4 + wave)][4][d]
+  float* P = a.partial + (long)(blockIdx.x * 4 + wave) * 4 * d;
+  for (int j = lane, k = 0; j < d; j += 64, ++k) {
+    P[j] = pg[k];
+    P[d + j] = pb[k];
+    P[2 * d + j] = pgd[k];
+    P[3 * d + j] = pbd[k];
+  }
+  (void)cnt;
+}
+
+// Column sums of the per-wave partials in a fixed order, then the parameter
+// epilogue on g (offset g_off) and b (offset b_off).
+template <typename T>
+__global__ void __launch_bounds__(256) ln_param_kernel(const float* __restrict__ partial,
+                                                       int nparts, int d, long g_off, long b_off,
+                                                       ParamArgs<T> P, float* out_g,
+                                                       float* out_b) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  float sg = 0.f, sb = 0.f, sgd = 0.f, sbd = 0.f;
+  for (int p = 0; p < nparts; ++p) {
+    const float* Pp = partial + (long)p * 4 * d;
+    sg += Pp[j];
+    sb += Pp[d + j];
+    sgd += Pp[2 * d + j];
+    sbd += Pp[3 * d + j];
+  }
+  const float cg = param_elem(P, g_off + j, sg, sgd);
+  const float cb = param_elem(P, b_off + j, sb, sbd);
+  if (out_g) out_g[j] = cg;
+  if (out_b) out_b[j] = cb;
+}
+
+// ------------------------------------------------------------------------------------
+// RoPE.  cos/sin table [seq][dh/2] in double precision, rounded to float.
+// Rotate-half pairing (j, j + dh/2): q'_j = q_j c - q_{j+h} s,
+// q'_{j+h} = q_{j+h} c + q_j s, with angle s * base^(-2j/dh).  Linear, so the
+// tangent uses the same rotation; the backward applies the transpose.
+// ------------------------------------------------------------------------------------
+__global__ void rope_table_kernel(int S, int dh, double base, float* cs, float* sn) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int half = dh / 2;
+  if (e >= S * half) return;
+  const int s = e / half, j = e % half;
+  const double ang = (double)s * pow(base, -2.0 * j / dh);
+  cs[e] = (float)cos(ang);
+  sn[e] = (float)sin(ang);
+}
+
+// qkv [N][3d] (columns q heads | k heads | v heads) -> per-head Q, K (rotated), V.
+__global__ void rope_split_kernel(RopeArgs a) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  const int d = a.H * a.dh, half = a.dh / 2;
+  if (e >= (long)a.N * d) return;
+  const int n = (int)(e / d), c = (int)(e % d);
+  const int h = c / a.dh, j = c % a.dh;
+  const int b = n / a.S, s = n % a.S;
+  const long src = (long)n * 3 * d;
+  const long dst = ((long)(b * a.H + h) * a.S + s) * a.dh + j;
+  const int jp = j < half ? j + half : j - half;
+  const float cs = a.cs[s * half + (j % half)], sn = a.sn[s * half + (j % half)];
+  const float sg = j < half ? -sn : sn;
+  for (int t = 0; t < (a.dual ? 2 : 1); ++t) {
+    const float* q = t == 0 ? a.qkv : a.qkvd;
+    float* Q = t == 0 ? a.Q : a.Qd;
+    float* K = t == 0 ? a.K : a.Kd;
+    float* Vv = t == 0 ? a.V : a.Vd;
+    Q[dst] = q[src + h * a.dh + j] * cs + sg * q[src + h * a.dh + jp];
+    K[dst] = q[src + d + h * a.dh + j] * cs + sg * q[src + d + h * a.dh + jp];
+    Vv[dst] = q[src + 2 * d + h * a.dh + j];
+  }
+}
+
+// Per-head dQ, dK (rotated frame), dV -> dqkv [N][3d] in the unrotated frame.
+__global__ void rope_merge_kernel(RopeArgs a) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  const int d = a.H * a.dh, half = a.dh / 2;
+  if (e >= (long)a.N * d) return;
+  const int n = (int)(e / d), c = (int)(e % d);
+  const int h = c / a.dh, j = c % a.dh;
+  const int b = n / a.S, s = n % a.S;
+  const long dst = (long)n * 3 * d;
+  const long src = ((long)(b * a.H + h) * a.S + s) * a.dh;
+  const int jp = j < half ? j + half : j - half;
+  const float cs = a.cs[s * half + (j % half)], sn = a.sn[s * half + (j % half)];
+  const float sg = j < half ? sn : -sn;  // transpose of the rotation
+  for (int t = 0; t < (a.dual ? 2 : 1); ++t) {
+    const float* Q = t == 0 ? a.Q : a.Qd;
+    const float* K = t == 0 ? a.K : a.Kd;
+    const float* Vv = t == 0 ? a.V : a.Vd;
+    float* q = t == 0 ? a.qkv_out : a.qkvd_out;
+    q[dst + h * a.dh + j] = Q[src + j] * cs + sg * Q[src + jp];
+    q[dst + d + h * a.dh + j] = K[src + j] * cs + sg * K[src + jp];
+    q[dst + 2 * d + h * a.dh + j] = Vv[src + j];
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Causal softmax over keys 0..q of each query row q, one wavefront per row.
+// Tangent: Pd = P (Sd - <P, Sd>).  Scores arrive already scaled.
+// ------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) softmax_fwd_kernel(SoftmaxArgs a) {
+  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.rows) return;
+  const int S = a.S;
+  const int q = (int)(row % S);
+  const long base = row * S;
+  float mx = -INFINITY;
+  for (int k = lane; k <= q; k += 64) mx = fmaxf(mx, a.Sc[base + k]);
+  mx = wave_max(mx);
+  float se = 0.f;
+  for (int k = lane; k <= q; k += 64) se += expf(a.Sc[base + k] - mx);
+  se = wave_sum(se);
+  const float inv = 1.0f / se;
+  float sd = 0.f;
+  if (a.dual) {
+    for (int k = lane; k <= q; k += 64) sd += expf(a.Sc[base + k] - mx) * inv * a.Scd[base + k];
+    sd = wave_sum(sd);
+  }
+  for (int k = lane; k < S; k += 64) {
+    const float p = k <= q ? expf(a.Sc[base + k] - mx) * inv : 0.0f;
+    a.P[base + k] = p;
+    if (a.dual) a.Pd[base + k] = k <= q ? p * (a.Scd[base + k] - sd) : 0.0f;
+  }
+}
+
+// dS = scale P (dP - r), r = <P, dP>; tangent with rd = <Pd, dP> + <P, dPd>:
+// dSd = scale (Pd (dP - r) + P (dPd - rd)).
+__global__ void __launch_bounds__(256) softmax_bwd_kernel(SoftmaxArgs a) {
+  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.rows) return;
+  const int S = a.S;
+  const long base = row * S;
+  float r = 0.f, rd = 0.f;
+  for (int k = lane; k < S; k += 64) {
+    r += a.P[base + k] * a.dP[base + k];
+    if (a.dual) rd += a.Pd[base + k] * a.dP[base + k] + a.P[base + k] * a.dPd[base + k];
+  }
+  r = wave_sum(r);
+  if (a.dual) rd = wave_sum(rd);
+  for (int k = lane; k < S; k += 64) {
+    const float p = a.P[base + k], g = a.dP[base + k];
+    a.dS[base + k] = a.scale * p * (g - r);
+    if (a.dual)
+      a.dSd[base + k] = a.scale * (a.Pd[base + k] * (g - r) + p * (a.dPd[base + k] - rd));
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Embedding gradient.  The token ids of a batch are sorted once (bitonic sort of
+// (id, position) pairs in one workgroup), giving runs of equal ids; each
+// vocabulary row then sums the rows of its run in position order, which keeps
+// the scatter-add deterministic even for the Zipf-hot ids.
+// ------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(1024) sort_tokens_kernel(const int* __restrict__ ids, int N,
+                                                           int V, int* perm, int* run_start,
+                                                           int* run_len, int* tok2run) {
+  extern __shared__ unsigned long long key[];
+  int P2 = 1;
+  while (P2 < N) P2 <<= 1;
+  for (int i = threadIdx.x; i < P2; i += blockDim.x) {
+    const unsigned long long id = i < N ? (unsigned long long)(unsigned)(ids[i] < 0 ? V : ids[i])
+                                        : 0xffffffffull;
+    key[i] = (id << 32) | (unsigned)i;
+  }
+  for (int v = threadIdx.x; v < V; v += blockDim.x) tok2run[v] = -1;
+  __syncthreads();
+  for (int k = 2; k <= P2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < P2; i += blockDim.x) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const bool up = (i & k) == 0;
+          const unsigned long long x = key[i], y = key[ixj];
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < N; i += blockDim.x) perm[i] = (int)(key[i] & 0xffffffffu);
+  // run heads
+  for (int i = threadIdx.x; i < N; i += blockDim.x) {
+    const unsigned id = (unsigned)(key[i] >> 32);
+    if (id >= (unsigned)V) continue;
+    if (i == 0 || (unsigned)(key[i - 1] >> 32) != id) {
+      int e = i + 1;
+      while (e < N && (unsigned)(key[e] >> 32) == id) ++e;
+      tok2run[id] = i;
+      run_start[i] = i;
+      run_len[i] = e - i;
+    }
+  }
+}
+
+// g[v][j] = sum over positions n with ids[n] == v of dh[n][j] (tangent too), then
+// the parameter epilogue over every vocabulary row (rows without occurrences
+// get g = 0).
+template <typename T>
+__global__ void __launch_bounds__(256) embed_grad_kernel(EmbedGradArgs a, ParamArgs<T> P) {
+  const long e4 = ((long)blockIdx.x * 256 + threadIdx.x) * 4;  // 4 consecutive j
+  const int d = a.d;
+  if (e4 >= (long)a.V * d) return;
+  const int v = (int)(e4 / d), j = (int)(e4 % d);
+  float g[4] = {0.f, 0.f, 0.f, 0.f}, hv[4] = {0.f, 0.f, 0.f, 0.f}, cv[4];
+  const int cnt = min(4, d - j);
+  const int r = a.tok2run[v];
+  if (r >= 0) {
+    const int len = a.run_len[r];
+    for (int i = 0; i < len; ++i) {
+      const long n = a.perm[r + i];
+      for (int k = 0; k < cnt; ++k) {
+        g[k] += a.dh[n * d + j + k];
+        if (a.dhd) hv[k] += a.dhd[n * d + j + k];
+      }
+    }
+  }
+  param_apply(P, a.emb_off + (long)v * d + j, cnt, g, hv, cv);
+  if (a.outE)
+    for (int k = 0; k < cnt; ++k) a.outE[(long)v * d + j + k] = cv[k];
+}
+
+// ------------------------------------------------------------------------------------
+// Loss-weighting meta-model u = w2 . tanh(e W1 + b1) + b2 (alpha = sigmoid(u)):
+// the hidden layer is a gemm_nt product; these are its output row and VJP.
+// ------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) meta_out_kernel(const float* __restrict__ hid, int rows,
+                                                       int hdim, const float* __restrict__ w2,
+                                                       const float* __restrict__ b2, float* u) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  float s = 0.f;
+  for (int j = lane; j < hdim; j += 64) s += hid[(long)row * hdim + j] * w2[j];
+  s = wave_sum(s);
+  if (lane == 0) u[row] = s + b2[0];
+}
+
+// dhid[n][j] = ubar_n w2_j (1 - hid^2); per-block partials of
+// sum_n ubar_n hid[n][j] (-> d w2), sum_n dhid[n][j] (-> d b1), sum_n ubar_n (-> d b2).
+__global__ void __launch_bounds__(256) meta_vjp_rows_kernel(const float* __restrict__ hid,
+                                                            const float* __restrict__ ubar,
+                                                            int rows, int hdim,
+                                                            const float* __restrict__ w2,
+                                                            float* dhid, float* partial,
+                                                            int rows_per_block) {
+  // thread t handles column j = t of the block's row range (hdim <= 256)
+  const int j = threadIdx.x;
+  const int r0 = blockIdx.x * rows_per_block;
+  const int r1 = min(rows, r0 + rows_per_block);
+  float sw = 0.f, sb = 0.f, su = 0.f;
+  if (j < hdim) {
+    for (int n = r0; n < r1; ++n) {
+      const float h = hid[(long)n * hdim + j];
+      const float ub = ubar[n];
+      const float dh = ub * w2[j] * (1.0f - h * h);
+      dhid[(long)n * hdim + j] = dh;
+      sw += ub * h;
+      sb += dh;
+      su += ub;
+    }
+    float* Pp = partial + (long)blockIdx.x * (2 * hdim + 1);
+    Pp[j] = sw;
+    Pp[hdim + j] = sb;
+    if (j == 0) Pp[2 * hdim] = su;
+  }
+}
+
+__global__ void meta_vjp_reduce_kernel(const float* __restrict__ partial, int nparts, int hdim,
+                                       float* d_w2, float* d_b1, float* d_b2) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j > hdim) return;
+  if (j == hdim) {
+    float s = 0.f;
+    for (int p = 0; p < nparts; ++p) s += partial[(long)p * (2 * hdim + 1) + 2 * hdim];
+    d_b2[0] = s;
+    return;
+  }
+  float sw = 0.f, sb = 0.f;
+  for (int p = 0; p < nparts; ++p) {
+    sw += partial[(long)p * (2 * hdim + 1) + j];
+    sb += partial[(long)p * (2 * hdim + 1) + hdim + j];
+  }
+  d_w2[j] = sw;
+  d_b1[j] = sb;
+}
+
+}  // namespace
+
+hipError_t split_tokens(const int* tok, int B, int S, int V, int* ids, int* labels,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(split_tokens_kernel, dim3(cdivl((long)B * S, 256)), dim3(256), 0, s, tok, B,
+                     S, V, ids, labels);
+  return hipGetLastError();
+}
+
+hipError_t gather_rows(const int* ids, int N, int d, const float* E, const float* Ed, float* h,
+                       float* hd, hipStream_t s) {
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(cdivl((long)N * d, 256)), dim3(256), 0, s, ids, N, d,
+                     E, Ed, h, hd);
+  return hipGetLastError();
+}
+
+hipError_t ln_fwd(const LnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+int ln_bwd_parts(int N) { return cdivl(N, 4 * LN_ROWS_PER_WAVE) * 4; }
+
+template <typename T>
+hipError_t ln_bwd(const LnBwdArgs& a, long g_off, long b_off, const ParamArgs<T>& P,
+                  float* out_g, float* out_b, hipStream_t s) {
+  hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdivl(a.N, 4 * LN_ROWS_PER_WAVE)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(ln_param_kernel<T>, dim3(cdivl(a.d, 256)), dim3(256), 0, s, a.partial,
+                     ln_bwd_parts(a.N), a.d, g_off, b_off, P, out_g, out_b);
+  return hipGetLastError();
+}
+
+hipError_t rope_table(int S, int dh, double base, float* cs, float* sn, hipStream_t s) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(cdivl((long)S * dh / 2, 256)), dim3(256), 0, s, S, dh,
+                     base, cs, sn);
+  return hipGetLastError();
+}
+
+hipError_t rope_split(const RopeArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(rope_split_kernel, dim3(cdivl((long)a.N * a.H * a.dh, 256)), dim3(256), 0, s,
+                     a);
+  return hipGetLastError();
+}
+
+hipError_t rope_merge(const RopeArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(rope_merge_kernel, dim3(cdivl((long)a.N * a.H * a.dh, 256)), dim3(256), 0, s,
+                     a);
+  return hipGetLastError();
+}
+
+hipError_t softmax_fwd(const SoftmaxArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_fwd_kernel, dim3(cdivl(a.rows, 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t softmax_bwd(const SoftmaxArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_bwd_kernel, dim3(cdivl(a.rows, 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+bool sort_tokens_fits(int N) { return N >= 1 && N <= TOKEN_SORT_MAX; }
+
+hipError_t sort_tokens(const int* ids, int N, int V, int* perm, int* run_start, int* run_len,
+                       int* tok2run, hipStream_t s) {
+  int P2 = 1;
+  while (P2 < N) P2 <<= 1;
+  hipLaunchKernelGGL(sort_tokens_kernel, dim3(1), dim3(1024), P2 * sizeof(unsigned long long), s,
+                     ids, N, V, perm, run_start, run_len, tok2run);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t embed_grad(const EmbedGradArgs& a, const ParamArgs<T>& P, hipStream_t s) {
+  hipLaunchKernelGGL(embed_grad_kernel<T>, dim3(cdivl((long)a.V * a.d / 4 + 1, 256)), dim3(256), 0,
+                     s, a, P);
+  return hipGetLastError();
+}
+
+hipError_t meta_out(const float* hid, int rows, int hdim, const float* w2, const float* b2,
+                    float* u, hipStream_t s) {
+  hipLaunchKernelGGL(meta_out_kernel, dim3(cdivl(rows, 4)), dim3(256), 0, s, hid, rows, hdim, w2,
+                     b2, u);
+  return hipGetLastError();
+}
+
+int meta_vjp_parts(int rows) { return cdivl(rows, META_ROWS_PER_BLOCK); }
+
+hipError_t meta_vjp(const float* hid, const float* ubar, int rows, int hdim, const float* w2,
+                    float* dhid, float* partial, float* d_w2, float* d_b1, float* d_b2,
+                    hipStream_t s) {
+  const int parts = meta_vjp_parts(rows);
+  hipLaunchKernelGGL(meta_vjp_rows_kernel, dim3(parts), dim3(256), 0, s, hid, ubar, rows, hdim, w2,
+                     dhid, partial, META_ROWS_PER_BLOCK);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(meta_vjp_reduce_kernel, dim3(cdivl(hdim + 1, 256)), dim3(256), 0, s, partial,
+                     parts, hdim, d_w2, d_b1, d_b2);
+  return hipGetLastError();
+}
+
+template hipError_t ln_bwd<bf16_t>(const LnBwdArgs&, long, long, const ParamArgs<bf16_t>&, float*, float*, hipStream_t);
+template hipError_t ln_bwd<float>(const LnBwdArgs&, long, long, const ParamArgs<float>&, float*, float*, hipStream_t);
+template hipError_t embed_grad<bf16_t>(const EmbedGradArgs&, const ParamArgs<bf16_t>&, hipStream_t);
+template hipError_t embed_grad<float>(const EmbedGradArgs&, const ParamArgs<float>&, hipStream_t);
+
+}  // namespace mfmg

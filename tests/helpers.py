@@ -11,6 +11,14 @@ BF16_TOL = 2e-2   # bfloat16 GEMM operands, against the oracle's bf16-emulation 
 
 def desc_of(cfg: W.Config):
     from paper_2505_00793_amd import _lib as M
+    if cfg.kind == W.KIND_TRANSFORMER:
+        return M.make_desc(kind=1, widths=(1, 1), loss=cfg.loss, optimizer=cfg.optimizer,
+                           meta=cfg.meta, precision=cfg.precision, has_bias=False,
+                           rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
+                           d_model=cfg.d_model, n_heads=cfg.n_heads, d_ff=cfg.d_ff,
+                           vocab=cfg.vocab, seq=cfg.seq, n_blocks=cfg.n_blocks,
+                           meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps,
+                           rope_base=cfg.rope_base)
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
@@ -29,10 +37,13 @@ def relerr(a, b) -> float:
 
 def eta_groups(cfg: W.Config):
     """Index groups over which the normwise error of d eta is taken: each
-    per-layer log-lr and the weight decay separately; otherwise all of eta."""
+    per-layer log-lr and the weight decay separately; each meta-model tensor;
+    otherwise all of eta."""
     n = W.n_eta(cfg)
     if cfg.meta == W.META_LOGLR_PER_LAYER_WD:
         return [np.array([i]) for i in range(n)]
+    if cfg.meta == W.META_TOKEN_WEIGHT_MLP:
+        return [np.arange(off, off + int(np.prod(shape))) for _, off, shape in W.meta_layout(cfg)]
     return [np.arange(n)]
 
 

@@ -1,0 +1,134 @@
+"""GPU parity for the transformer workload (decoder blocks with RoPE, causal
+attention, LayerNorm, GELU MLP; per-token loss weights from a meta-model),
+through the C ABI, against the float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from helpers import desc_of, group_errors, relerr, to_device, tol_of
+from oracle import models as OM
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_00793_amd import _lib
+    _lib.lib()
+
+
+def M():
+    from paper_2505_00793_amd import _lib
+    return _lib
+
+
+def c(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+SMALL = W.SMALL["c4_small"]
+CASES = {"fp32": SMALL.with_(precision=W.PREC_FP32), "bf16": SMALL}
+
+
+def token_alpha(cfg, theta, eta, tokens):
+    """The loss weights the GPU uses in single-step calls: the meta-model on the
+    embedding rows of the theta passed in."""
+    th = torch.from_numpy(theta).double()
+    emb = OM.unpack(th, W.theta_layout(cfg))["emb"]
+    xin, _ = OM.split_tokens(torch.from_numpy(tokens).long())
+    return OM.meta_mlp_alpha(cfg, torch.from_numpy(eta).double(), emb[xin]).reshape(-1).numpy()
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_tf_inner_step(prec):
+    cfg = CASES[prec]
+    inp = W.make_inputs(cfg)
+    n = W.n_theta(cfg)
+    theta = inp["theta0"] + 0.02 * W.random_direction(n, 51)
+    tok = inp["train_x"][0]
+    alpha = token_alpha(cfg, theta, inp["eta"], tok)
+    print(f"\n[tf inner_step] {prec}", flush=True)
+    th1_ref, _, g_ref, L_ref = oracle.inner_step(cfg, theta, None, inp["eta"], tok, None, 0,
+                                                 alpha=alpha, bf16=prec == "bf16")
+    P = M().Problem(desc_of(cfg))
+    th1 = torch.empty(n, device="cuda")
+    g = torch.empty(n, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    dummy_y = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.mfmg_inner_step(c(theta), None, c(inp["eta"]), c(tok), dummy_y, 0, th1, None, g, loss)
+    torch.cuda.synchronize()
+    e_g = relerr(g.cpu().numpy(), g_ref)
+    e_up = relerr(th1.cpu().numpy() - theta, th1_ref - theta)
+    print(f"  grad {e_g:.2e} update {e_up:.2e} loss {loss.item():.6f} ref {L_ref:.6f}", flush=True)
+    lay = W.theta_layout(cfg)
+    gg = g.cpu().numpy()
+    for name, off, shape in lay:
+        k = int(np.prod(shape))
+        e = relerr(gg[off:off + k], g_ref[off:off + k])
+        if e > tol_of(cfg):
+            print(f"    {name}: {e:.2e}", flush=True)
+    assert e_g <= tol_of(cfg) and e_up <= tol_of(cfg)
+    assert abs(loss.item() - L_ref) <= tol_of(cfg) * abs(L_ref)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_tf_hvp(prec):
+    cfg = CASES[prec]
+    inp = W.make_inputs(cfg)
+    n = W.n_theta(cfg)
+    theta = inp["theta0"] + 0.02 * W.random_direction(n, 52)
+    v = 0.1 * W.random_direction(n, 53)
+    tok = inp["train_x"][0]
+    alpha = token_alpha(cfg, theta, inp["eta"], tok)
+    bf16 = prec == "bf16"
+    print(f"\n[tf hvp] {prec}", flush=True)
+    hv_ref = oracle.hvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
+    mv_ref = oracle.mvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
+    g_ref, _ = oracle.grad_and_loss(cfg, theta, tok, None, alpha=alpha, bf16=bf16)
+    P = M().Problem(desc_of(cfg))
+    g = torch.empty(n, device="cuda")
+    hv = torch.empty(n, device="cuda")
+    mv = torch.empty(cfg.rows * cfg.seq, device="cuda")
+    dummy_y = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.mfmg_hvp_fwd_over_rev(c(theta), c(inp["eta"]), c(tok), dummy_y, 0, c(v), g, hv, mv)
+    torch.cuda.synchronize()
+    e = (relerr(g.cpu().numpy(), g_ref), relerr(hv.cpu().numpy(), hv_ref),
+         relerr(mv.cpu().numpy(), mv_ref))
+    print(f"  grad {e[0]:.2e} hvp {e[1]:.2e} mvp {e[2]:.2e}", flush=True)
+    hh = hv.cpu().numpy()
+    for name, off, shape in W.theta_layout(cfg):
+        k = int(np.prod(shape))
+        ee = relerr(hh[off:off + k], hv_ref[off:off + k])
+        if ee > tol_of(cfg):
+            print(f"    {name}: hvp {ee:.2e}", flush=True)
+    assert max(e) <= tol_of(cfg)
+
+
+def run_meta_tf(cfg, inp):
+    P = M().Problem(desc_of(cfg))
+    dev = to_device(inp)
+    d = torch.full((W.n_eta(cfg),), float("nan"), device="cuda")
+    vl = torch.full((1,), float("nan"), device="cuda")
+    dummy = torch.zeros(1, dtype=torch.int32, device="cuda")
+    peak = P.mfmg_meta_grad(dev["theta0"], None, dev["eta"], dev["xs"], [dummy] * len(dev["xs"]),
+                            dev["vx"], dummy, d, vl)
+    torch.cuda.synchronize()
+    return d.cpu().numpy().astype(np.float64), float(vl.item()), peak
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_tf_meta_grad(prec):
+    cfg = CASES[prec]
+    inp = W.make_inputs(cfg)
+    print(f"\n[tf meta_grad] {prec} T={cfg.T}", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=prec == "bf16")
+    errs = group_errors(cfg, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)

@@ -123,6 +123,9 @@ SMALL: Dict[str, Config] = {
                              precision=PREC_FP32, rows=33, val_rows=20, T=3),
     "c3_fp32": C3.with_(name="c3_fp32", cfg_id=108, widths=(40, 48, 9), precision=PREC_FP32,
                         rows=36, val_rows=25, T=3, loglr_init=math.log(1e-2)),
+    # large enough that every layer's products use the 128 x 128 bf16 tiles
+    "c5_mid": C5.with_(name="c5_mid", cfg_id=109, widths=(2048, 2048, 2048, 64), rows=2048,
+                       val_rows=512, T=2),
     "c4_small": C4.with_(name="c4_small", cfg_id=104, d_model=64, n_heads=4, d_ff=128, vocab=97,
                          seq=24, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2),
 }
