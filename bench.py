@@ -108,6 +108,9 @@ def main():
     ap.add_argument("--sweep-steps", type=int, default=3,
                     help="timed calls per T of the memory sweep (0 = sizes only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="first run a plain device copy of this many bytes (a known-size "
+                         "reference for hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the meta-gradient path is single-device "
@@ -116,6 +119,15 @@ def main():
 
     import torch
     from paper_2505_00793_amd import _lib as M
+
+    if args.copy_bytes > 0:
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
 
     cfg = W.C5.with_(T=args.T)
     T = args.T

@@ -26,7 +26,8 @@ import oracle  # noqa: E402
 import workloads as W  # noqa: E402
 from oracle.metagrad import working_precision  # noqa: E402
 
-CASES = [("c5_mlp_relu_8x4096", 2), ("c5_mlp_relu_8x4096", 4), ("c3_mlp_gelu_adam", 16)]
+CASES = [("c5_mlp_relu_8x4096", 2), ("c5_mlp_relu_8x4096", 4), ("c3_mlp_gelu_adam", 16),
+         ("c4_transformer_tokenweights", 2)]
 FP32_CASES = [("c3_mlp_gelu_adam", 16)]
 
 
@@ -45,11 +46,12 @@ def rel(a, b, g):
 def main():
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "bf16_spread.json")
     only_fp32 = "--fp32-only" in sys.argv
-    out = json.load(open(path)) if only_fp32 and os.path.exists(path) else {"note": ("normwise relative distances per eta group between the oracle's bf16-operand "
+    only = [a.split("=", 1)[1] for a in sys.argv if a.startswith("--only=")]
+    out = json.load(open(path)) if (only_fp32 or only) and os.path.exists(path) else {"note": ("normwise relative distances per eta group between the oracle's bf16-operand "
                     "emulations accumulated in float64 ('emu64') and in float32 ('emu32'), and "
                     "each to the unrounded float64 oracle ('fp64'); '/fp32' entries: float32 "
                     "GEMMs ('fp32') and the whole oracle in float32 ('fp32all') against float64")}
-    for name, T in ([] if only_fp32 else CASES):
+    for name, T in ([] if only_fp32 else [c for c in CASES if not only or c[0] in only]):
         cfg = W.CONFIGS[name].with_(T=T)
         inp = W.make_inputs(cfg, T=T)
         d64, _ = oracle.meta_grad_checkpointed(cfg, inp)
@@ -62,7 +64,7 @@ def main():
             "emu32_vs_fp64": [rel(e32, d64, g) for g in gs],
         }
         print(name, T, out[f"{name}/T{T}"], flush=True)
-    for name, T in FP32_CASES:
+    for name, T in ([] if only else FP32_CASES):
         cfg = W.CONFIGS[name].with_(T=T, precision=W.PREC_FP32)
         inp = W.make_inputs(cfg, T=T)
         d64, _ = oracle.meta_grad_checkpointed(cfg, inp)
