@@ -263,6 +263,15 @@ struct Stage {
   static constexpr int SLD = BN + 4;  // padded LDS row stride, floats
 };
 
+// NPASS: the tile is staged in NPASS slabs of BM / NPASS rows.
+template <int FLAGS, int BM, int BN, int NPASS>
+struct EpiSmem {
+  static constexpr int NS = (FLAGS & (G_AD | G_BD)) ? 2 : 1;  // staged accumulators
+  static constexpr int BYTES = NS * (BM / NPASS) * Stage<BN>::SLD * 4;
+};
+
+// LDS of the register-staged main loop: double-buffered tiles, rows padded by
+// one 16-byte chunk.
 template <typename T, int FLAGS, int BM, int BN, int BK>
 struct Smem {
   static constexpr int VE = Elem<T>::VE;
@@ -270,12 +279,153 @@ struct Smem {
   static constexpr int NAS = (FLAGS & G_AD) ? 2 : 1;
   static constexpr int NBS = (FLAGS & G_BD) ? 2 : 1;
   static constexpr int STAGE = (NAS * BM + NBS * BN) * LDL;  // elements
-  static constexpr int NS = (FLAGS & (G_AD | G_BD)) ? 2 : 1;  // staged accumulators
   static constexpr int PIPE_BYTES = 2 * STAGE * (int)sizeof(T);
-  static constexpr int EPI_BYTES = NS * (BM / 2) * Stage<BN>::SLD * 4;
+  static constexpr int EPI_BYTES = EpiSmem<FLAGS, BM, BN, 2>::BYTES;
   static constexpr int BYTES = PIPE_BYTES > EPI_BYTES ? PIPE_BYTES : EPI_BYTES;
 };
 
+// Tile order.  Workgroup ids are dispatched round-robin over the 8 XCDs; give
+// each XCD a contiguous range of tiles, then walk tiles in groups of 8 tile
+// rows so that neighbouring tiles share A and B panels in that XCD's L2.
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tiles_n = (N + BN - 1) / BN;
+  const int nt = tiles_m * tiles_n;
+  int pid = blockIdx.x;
+  if ((nt & 7) == 0) pid = (pid & 7) * (nt >> 3) + (pid >> 3);
+  constexpr int GM = 8;
+  const int group = pid / (GM * tiles_n);
+  const int first_m = group * GM;
+  const int gsz = min(tiles_m - first_m, GM);
+  const int within = pid - group * GM * tiles_n;
+  m0 = (first_m + within % gsz) * BM;
+  n0 = (within / gsz) * BN;
+}
+
+// Position of element (row, col) in the epilogue staging buffer: rows padded
+// to SLD floats, and 4-float column groups XOR-swizzled by row bits 4..5 so
+// that the transposed walk (16 lanes reading one column at rows 4 t + k) hits
+// 16 different banks; 4-float groups stay contiguous for the row walk.
+template <int SLD>
+__device__ __forceinline__ int stage_idx(int row, int col) {
+  return row * SLD + (col ^ (((row >> 4) & 3) << 2));
+}
+
+// Accumulators of the four computing waves (2 x 2 arrangement, each TM x TN
+// tiles of 16 x 16) -> LDS staging buffer, rows [row0, row0 + RP) of the tile.
+// C layout of a 16x16 MFMA tile: lane holds rows 4*(lane/16) + 0..3 of column
+// lane%16.  Called by the waves whose rows fall in the slab.
+template <int FLAGS, int BM, int BN, int RP>
+__device__ __forceinline__ void stage_tile(const f32x4 (&acc1)[BM / 32][BN / 32],
+                                           const f32x4 (&acc2)[BM / 32][BN / 32], float* S1,
+                                           float* S2, int rbase) {
+  constexpr bool HC1 = (FLAGS & G_C1) != 0;
+  constexpr bool HC2 = (FLAGS & (G_AD | G_BD)) != 0;
+  constexpr int WTN = BN / 2;
+  constexpr int TM = BM / 32, TN = BN / 32;
+  constexpr int SLD = Stage<BN>::SLD;
+  const int lane = threadIdx.x & 63;
+  const int wn = (threadIdx.x >> 6) & 1;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int c = wn * WTN + j * 16 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int rl = rbase + i * 16 + (lane >> 4) * 4 + r;
+        S1[stage_idx<SLD>(rl, c)] = HC1 ? acc1[i][j][r] : 0.0f;
+        if constexpr (HC2) S2[stage_idx<SLD>(rl, c)] = acc2[i][j][r];
+      }
+    }
+}
+
+// Epilogue walk over a staged slab of RP rows (tile rows mr0 .. mr0 + RP - 1) by
+// all NT threads: a row-major walk with 16-byte accesses calls epi.row, then
+// (for outputs also needed transposed) a walk down the columns writes
+// contiguous runs of the transpose.  Ends with the LDS free again.
+template <int FLAGS, int BN, int RP, int NT, class Epi>
+__device__ __forceinline__ void walk_tile(float* S1, float* S2, int mr0, int n0, int bz,
+                                          const Epi& epi) {
+  constexpr bool HC2 = (FLAGS & (G_AD | G_BD)) != 0;
+  constexpr int SLD = Stage<BN>::SLD;
+  const int tid = threadIdx.x;
+  const int nT = epi.n_trans();
+  {
+    constexpr int TPR = BN / 4;        // threads per row, 4 columns each
+    constexpr int RPI = NT / TPR;      // rows per iteration
+    const int c = (tid % TPR) * 4;
+    const int n = n0 + c;
+    for (int rr = tid / TPR; rr < RP; rr += RPI) {
+      const int m = mr0 + rr;
+      if (m < epi.M && n < epi.N) {
+        float c1[4], c2[4], t1[4], t2[4];
+        const int si = stage_idx<SLD>(rr, c);
+        const float4 x1 = *reinterpret_cast<const float4*>(S1 + si);
+        c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
+        if constexpr (HC2) {
+          const float4 x2 = *reinterpret_cast<const float4*>(S2 + si);
+          c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
+        } else {
+          c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
+        }
+        epi.row(bz, m, n, min(4, epi.N - n), c1, c2, t1, t2);
+        if (nT > 0) *reinterpret_cast<float4*>(S1 + si) = make_float4(t1[0], t1[1], t1[2], t1[3]);
+        if (nT > 1) *reinterpret_cast<float4*>(S2 + si) = make_float4(t2[0], t2[1], t2[2], t2[3]);
+      }
+    }
+  }
+  if (nT > 0) {
+    __syncthreads();
+    constexpr int TPC = RP / 4;        // threads per transposed row, 4 rows of C each
+    constexpr int CPI = NT / TPC;
+    const int r4 = (tid % TPC) * 4;
+    const int m = mr0 + r4;
+    for (int cc = tid / TPC; cc < BN; cc += CPI) {
+      const int n = n0 + cc;
+      if (n < epi.N && m < epi.M) {
+        const int cnt = min(4, epi.M - m);
+        float v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = S1[stage_idx<SLD>(r4 + k, cc)];
+        epi.trans(0, bz, n, m, cnt, v);
+        if (nT > 1) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = S2[stage_idx<SLD>(r4 + k, cc)];
+          epi.trans(1, bz, n, m, cnt, v);
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Two-slab epilogue of the 256-thread kernels: one wave row (BM / 2 rows) at a
+// time in half the LDS.  The caller guarantees that no wave still reads or
+// writes smem.
+template <int FLAGS, int BM, int BN, class Epi>
+__device__ __forceinline__ void run_epilogue(const f32x4 (&acc1)[BM / 32][BN / 32],
+                                             const f32x4 (&acc2)[BM / 32][BN / 32],
+                                             char* smem_raw, int m0, int n0, int bz,
+                                             const Epi& epi) {
+  constexpr int RP = BM / 2;
+  float* S1 = reinterpret_cast<float*>(smem_raw);
+  float* S2 = S1 + RP * Stage<BN>::SLD;
+  const int wm = threadIdx.x >> 7;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (wm == pass) stage_tile<FLAGS, BM, BN, RP>(acc1, acc2, S1, S2, 0);
+    __syncthreads();
+    walk_tile<FLAGS, BN, RP, 256>(S1, S2, m0 + pass * RP, n0, bz, epi);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Main loop, register-staged: each thread loads its 16-byte chunks of the next
+// k step into registers while the current one is multiplied, then stores them
+// to the other LDS buffer.  Handles any K, leading dimension and element type.
+// ------------------------------------------------------------------------------------
 template <typename T, int FLAGS, int BM, int BN, int BK, class Epi>
 __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   typedef Smem<T, FLAGS, BM, BN, BK> SM;
@@ -284,7 +434,6 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   constexpr bool HC1 = (FLAGS & G_C1) != 0;
   constexpr bool HAD = (FLAGS & G_AD) != 0;
   constexpr bool HBD = (FLAGS & G_BD) != 0;
-  constexpr bool HC2 = HAD || HBD;
   constexpr int NAS = SM::NAS;
   constexpr int NBS = SM::NBS;
   constexpr int STAGE = SM::STAGE;
@@ -304,23 +453,8 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-
-  // Tile order.  Workgroup ids are dispatched round-robin over the 8 XCDs; give
-  // each XCD a contiguous range of tiles, then walk tiles in groups of 8 tile
-  // rows so that neighbouring tiles share A and B panels in that XCD's L2.
-  const int tiles_m = (op.M + BM - 1) / BM;
-  const int tiles_n = (op.N + BN - 1) / BN;
-  const int nt = tiles_m * tiles_n;
-  int pid = blockIdx.x;
-  if ((nt & 7) == 0) pid = (pid & 7) * (nt >> 3) + (pid >> 3);
-  constexpr int GM = 8;
-  const int group = pid / (GM * tiles_n);
-  const int first_m = group * GM;
-  const int gsz = min(tiles_m - first_m, GM);
-  const int within = pid - group * GM * tiles_n;
-  const int tm = first_m + within % gsz;
-  const int tn = within / gsz;
-  const int m0 = tm * BM, n0 = tn * BN;
+  int m0, n0;
+  tile_origin<BM, BN>(op.M, op.N, m0, n0);
   const int bz = blockIdx.y;
   if (bz > 0) {
     op.A += bz * op.sA;
@@ -418,91 +552,339 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
     if (kt + 1 < nk) sstore(buf ^ 1);
     __syncthreads();
   }
+  run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem_raw, m0, n0, bz, epi);
+}
 
-  // ---- staged epilogue ----
-  // C layout of a 16x16 MFMA tile: lane holds rows 4*(lane/16) + 0..3 of
-  // column lane%16.
-  constexpr int SLD = Stage<BN>::SLD;
-  constexpr int RP = WTM;               // rows per pass
-  float* S1 = reinterpret_cast<float*>(smem_raw);
-  float* S2 = S1 + RP * SLD;
-  const int nT = epi.n_trans();
+// ------------------------------------------------------------------------------------
+// Main loop, direct to LDS (bfloat16).  Tiles go from HBM to LDS with
+// buffer_load_dwordx4 ... lds, which needs no registers, so NST k steps are in
+// flight at once (NST - 1 loading while one is multiplied).  Each load
+// instruction fills 1 KB of LDS, lane l at byte 16 l; a lane picks which
+// 16-byte chunk of which row it fetches so that the tile lands row-major with
+// the chunk index XOR-swizzled by the row (conflict-free fragment reads, no
+// padding).  Rows past M or N and chunks past K read zero: the buffer
+// descriptor's range check turns an offset at or above num_records into a zero
+// load, and such lanes are given the offset 2^31.  Requires K, the leading
+// dimensions and the batch strides to be multiples of 8 elements, 16-byte
+// aligned operands, and each operand to span less than 2^31 bytes.
+// ------------------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Chunk swizzle by row.  For the fragment reads below (16 consecutive rows, one
+// logical chunk per 16 lanes) both forms were measured free of LDS bank
+// conflicts on gfx950 with the SQ_LDS_BANK_CONFLICT counter, while mixing
+// row bit 3 into either leaves half of the LDS cycles in conflict.
+template <int CPR>
+__device__ __forceinline__ int chunk_swizzle(int r) {
+  static_assert(CPR == 8 || CPR == 4, "16-byte chunks per row");
+  if constexpr (CPR == 8) return r & 7;    // 128-byte rows
+  else return (r >> 1) & 3;                // 64-byte rows
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0), leaving expcnt free (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+// Workgroup barrier that orders LDS accesses only: the explicit waitcnt before
+// it decides which global-to-LDS loads have landed.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int FLAGS, int BM, int BN, int BK, int NST, int NPASS>
+struct DmaSmem {
+  static constexpr bool LA = (FLAGS & (G_C1 | G_BD)) != 0;  // tiles loaded
+  static constexpr bool LAD = (FLAGS & G_AD) != 0;
+  static constexpr bool LB = (FLAGS & (G_C1 | G_AD)) != 0;
+  static constexpr bool LBD = (FLAGS & G_BD) != 0;
+  static constexpr int ROWB = BK * 2;                         // bytes per tile row
+  static constexpr int OFF_AD = (LA ? BM : 0) * ROWB;
+  static constexpr int OFF_B = OFF_AD + (LAD ? BM : 0) * ROWB;
+  static constexpr int OFF_BD = OFF_B + (LB ? BN : 0) * ROWB;
+  static constexpr int STAGE_BYTES = OFF_BD + (LBD ? BN : 0) * ROWB;
+  static constexpr int CPR = BK / 8;
+  static constexpr int LPW = STAGE_BYTES / 1024 / 4;         // load instructions per wave
+  static constexpr int PIPE_BYTES = NST * STAGE_BYTES;
+  static constexpr int EPI_BYTES = EpiSmem<FLAGS, BM, BN, NPASS>::BYTES;
+  static constexpr int BYTES = PIPE_BYTES > EPI_BYTES ? PIPE_BYTES : EPI_BYTES;
+};
+
+// Per-lane state for one operand tile: which rows this lane fetches.
+template <int ROWS, int CPR>
+struct DmaTile {
+  static constexpr int RPB = 64 / CPR;         // tile rows per 1 KB load
+  static constexpr int BPW = ROWS / RPB / 4;   // loads per wave per k step
+  static_assert(BPW >= 1 && ROWS % (4 * RPB) == 0, "tile rows");
+  __amdgpu_buffer_rsrc_t rsrc;
+  unsigned row_off[BPW];   // byte offset of the lane's row plus its chunk, or 2^31
+  int kq;                  // element offset of the lane's chunk within a k step
+
+  // w: index 0..3 of this wave among the four that load the tile
+  __device__ __forceinline__ void init(const bf16_t* base, int rows, int ld, int K, int row0,
+                                       int w) {
+    const unsigned bytes = rows > 0 ? (unsigned)(((long)(rows - 1) * ld + K) * 2) : 0u;
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), 0, (int)bytes, 0x00020000);
+    const int lane = threadIdx.x & 63;
+    const int p = lane % CPR;
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    if (wm == pass) {
+    for (int c = 0; c < BPW; ++c) {
+      const int r = (c * 4 + w) * RPB + lane / CPR;
+      const int q = p ^ chunk_swizzle<CPR>(r);
+      const int gr = row0 + r;
+      row_off[c] = gr < rows ? (unsigned)((long)gr * ld + q * 8) * 2u : 0x80000000u;
+      kq = q * 8;   // the same for every c: the swizzle reads row bits that c does not change
+    }
+  }
+  // Issue the loads of k step k0 into the tile at dst (LDS).
+  __device__ __forceinline__ void issue(char* dst, int k0, int K, int w) const {
+    const bool kin = k0 + kq < K;
+#pragma unroll
+    for (int c = 0; c < BPW; ++c) {
+      const unsigned off = (kin && row_off[c] != 0x80000000u) ? row_off[c] + (unsigned)k0 * 2u
+                                                             : 0x80000000u;
+      char* d = dst + (c * 4 + w) * RPB * (CPR * 16);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)d, 16, off, 0, 0, 0);
+    }
+  }
+};
+
+template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
+__global__ void __launch_bounds__(256) gemm_nt_dma(GemmOperands<bf16_t> op, Epi epi) {
+  typedef DmaSmem<FLAGS, BM, BN, BK, NST, 2> SM;
+  constexpr bool HC1 = (FLAGS & G_C1) != 0;
+  constexpr bool HAD = (FLAGS & G_AD) != 0;
+  constexpr bool HBD = (FLAGS & G_BD) != 0;
+  constexpr int CPR = SM::CPR;
+  constexpr int ROWB = SM::ROWB;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  constexpr int NCH = CPR / 4;                 // 32-deep MFMA steps per k step
+  static_assert(NST >= 2 && SM::LPW * (NST - 2) < 64, "pipeline depth");
+
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  int m0, n0;
+  tile_origin<BM, BN>(op.M, op.N, m0, n0);
+  const int bz = blockIdx.y;
+  const int K = op.K;
+
+  DmaTile<BM, CPR> tA, tAd;
+  DmaTile<BN, CPR> tB, tBd;
+  if constexpr (SM::LA) tA.init(op.A + bz * op.sA, op.M, op.lda, K, m0, wave);
+  if constexpr (SM::LAD) tAd.init(op.Ad + bz * op.sA, op.M, op.lda, K, m0, wave);
+  if constexpr (SM::LB) tB.init(op.B + bz * op.sB, op.N, op.ldb, K, n0, wave);
+  if constexpr (SM::LBD) tBd.init(op.Bd + bz * op.sB, op.N, op.ldb, K, n0, wave);
+
+  auto issue = [&](int kt) {
+    char* st = smem + (kt % NST) * SM::STAGE_BYTES;
+    const int k0 = kt * BK;
+    if constexpr (SM::LA) tA.issue(st, k0, K, wave);
+    if constexpr (SM::LAD) tAd.issue(st + SM::OFF_AD, k0, K, wave);
+    if constexpr (SM::LB) tB.issue(st + SM::OFF_B, k0, K, wave);
+    if constexpr (SM::LBD) tBd.issue(st + SM::OFF_BD, k0, K, wave);
+  };
+
+  f32x4 acc1[TM][TN], acc2[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      acc1[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  // Fragment addressing: lane reads row (lane % 16) of a 16-row slab, logical
+  // chunk lane / 16 + 4 c, stored at chunk (lane / 16 + 4 c) ^ swizzle(row).
+  const int sw = chunk_swizzle<CPR>(lane & 15);
+  int foff[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) foff[c] = (lane & 15) * ROWB + (((lane >> 4) + 4 * c) ^ sw) * 16;
+
+  const int nk = (K + BK - 1) / BK;
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s) issue(s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // k step kt has landed once at most the loads of the NST - 2 later steps
+    // are outstanding; the barrier also retires every read of the stage that
+    // the next issue overwrites (read in step kt - 1).
+    wait_vm_lgkm<SM::LPW * (NST - 2)>();
+    lds_barrier();
+    issue(kt + NST - 1);   // past the last step: zero loads into a dead stage
+    const char* st = smem + (kt % NST) * SM::STAGE_BYTES;
+    const char* As = st;
+    const char* Ads = st + SM::OFF_AD;
+    const char* Bs = st + SM::OFF_B;
+    const char* Bds = st + SM::OFF_BD;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      bf16x8 a[TM], ad[TM], b[TN], bd[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r0 = (wm * WTM + i * 16) * ROWB + foff[c];
+        if constexpr (SM::LA) a[i] = *reinterpret_cast<const bf16x8*>(As + r0);
+        if constexpr (HAD) ad[i] = *reinterpret_cast<const bf16x8*>(Ads + r0);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r0 = (wn * WTN + j * 16) * ROWB + foff[c];
+        if constexpr (SM::LB) b[j] = *reinterpret_cast<const bf16x8*>(Bs + r0);
+        if constexpr (HBD) bd[j] = *reinterpret_cast<const bf16x8*>(Bds + r0);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const int c = wn * WTN + j * 16 + (lane & 15);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int rl = i * 16 + (lane >> 4) * 4 + r;
-            S1[rl * SLD + c] = HC1 ? acc1[i][j][r] : 0.0f;
-            if constexpr (HC2) S2[rl * SLD + c] = acc2[i][j][r];
-          }
+          if constexpr (HC1) mma(acc1[i][j], a[i], b[j]);
+          if constexpr (HAD) mma(acc2[i][j], ad[i], b[j]);
+          if constexpr (HBD) mma(acc2[i][j], a[i], bd[j]);
         }
     }
-    __syncthreads();
-    {
-      constexpr int TPR = BN / 4;        // threads per row, 4 columns each
-      constexpr int RPI = 256 / TPR;     // rows per iteration
-      const int c = (tid % TPR) * 4;
-      const int n = n0 + c;
-      for (int rr = tid / TPR; rr < RP; rr += RPI) {
-        const int m = m0 + pass * RP + rr;
-        if (m < epi.M && n < epi.N) {
-          float c1[4], c2[4], t1[4], t2[4];
-          const float4 x1 = *reinterpret_cast<const float4*>(S1 + rr * SLD + c);
-          c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
-          if constexpr (HC2) {
-            const float4 x2 = *reinterpret_cast<const float4*>(S2 + rr * SLD + c);
-            c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
-          } else {
-            c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
-          }
-          epi.row(bz, m, n, min(4, epi.N - n), c1, c2, t1, t2);
-          if (nT > 0) *reinterpret_cast<float4*>(S1 + rr * SLD + c) = make_float4(t1[0], t1[1], t1[2], t1[3]);
-          if (nT > 1) *reinterpret_cast<float4*>(S2 + rr * SLD + c) = make_float4(t2[0], t2[1], t2[2], t2[3]);
-        }
-      }
-    }
-    if (nT > 0) {
-      __syncthreads();
-      constexpr int TPC = RP / 4;        // threads per transposed row, 4 rows of C each
-      constexpr int CPI = 256 / TPC;
-      const int r4 = (tid % TPC) * 4;
-      const int m = m0 + pass * RP + r4;
-      for (int cc = tid / TPC; cc < BN; cc += CPI) {
-        const int n = n0 + cc;
-        if (n < epi.N && m < epi.M) {
-          const int cnt = min(4, epi.M - m);
-          float v[4];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) v[k] = S1[(r4 + k) * SLD + cc];
-          epi.trans(0, bz, n, m, cnt, v);
-          if (nT > 1) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = S2[(r4 + k) * SLD + cc];
-            epi.trans(1, bz, n, m, cnt, v);
-          }
-        }
-      }
-    }
-    __syncthreads();
   }
+  // the trailing zero loads must land before the epilogue reuses the LDS
+  wait_vm_lgkm<0>();
+  lds_barrier();
+  run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem, m0, n0, bz, epi);
+}
+
+// ------------------------------------------------------------------------------------
+// Main loop, warp-specialised (bfloat16, 512 threads).  A wave that issues a
+// global load stalls until the compute unit's load unit takes it (about 16
+// cycles per 1 KB load, one unit per compute unit), and in-order issue holds
+// back its MFMAs meanwhile.  Here waves 4..7 only issue the direct-to-LDS loads
+// and waves 0..3 only read fragments and multiply, so each SIMD has one wave
+// that keeps its matrix core busy while the other waits on the load unit.  Tile,
+// LDS layout, zero fill and pipeline are those of gemm_nt_dma; the eight waves
+// meet at one barrier per k step and all of them walk the epilogue.
+// ------------------------------------------------------------------------------------
+template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
+__global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi epi) {
+  typedef DmaSmem<FLAGS, BM, BN, BK, NST, 1> SM;
+  constexpr bool HC1 = (FLAGS & G_C1) != 0;
+  constexpr bool HAD = (FLAGS & G_AD) != 0;
+  constexpr bool HBD = (FLAGS & G_BD) != 0;
+  constexpr int CPR = SM::CPR;
+  constexpr int ROWB = SM::ROWB;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  constexpr int NCH = CPR / 4;
+  static_assert(NST >= 2 && SM::LPW * (NST - 2) < 64, "pipeline depth");
+
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
+  float* S1 = reinterpret_cast<float*>(smem);
+  float* S2 = S1 + BM * Stage<BN>::SLD;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int m0, n0;
+  tile_origin<BM, BN>(op.M, op.N, m0, n0);
+  const int bz = blockIdx.y;
+  const int K = op.K;
+  const int nk = (K + BK - 1) / BK;
+
+  // The two roles run separate loops, so their registers do not add up; both
+  // pass the same barriers: one per k step, one when the LDS turns into the
+  // staging buffer and one when the staged tile is complete.
+  if (wave >= 4) {
+    const int pw = wave - 4;
+    DmaTile<BM, CPR> tA, tAd;
+    DmaTile<BN, CPR> tB, tBd;
+    if constexpr (SM::LA) tA.init(op.A + bz * op.sA, op.M, op.lda, K, m0, pw);
+    if constexpr (SM::LAD) tAd.init(op.Ad + bz * op.sA, op.M, op.lda, K, m0, pw);
+    if constexpr (SM::LB) tB.init(op.B + bz * op.sB, op.N, op.ldb, K, n0, pw);
+    if constexpr (SM::LBD) tBd.init(op.Bd + bz * op.sB, op.N, op.ldb, K, n0, pw);
+    auto issue = [&](int kt) {
+      char* st = smem + (kt % NST) * SM::STAGE_BYTES;
+      const int k0 = kt * BK;
+      if constexpr (SM::LA) tA.issue(st, k0, K, pw);
+      if constexpr (SM::LAD) tAd.issue(st + SM::OFF_AD, k0, K, pw);
+      if constexpr (SM::LB) tB.issue(st + SM::OFF_B, k0, K, pw);
+      if constexpr (SM::LBD) tBd.issue(st + SM::OFF_BD, k0, K, pw);
+    };
+#pragma unroll
+    for (int s = 0; s < NST - 1; ++s) issue(s);
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_vm_lgkm<SM::LPW * (NST - 2)>();   // this wave's loads of step kt have landed
+      lds_barrier();                         // ... and every other wave's
+      issue(kt + NST - 1);                   // past the last step: zero loads into a dead stage
+    }
+    wait_vm_lgkm<0>();
+    lds_barrier();
+    lds_barrier();
+  } else {
+    const int wm = wave >> 1, wn = wave & 1;
+    f32x4 acc1[TM][TN], acc2[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        acc1[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    // lane reads row (lane % 16) of a 16-row slab, logical chunk lane / 16 + 4 c
+    const int sw = chunk_swizzle<CPR>(lane & 15);
+    int foff[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) foff[c] = (lane & 15) * ROWB + (((lane >> 4) + 4 * c) ^ sw) * 16;
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_vm_lgkm<0>();   // reads of step kt - 1 done: its stage may be refilled
+      lds_barrier();       // every load of step kt has landed
+      const char* st = smem + (kt % NST) * SM::STAGE_BYTES;
+      const char* As = st;
+      const char* Ads = st + SM::OFF_AD;
+      const char* Bs = st + SM::OFF_B;
+      const char* Bds = st + SM::OFF_BD;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        bf16x8 a[TM], ad[TM], b[TN], bd[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r0 = (wm * WTM + i * 16) * ROWB + foff[c];
+          if constexpr (SM::LA) a[i] = *reinterpret_cast<const bf16x8*>(As + r0);
+          if constexpr (HAD) ad[i] = *reinterpret_cast<const bf16x8*>(Ads + r0);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r0 = (wn * WTN + j * 16) * ROWB + foff[c];
+          if constexpr (SM::LB) b[j] = *reinterpret_cast<const bf16x8*>(Bs + r0);
+          if constexpr (HBD) bd[j] = *reinterpret_cast<const bf16x8*>(Bds + r0);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            if constexpr (HC1) mma(acc1[i][j], a[i], b[j]);
+            if constexpr (HAD) mma(acc2[i][j], ad[i], b[j]);
+            if constexpr (HBD) mma(acc2[i][j], a[i], bd[j]);
+          }
+      }
+    }
+    wait_vm_lgkm<0>();
+    lds_barrier();         // the trailing zero loads have landed: LDS is free
+    stage_tile<FLAGS, BM, BN, BM>(acc1, acc2, S1, S2, wm * WTM);
+    wait_vm_lgkm<0>();     // the staging writes are complete before other waves read them
+    lds_barrier();
+  }
+  walk_tile<FLAGS, BN, BM, 512>(S1, S2, m0, n0, bz, epi);
 }
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// k depth per LDS stage: 64 keeps more MFMA work in flight per prefetch; the dual
-// backward-weight kernels (short k = batch rows, heavy epilogue) use 32 so that
-// their double-buffered tiles stay at 80 KB of LDS.
+// k depth per LDS stage of the register-staged loop: 64 keeps more MFMA work in
+// flight per prefetch; the dual backward-weight kernels (short k = batch rows,
+// heavy epilogue) use 32 so that their double-buffered tiles stay at 80 KB.
 template <int FLAGS, class Epi>
 struct KDepth {
   static constexpr int value = 64;
 };
-template <typename T> struct ParamOp;
 template <typename T>
 struct KDepth<G_C1 | G_AD | G_BD, ParamOp<T>> {
   static constexpr int value = 32;
@@ -520,9 +902,59 @@ struct KDepth<G_BD, ParamOp<T>> {
   static constexpr int value = 32;
 };
 
+// Direct-to-LDS pipeline shape: k depth and stages, sized to about 128 KB of
+// LDS.  One operand pair: 64 deep x 4 stages; three or four operand tiles:
+// 32 deep x 4 stages.
+template <int FLAGS, class Epi>
+struct DmaShape {
+  static constexpr int NOPS = ((FLAGS & (G_C1 | G_BD)) ? 1 : 0) + ((FLAGS & G_AD) ? 1 : 0) +
+                              ((FLAGS & (G_C1 | G_AD)) ? 1 : 0) + ((FLAGS & G_BD) ? 1 : 0);
+  static constexpr int BK = NOPS <= 2 ? 64 : 32;
+  static constexpr int NST = 4;
+  static constexpr bool ENABLED = true;
+  static constexpr bool WS = true;   // warp-specialised 512-thread kernel
+};
+// Backward-weight products with the parameter epilogue: many tiles over a short
+// k (the batch rows) and a heavy epilogue.  Two stages keep a workgroup within
+// 80 KB of LDS, so two of them share a compute unit and one's epilogue overlaps
+// the other's main loop.
+template <int FLAGS, typename T>
+struct DmaShape<FLAGS, ParamOp<T>> : DmaShape<FLAGS, StoreOp> {
+  static constexpr int NST = 2;
+  static constexpr bool WS = false;
+};
+
+template <typename T>
+bool dma_operand_ok(const T* p, int rows, int ld, int K, long stride) {
+  if (!p) return true;
+  if ((reinterpret_cast<uintptr_t>(p) & 15) || (ld & 7) || (stride & 7)) return false;
+  return rows <= 0 || ((long)(rows - 1) * ld + K) * (long)sizeof(T) < (1L << 31);
+}
+
+template <typename T>
+bool dma_ok(const GemmOperands<T>& op) {
+  if (sizeof(T) != 2 || (op.K & 7)) return false;
+  return dma_operand_ok(op.A, op.M, op.lda, op.K, op.sA) &&
+         dma_operand_ok(op.Ad, op.M, op.lda, op.K, op.sA) &&
+         dma_operand_ok(op.B, op.N, op.ldb, op.K, op.sB) &&
+         dma_operand_ok(op.Bd, op.N, op.ldb, op.K, op.sB);
+}
+
 template <typename T, int FLAGS, int BM, int BN, class Epi>
 hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   const int tiles = cdiv(op.M, BM) * cdiv(op.N, BN);
+  if constexpr (sizeof(T) == 2) {
+    typedef DmaShape<FLAGS, Epi> DS;
+    if (DS::ENABLED && dma_ok(op)) {
+      if constexpr (DS::WS)
+        hipLaunchKernelGGL((gemm_nt_ws<FLAGS, BM, BN, DS::BK, DS::NST, Epi>),
+                           dim3(tiles, op.batch), dim3(512), 0, s, op, epi);
+      else
+        hipLaunchKernelGGL((gemm_nt_dma<FLAGS, BM, BN, DS::BK, DS::NST, Epi>),
+                           dim3(tiles, op.batch), dim3(256), 0, s, op, epi);
+      return hipGetLastError();
+    }
+  }
   constexpr int BK = KDepth<FLAGS, Epi>::value;
   hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi>), dim3(tiles, op.batch), dim3(256), 0, s,
                      op, epi);

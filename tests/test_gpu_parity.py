@@ -54,7 +54,7 @@ def run_meta(cfg, inp):
 
 
 META_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small",
-              "c3_small", "c5_mid", "c1_linreg", "c2_mlp_tanh_lossweights"]
+              "c3_small", "c5_mid", "c5_r8", "c1_linreg", "c2_mlp_tanh_lossweights"]
 
 
 def cfg_of(name):
@@ -81,7 +81,8 @@ def test_meta_grad_parity(name):
     assert peak > 0
 
 
-INNER_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_small", "c3_small"]
+INNER_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_small", "c3_small", "c5_r8",
+               "c5_mid_r8"]
 
 
 @pytest.mark.parametrize("name", INNER_CASES)
@@ -122,7 +123,7 @@ def test_inner_step_parity(name):
 
 
 HVP_CASES = ["c1_small", "c2_small", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c3_small",
-             "c5_mid"]
+             "c5_mid", "c5_r8", "c5_mid_r8"]
 
 
 @pytest.mark.parametrize("name", HVP_CASES)

@@ -126,6 +126,12 @@ SMALL: Dict[str, Config] = {
     # large enough that every layer's products use the 128 x 128 bf16 tiles
     "c5_mid": C5.with_(name="c5_mid", cfg_id=109, widths=(2048, 2048, 2048, 64), rows=2048,
                        val_rows=512, T=2),
+    # every dimension a multiple of 8 but not of the tile sizes: ragged row,
+    # column and k tails on the direct-to-LDS GEMM path (64 and 128 tiles)
+    "c5_r8": C5.with_(name="c5_r8", cfg_id=110, widths=(200, 264, 136, 40), rows=200,
+                      val_rows=136, T=3),
+    "c5_mid_r8": C5.with_(name="c5_mid_r8", cfg_id=111, widths=(1544, 2056, 1032, 40), rows=1544,
+                          val_rows=520, T=2),
     "c4_small": C4.with_(name="c4_small", cfg_id=104, d_model=64, n_heads=4, d_ff=128, vocab=97,
                          seq=24, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2),
 }
