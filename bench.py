@@ -63,6 +63,146 @@ def algorithmic_flops(cfg: W.Config, T: int):
     return f
 
 
+def algorithmic_bytes(cfg: W.Config, T: int):
+    """HBM bytes per kernel class per meta-gradient that the method must move
+    with this design (SGD with per-parameter log learning rates; bf16 operands
+    in both layouts, float32 parameter streams): every operand tile read once,
+    every output written once, no re-reads.  None for classes not modelled."""
+    if cfg.optimizer != W.OPT_SGD or cfg.meta != W.META_LOGLR_PER_PARAM:
+        return [None] * len(KERNEL_CLASSES)
+    R, Rv, L = cfg.rows, cfg.val_rows, cfg.n_layers
+    b = [0.0] * len(KERNEL_CLASSES)
+    for l in range(L):
+        i, o = cfg.widths[l], cfg.widths[l + 1]
+        P = i * o
+        last = l == L - 1
+        for rows in [R] * T + [Rv]:
+            # forward: A and W^T read; z (float32) written, and for hidden layers
+            # the next operand in both bf16 layouts
+            b[0] += 2 * rows * i + 2 * P + 4 * rows * o + (0 if last else 4 * rows * o)
+            if l > 0:   # backward-data: dZ, W, z_{l-1} read; dZ_{l-1} written in both layouts
+                b[1] += 2 * rows * o + 2 * P + 4 * rows * i + 4 * rows * i
+        # backward-weight with the update (T steps): A^T, dZ^T read; theta, eta
+        # read, theta' written, new operands W, W^T written
+        b[2] += T * (2 * R * i + 2 * R * o + 16 * P)
+        # validation seed: theta-bar written, eta read, tangent W, W^T written
+        b[2] += 2 * Rv * i + 2 * Rv * o + 12 * P
+        for t in range(T):
+            first, last_rev = t == 0, t == T - 1      # reverse order: first = step T-1
+            # dual forward: A, A' (not layer 0), W^T, W'^T read; z, z' written,
+            # hidden layers write both operands in both layouts
+            b[3] += (2 if l == 0 else 4) * R * i + 4 * P + 8 * R * o + (0 if last else 8 * R * o)
+            if l > 0:   # dual backward-data: dZ, dZ', W, W', z, z' read; outputs in both layouts
+                b[4] += 4 * R * o + 4 * P + 8 * R * i + 8 * R * i
+            # dual backward-weight with the reverse epilogue: operands read once;
+            # theta-bar read and written, eta read, eta-bar read (not on the first
+            # reverse step) and written, next tangent W, W^T (not after the last)
+            par = (8 + 4 + (0 if first else 4) + 4 + (0 if last_rev else 4)) * P
+            ops = 2 * R * o * 2 + (2 if l == 0 else 4) * R * i
+            b[5 if l == 0 else 8] += par + ops
+    return b
+
+
+# Kernel instantiation that makes up each kernel class in the c5 run (bf16,
+# 128 x 128 tiles on the direct-to-LDS path), for matching counter records.
+CLASS_KERNEL = {
+    "dual_bwd_weight_gemm_reverse": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ParamOp",
+    "bwd_weight_gemm_update": "gemm_nt_ws<1, 128, 128, 64, 4, mfmg::(anonymous namespace)::ParamOp",
+    "dual_fwd_gemm": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ActFwdOp",
+    "dual_bwd_data_gemm": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ActBwdOp",
+}
+KERNEL_SOURCES = ["paper_2505_00793_amd/csrc/gemm.hip", "paper_2505_00793_amd/csrc/param_epi.h",
+                  "paper_2505_00793_amd/csrc/kernels.h", "paper_2505_00793_amd/csrc/common.h"]
+
+
+def counters_file(cls: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{cls}_c5_mlp8x4096_T8_hbm_counters.md")
+
+
+def kernel_sources_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(cls: str):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary of
+    this kernel class, or None if there is none or the kernel sources changed
+    since the counters were taken."""
+    path = counters_file(cls)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    i = text.find("```json")
+    if i < 0:
+        return None
+    rec = json.loads(text[i + 7:text.index("```", i + 7)])
+    if rec.get("kernel_sources_sha256") != kernel_sources_sha():
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
+def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, command: str):
+    """Turns two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per
+    dispatch) of `bench.py --copy-bytes N` into per-launch HBM bytes of one
+    kernel class, each counter scaled by what it reads for the plain N-byte copy."""
+    import csv
+
+    def load(path, counter):
+        per = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            per.setdefault(r["Dispatch_Id"], [r["Kernel_Name"], 0.0])[1] += float(r["Counter_Value"])
+        return list(per.values())
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = load(path, counter)
+        copies = sorted((v for n, v in rows if "copyBuffer" in n), reverse=True)[:3]
+        factor = (copy_bytes / 1024.0) / (sum(copies) / len(copies))
+        ks = [v for n, v in rows if CLASS_KERNEL[cls] in n]
+        out[counter] = {"copy_kib_per_dispatch": round(sum(copies) / len(copies), 1),
+                        "scale": round(factor, 4), "dispatches": len(ks),
+                        "kib_per_dispatch": round(sum(ks) / len(ks), 1),
+                        "bytes_per_launch": sum(ks) / len(ks) * 1024.0 * factor}
+    rec = {"kernel_class": cls, "kernel": CLASS_KERNEL[cls], "copy_bytes": copy_bytes,
+           "fetch": out["FETCH_SIZE"], "write": out["WRITE_SIZE"],
+           "hbm_bytes_per_launch": round(out["FETCH_SIZE"]["bytes_per_launch"]
+                                         + out["WRITE_SIZE"]["bytes_per_launch"]),
+           "kernel_sources_sha256": kernel_sources_sha()}
+    cfg = W.C5
+    T = 8
+    alg = algorithmic_bytes(cfg, T)[KERNEL_CLASSES.index(cls)]
+    launches = {"dual_bwd_weight_gemm_reverse": T * (cfg.n_layers - 1)}.get(cls)
+    body = [f"# HBM traffic counters: `{cls}` (MLP 4096-(4096x7)-1000, batch 1024, T=8, bf16)",
+            "", "Commands (repository root, one MI355X), one counter per pass:", "", "```",
+            command, "```", "",
+            f"Each counter is scaled by its reading for a plain device copy of {copy_bytes} bytes "
+            f"(`__amd_rocclr_copyBuffer`, which reads and writes exactly that many bytes), then "
+            f"averaged over the {out['FETCH_SIZE']['dispatches']} dispatches of "
+            f"`{CLASS_KERNEL[cls]}>`.", "",
+            "| counter | copy reads (KiB) | scale | kernel (KiB/dispatch) | bytes per launch |",
+            "|---|---:|---:|---:|---:|"]
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        o = out[counter]
+        body.append(f"| {counter} | {o['copy_kib_per_dispatch']} | {o['scale']} | "
+                    f"{o['kib_per_dispatch']} | {o['bytes_per_launch'] / 1e6:.1f} MB |")
+    if alg and launches:
+        body += ["", f"Algorithmic bytes per launch (bench.py `algorithmic_bytes`): "
+                 f"{alg / launches / 1e6:.1f} MB; measured / algorithmic = "
+                 f"{rec['hbm_bytes_per_launch'] / (alg / launches):.3f}."]
+    body += ["", "bench.py reads the record below for `roofline.traffic` while the kernel "
+             "sources hash to the same value.", "", "```json", json.dumps(rec, indent=1), "```", ""]
+    path = counters_file(cls)
+    with open(path, "w") as f:
+        f.write("\n".join(body))
+    print(path)
+
+
 def desc_of(cfg: W.Config):
     from paper_2505_00793_amd import _lib as M
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
@@ -111,7 +251,16 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="first run a plain device copy of this many bytes (a known-size "
                          "reference for hardware traffic counters)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the HBM counter summary of --pmc-class from two rocprofv3 "
+                         "--pmc runs (made with --copy-bytes) and exit; no GPU needed")
+    ap.add_argument("--pmc-class", default="dual_bwd_weight_gemm_reverse")
+    ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_bytes or (1 << 30),
+                    args.pmc_class, args.pmc_command)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the meta-gradient path is single-device "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
@@ -158,11 +307,7 @@ def main():
     for _ in range(args.warmup):
         peak = call(T, ws)
     torch.cuda.synchronize()
-    M.mfmg_timing_enable(True)
-    for c in range(len(KERNEL_CLASSES)):
-        M.mfmg_timing_read(c)
     log(f"[bench] timing {args.steps} meta-gradients at T={T}")
-    torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record(stream)
@@ -171,8 +316,18 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    M.mfmg_timing_enable(False)
     ms = start.elapsed_time(stop) / args.steps
+    # Per-kernel durations: a second pass of the same calls with HIP events
+    # recorded around every launch on the library's stream (the events cost a
+    # few percent of a step, so the throughput above is timed without them).
+    log(f"[bench] per-kernel HIP-event pass, {args.steps} meta-gradients")
+    for c in range(len(KERNEL_CLASSES)):
+        M.mfmg_timing_read(c)
+    M.mfmg_timing_enable(True)
+    for _ in range(args.steps):
+        call(T, ws)
+    torch.cuda.synchronize()
+    M.mfmg_timing_enable(False)
     kern = {}
     flops = algorithmic_flops(cfg, T)
     for c, name in enumerate(KERNEL_CLASSES):
@@ -181,14 +336,33 @@ def main():
             kern[name] = {"launches_per_step": n / args.steps, "ms_per_step": tot / args.steps,
                           "tflops": (flops[c] * args.steps / (tot * 1e-3) / 1e12) if flops[c] else None}
     log(f"[bench] {ms:.2f} ms per meta-gradient (wall {wall / args.steps * 1e3:.2f} ms)")
+    nbytes = algorithmic_bytes(cfg, T)
+    for c, name in enumerate(KERNEL_CLASSES):
+        if name in kern:
+            k = kern[name]
+            k["mfma_util"] = round(k["tflops"] / PEAK_BF16_TFLOPS, 4) if k["tflops"] else None
+            k["gb_per_s"] = round(nbytes[c] / (k["ms_per_step"] * 1e-3) / 1e9, 1) if nbytes[c] else None
     dom = max((k for k in kern if kern[k]["tflops"]), key=lambda k: kern[k]["ms_per_step"])
-    achieved = kern[dom]["tflops"]
     c = KERNEL_CLASSES.index(dom)
-    per_launch = flops[c] / kern[dom]["launches_per_step"]
-    roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None, "gflop_per_launch": round(per_launch / 1e9, 3),
-            "us_per_launch": round(kern[dom]["ms_per_step"] / kern[dom]["launches_per_step"] * 1e3, 2)}
+    launches = kern[dom]["launches_per_step"]
+    us = kern[dom]["ms_per_step"] / launches * 1e3
+    flop_launch = flops[c] / launches
+    byte_launch = nbytes[c] / launches if nbytes[c] else None
+    # the bound is whichever floor is higher: flops at the MFMA peak or bytes at the HBM peak
+    t_mfma = flop_launch / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = byte_launch / (PEAK_HBM_GBS * 1e9) if byte_launch else 0.0
+    if t_hbm > t_mfma:
+        achieved = byte_launch / (us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    else:
+        achieved = flop_launch / (us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    roof.update({"traffic": measured_traffic(dom), "algorithmic_bytes_per_launch": byte_launch,
+                 "gflop_per_launch": round(flop_launch / 1e9, 3), "us_per_launch": round(us, 2),
+                 "mfma_frac": round(flop_launch / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                 "floor_us": {"mfma": round(t_mfma * 1e6, 2), "hbm": round(t_hbm * 1e6, 2)}})
     finite = bool(torch.isfinite(d_eta).all().item())
 
     sweep = {}
@@ -231,7 +405,9 @@ def main():
                    "parallelism": "single GPU"},
         "peak_bytes": peak, "static_bytes": sizes.static_bytes,
         "dynamic_bytes": sizes.dynamic_bytes, "memory_vs_T": sweep,
-        "roofline": roof, "kernels": kern, "cpu_baseline": cpu, "d_eta_finite": finite,
+        "roofline": roof, "kernels": kern,
+        "kernel_timing": "HIP events around each launch on the library stream, separate pass of the same calls",
+        "cpu_baseline": cpu, "d_eta_finite": finite,
     }
     print(json.dumps(out))
 

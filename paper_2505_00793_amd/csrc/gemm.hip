@@ -14,9 +14,14 @@
 // weight tile serves the primal and the tangent product.
 //
 // Matrix cores: v_mfma_f32_16x16x32_bf16 (bf16 operands) or
-// v_mfma_f32_16x16x4_f32 (float32 operands), 64-lane wavefronts, 4 waves per
-// workgroup in a 2 x 2 arrangement, double-buffered LDS, one barrier per
-// 32-deep k step.
+// v_mfma_f32_16x16x4_f32 (float32 operands), 64-lane wavefronts, four
+// computing waves per workgroup in a 2 x 2 arrangement.  Two main loops:
+//   gemm_nt_ws  bf16 operands with k, leading dimensions and strides multiples
+//               of 8: a 4-stage LDS ring filled by buffer_load ... lds from
+//               four loader waves while four waves multiply (512 threads);
+//   gemm_nt     everything else (float32, ragged k): register-staged,
+//               double-buffered LDS, 256 threads.
+// Both end in the same staged epilogue.
 #include "kernels.h"
 #include "param_epi.h"
 
@@ -79,6 +84,8 @@ template <typename T>
 struct ActFwdOp {
   EpiActFwd<T> e;
   int M, N;
+  static constexpr bool PRELOAD = false;
+  typedef int In;
   __device__ int n_trans() const { return e.last ? 0 : (e.dual ? 2 : 1); }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
@@ -117,22 +124,43 @@ template <typename T>
 struct ActBwdOp {
   EpiActBwd<T> e;
   int M, N;
+  // the walk of an interior tile loads every row's z (zd) before the first row's stores
+  static constexpr bool PRELOAD = true;
+  struct In {
+    float z[4], zd[4];
+  };
   __device__ int n_trans() const { return e.dual ? 2 : 1; }
-  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
-                                      const float* c2, float* t1, float* t2) const {
-    const bool vec = cnt == 4 && (e.N & 3) == 0;
-    float z[4], zd[4] = {0.f, 0.f, 0.f, 0.f};
-    ld4(e.Zp, (long)m * e.N + n, cnt, vec, z);
-    if (e.dual) ld4(e.Zdp, (long)m * e.N + n, cnt, vec, zd);
+  __device__ bool aligned() const { return (e.N & 3) == 0; }
+  template <int NIT>
+  __device__ __forceinline__ void load_rows(int bz, int m, int dm, int n, In (&in)[NIT]) const {
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) ld4v(e.Zp, (long)(m + it * dm) * e.N + n, in[it].z);
+    if (e.dual) {
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) ld4v(e.Zdp, (long)(m + it * dm) * e.N + n, in[it].zd);
+    }
+  }
+  __device__ __forceinline__ void row_in(int bz, int m, int n, int cnt, const In& in,
+                                         const float* c1, const float* c2, float* t1,
+                                         float* t2) const {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       float d1, d2;
-      act_d12(e.act, z[k], d1, d2);
+      act_d12(e.act, in.z[k], d1, d2);
       t1[k] = c1[k] * d1;
-      t2[k] = e.dual ? c2[k] * d1 + c1[k] * d2 * zd[k] : 0.0f;
+      t2[k] = e.dual ? c2[k] * d1 + c1[k] * d2 * in.zd[k] : 0.0f;
     }
     store_row4(e.dZ, (long)m * e.ld + n, cnt, t1);
     if (e.dual) store_row4(e.dZd, (long)m * e.ld + n, cnt, t2);
+  }
+  __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
+                                      const float* c2, float* t1, float* t2) const {
+    const bool vec = cnt == 4 && (e.N & 3) == 0;
+    In in;
+    in.zd[0] = in.zd[1] = in.zd[2] = in.zd[3] = 0.f;
+    ld4(e.Zp, (long)m * e.N + n, cnt, vec, in.z);
+    if (e.dual) ld4(e.Zdp, (long)m * e.N + n, cnt, vec, in.zd);
+    row_in(bz, m, n, cnt, in, c1, c2, t1, t2);
   }
   __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
                                         const float* v) const {
@@ -144,11 +172,37 @@ template <typename T>
 struct ParamOp {
   ParamArgs<T> P;
   int M, N;
+  // the walk loads every row's inputs before the first row's arithmetic
+  static constexpr bool PRELOAD = true;
+  typedef ParamIn In;
   __device__ int n_trans() const { return P.outWT ? 1 : 0; }
+  __device__ bool aligned() const { return (P.nout & 3) == 0 && (P.w_off & 3) == 0; }
+  template <int NIT>
+  __device__ __forceinline__ void load_rows(int bz, int m, int dm, int n, ParamIn (&in)[NIT]) const {
+    const float* src[3];
+    param_sources(P, src);
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+      if (src[s]) {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it)
+          ld4v(src[s], P.w_off + (long)(m + it * dm) * P.nout + n, in[it].x[s]);
+      }
+  }
+  __device__ __forceinline__ void load(int bz, int m, int n, int cnt, ParamIn& in) const {
+    param_load(P, P.w_off + (long)m * P.nout + n, cnt, in);
+  }
+  __device__ __forceinline__ void row_in(int bz, int m, int n, int cnt, const ParamIn& in,
+                                         const float* c1, const float* c2, float* t1,
+                                         float* t2) const {
+    param_finish(P, P.w_off + (long)m * P.nout + n, cnt, in, c1, c2, t1);
+    if (P.outW) store_row4(P.outW, (long)m * P.ldW + n, cnt, t1);
+  }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
-    param_apply(P, P.w_off + (long)m * P.nout + n, cnt, c1, c2, t1);
-    if (P.outW) store_row4(P.outW, (long)m * P.ldW + n, cnt, t1);
+    ParamIn in;
+    load(bz, m, n, cnt, in);
+    row_in(bz, m, n, cnt, in, c1, c2, t1, t2);
   }
   __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,
                                         const float* v) const {
@@ -159,6 +213,8 @@ struct ParamOp {
 struct StoreOp {
   EpiStore e;
   int M, N;
+  static constexpr bool PRELOAD = false;
+  typedef int In;
   __device__ int n_trans() const { return 0; }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
@@ -180,6 +236,8 @@ struct StoreOp {
 struct ResidOp {
   EpiResid e;
   int M, N;
+  static constexpr bool PRELOAD = false;
+  typedef int In;
   __device__ int n_trans() const { return 0; }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
@@ -204,6 +262,8 @@ template <typename T>
 struct HeadMergeOp {
   EpiHeadMerge<T> e;
   int M, N;
+  static constexpr bool PRELOAD = false;
+  typedef int In;
   __device__ int n_trans() const { return e.dual ? 2 : 1; }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
@@ -229,6 +289,8 @@ template <typename T>
 struct HeadSplitOp {
   EpiHeadSplit<T> e;
   int M, N;
+  static constexpr bool PRELOAD = false;
+  typedef int In;
   __device__ int n_trans() const { return e.dual ? 2 : 1; }
   __device__ __forceinline__ void row(int bz, int m, int n, int cnt, const float* c1,
                                       const float* c2, float* t1, float* t2) const {
@@ -352,7 +414,41 @@ __device__ __forceinline__ void walk_tile(float* S1, float* S2, int mr0, int n0,
   constexpr int SLD = Stage<BN>::SLD;
   const int tid = threadIdx.x;
   const int nT = epi.n_trans();
-  {
+  bool walked = false;
+  if constexpr (Epi::PRELOAD && NT == 512) {
+    // Interior tile, aligned rows: every row's global inputs are requested with
+    // unconditional 16-byte loads before the first row's arithmetic, so a
+    // thread keeps all of them in flight at once.
+    if (mr0 + RP <= epi.M && n0 + BN <= epi.N && epi.aligned()) {
+      constexpr int TPR = BN / 4;
+      constexpr int RPI = NT / TPR;
+      constexpr int NIT = RP / RPI;
+      static_assert(RP % RPI == 0, "rows per thread");
+      const int c = (tid % TPR) * 4;
+      const int n = n0 + c;
+      typename Epi::In in[NIT];
+      epi.template load_rows<NIT>(bz, mr0 + tid / TPR, RPI, n, in);
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int rr = tid / TPR + it * RPI;
+        float c1[4], c2[4], t1[4], t2[4];
+        const int si = stage_idx<SLD>(rr, c);
+        const float4 x1 = *reinterpret_cast<const float4*>(S1 + si);
+        c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
+        if constexpr (HC2) {
+          const float4 x2 = *reinterpret_cast<const float4*>(S2 + si);
+          c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
+        } else {
+          c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
+        }
+        epi.row_in(bz, mr0 + rr, n, 4, in[it], c1, c2, t1, t2);
+        if (nT > 0) *reinterpret_cast<float4*>(S1 + si) = make_float4(t1[0], t1[1], t1[2], t1[3]);
+        if (nT > 1) *reinterpret_cast<float4*>(S2 + si) = make_float4(t2[0], t2[1], t2[2], t2[3]);
+      }
+      walked = true;
+    }
+  }
+  if (!walked) {
     constexpr int TPR = BN / 4;        // threads per row, 4 columns each
     constexpr int RPI = NT / TPR;      // rows per iteration
     const int c = (tid % TPR) * 4;
@@ -556,7 +652,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 }
 
 // ------------------------------------------------------------------------------------
-// Main loop, direct to LDS (bfloat16).  Tiles go from HBM to LDS with
+// Direct-to-LDS tile loads (bfloat16).  Tiles go from HBM to LDS with
 // buffer_load_dwordx4 ... lds, which needs no registers, so NST k steps are in
 // flight at once (NST - 1 loading while one is multiplied).  Each load
 // instruction fills 1 KB of LDS, lane l at byte 16 l; a lane picks which
@@ -652,117 +748,14 @@ struct DmaTile {
   }
 };
 
-template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
-__global__ void __launch_bounds__(256) gemm_nt_dma(GemmOperands<bf16_t> op, Epi epi) {
-  typedef DmaSmem<FLAGS, BM, BN, BK, NST, 2> SM;
-  constexpr bool HC1 = (FLAGS & G_C1) != 0;
-  constexpr bool HAD = (FLAGS & G_AD) != 0;
-  constexpr bool HBD = (FLAGS & G_BD) != 0;
-  constexpr int CPR = SM::CPR;
-  constexpr int ROWB = SM::ROWB;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
-  constexpr int TM = WTM / 16, TN = WTN / 16;
-  constexpr int NCH = CPR / 4;                 // 32-deep MFMA steps per k step
-  static_assert(NST >= 2 && SM::LPW * (NST - 2) < 64, "pipeline depth");
-
-  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  int m0, n0;
-  tile_origin<BM, BN>(op.M, op.N, m0, n0);
-  const int bz = blockIdx.y;
-  const int K = op.K;
-
-  DmaTile<BM, CPR> tA, tAd;
-  DmaTile<BN, CPR> tB, tBd;
-  if constexpr (SM::LA) tA.init(op.A + bz * op.sA, op.M, op.lda, K, m0, wave);
-  if constexpr (SM::LAD) tAd.init(op.Ad + bz * op.sA, op.M, op.lda, K, m0, wave);
-  if constexpr (SM::LB) tB.init(op.B + bz * op.sB, op.N, op.ldb, K, n0, wave);
-  if constexpr (SM::LBD) tBd.init(op.Bd + bz * op.sB, op.N, op.ldb, K, n0, wave);
-
-  auto issue = [&](int kt) {
-    char* st = smem + (kt % NST) * SM::STAGE_BYTES;
-    const int k0 = kt * BK;
-    if constexpr (SM::LA) tA.issue(st, k0, K, wave);
-    if constexpr (SM::LAD) tAd.issue(st + SM::OFF_AD, k0, K, wave);
-    if constexpr (SM::LB) tB.issue(st + SM::OFF_B, k0, K, wave);
-    if constexpr (SM::LBD) tBd.issue(st + SM::OFF_BD, k0, K, wave);
-  };
-
-  f32x4 acc1[TM][TN], acc2[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      acc1[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-
-  // Fragment addressing: lane reads row (lane % 16) of a 16-row slab, logical
-  // chunk lane / 16 + 4 c, stored at chunk (lane / 16 + 4 c) ^ swizzle(row).
-  const int sw = chunk_swizzle<CPR>(lane & 15);
-  int foff[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) foff[c] = (lane & 15) * ROWB + (((lane >> 4) + 4 * c) ^ sw) * 16;
-
-  const int nk = (K + BK - 1) / BK;
-#pragma unroll
-  for (int s = 0; s < NST - 1; ++s) issue(s);
-  for (int kt = 0; kt < nk; ++kt) {
-    // k step kt has landed once at most the loads of the NST - 2 later steps
-    // are outstanding; the barrier also retires every read of the stage that
-    // the next issue overwrites (read in step kt - 1).
-    wait_vm_lgkm<SM::LPW * (NST - 2)>();
-    lds_barrier();
-    issue(kt + NST - 1);   // past the last step: zero loads into a dead stage
-    const char* st = smem + (kt % NST) * SM::STAGE_BYTES;
-    const char* As = st;
-    const char* Ads = st + SM::OFF_AD;
-    const char* Bs = st + SM::OFF_B;
-    const char* Bds = st + SM::OFF_BD;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      bf16x8 a[TM], ad[TM], b[TN], bd[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r0 = (wm * WTM + i * 16) * ROWB + foff[c];
-        if constexpr (SM::LA) a[i] = *reinterpret_cast<const bf16x8*>(As + r0);
-        if constexpr (HAD) ad[i] = *reinterpret_cast<const bf16x8*>(Ads + r0);
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r0 = (wn * WTN + j * 16) * ROWB + foff[c];
-        if constexpr (SM::LB) b[j] = *reinterpret_cast<const bf16x8*>(Bs + r0);
-        if constexpr (HBD) bd[j] = *reinterpret_cast<const bf16x8*>(Bds + r0);
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          if constexpr (HC1) mma(acc1[i][j], a[i], b[j]);
-          if constexpr (HAD) mma(acc2[i][j], ad[i], b[j]);
-          if constexpr (HBD) mma(acc2[i][j], a[i], bd[j]);
-        }
-    }
-  }
-  // the trailing zero loads must land before the epilogue reuses the LDS
-  wait_vm_lgkm<0>();
-  lds_barrier();
-  run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem, m0, n0, bz, epi);
-}
-
 // ------------------------------------------------------------------------------------
 // Main loop, warp-specialised (bfloat16, 512 threads).  A wave that issues a
 // global load stalls until the compute unit's load unit takes it (about 16
 // cycles per 1 KB load, one unit per compute unit), and in-order issue holds
 // back its MFMAs meanwhile.  Here waves 4..7 only issue the direct-to-LDS loads
 // and waves 0..3 only read fragments and multiply, so each SIMD has one wave
-// that keeps its matrix core busy while the other waits on the load unit.  Tile,
-// LDS layout, zero fill and pipeline are those of gemm_nt_dma; the eight waves
-// meet at one barrier per k step and all of them walk the epilogue.
+// that keeps its matrix core busy while the other waits on the load unit.  The
+// eight waves meet at one barrier per k step and all of them walk the epilogue.
 // ------------------------------------------------------------------------------------
 template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
 __global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi epi) {
@@ -905,23 +898,12 @@ struct KDepth<G_BD, ParamOp<T>> {
 // Direct-to-LDS pipeline shape: k depth and stages, sized to about 128 KB of
 // LDS.  One operand pair: 64 deep x 4 stages; three or four operand tiles:
 // 32 deep x 4 stages.
-template <int FLAGS, class Epi>
+template <int FLAGS>
 struct DmaShape {
   static constexpr int NOPS = ((FLAGS & (G_C1 | G_BD)) ? 1 : 0) + ((FLAGS & G_AD) ? 1 : 0) +
                               ((FLAGS & (G_C1 | G_AD)) ? 1 : 0) + ((FLAGS & G_BD) ? 1 : 0);
   static constexpr int BK = NOPS <= 2 ? 64 : 32;
   static constexpr int NST = 4;
-  static constexpr bool ENABLED = true;
-  static constexpr bool WS = true;   // warp-specialised 512-thread kernel
-};
-// Backward-weight products with the parameter epilogue: many tiles over a short
-// k (the batch rows) and a heavy epilogue.  Two stages keep a workgroup within
-// 80 KB of LDS, so two of them share a compute unit and one's epilogue overlaps
-// the other's main loop.
-template <int FLAGS, typename T>
-struct DmaShape<FLAGS, ParamOp<T>> : DmaShape<FLAGS, StoreOp> {
-  static constexpr int NST = 2;
-  static constexpr bool WS = false;
 };
 
 template <typename T>
@@ -944,14 +926,10 @@ template <typename T, int FLAGS, int BM, int BN, class Epi>
 hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   const int tiles = cdiv(op.M, BM) * cdiv(op.N, BN);
   if constexpr (sizeof(T) == 2) {
-    typedef DmaShape<FLAGS, Epi> DS;
-    if (DS::ENABLED && dma_ok(op)) {
-      if constexpr (DS::WS)
-        hipLaunchKernelGGL((gemm_nt_ws<FLAGS, BM, BN, DS::BK, DS::NST, Epi>),
-                           dim3(tiles, op.batch), dim3(512), 0, s, op, epi);
-      else
-        hipLaunchKernelGGL((gemm_nt_dma<FLAGS, BM, BN, DS::BK, DS::NST, Epi>),
-                           dim3(tiles, op.batch), dim3(256), 0, s, op, epi);
+    typedef DmaShape<FLAGS> DS;
+    if (dma_ok(op)) {
+      hipLaunchKernelGGL((gemm_nt_ws<FLAGS, BM, BN, DS::BK, DS::NST, Epi>), dim3(tiles, op.batch),
+                         dim3(512), 0, s, op, epi);
       return hipGetLastError();
     }
   }

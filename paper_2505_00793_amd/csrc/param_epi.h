@@ -16,11 +16,6 @@
 
 namespace mfmg {
 
-// Up to four consecutive parameters: loaded inputs, outputs to store.
-struct P4 {
-  float th[4], et[4], tb[4], eb[4], m[4], v[4];
-};
-
 __device__ __forceinline__ void ld4(const float* __restrict__ p, long idx, int cnt, bool vec,
                                     float* out) {
   if (vec) {
@@ -30,6 +25,12 @@ __device__ __forceinline__ void ld4(const float* __restrict__ p, long idx, int c
 #pragma unroll
     for (int k = 0; k < 4; ++k) out[k] = k < cnt ? p[idx + k] : 0.0f;
   }
+}
+
+// 16-byte load of 4 consecutive floats at a 16-byte aligned index.
+__device__ __forceinline__ void ld4v(const float* __restrict__ p, long idx, float* out) {
+  const float4 v = *reinterpret_cast<const float4*>(p + idx);
+  out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
 }
 
 __device__ __forceinline__ void st4(float* __restrict__ p, long idx, int cnt, bool vec,
@@ -43,42 +44,73 @@ __device__ __forceinline__ void st4(float* __restrict__ p, long idx, int cnt, bo
   }
 }
 
-// cnt (1..4) consecutive parameters starting at flat index idx.  All loads are
-// issued before any store.  cv receives the values for the operand copies
-// (new theta for the update modes, the next tangent for the SGD seed/reverse
-// modes, 0 otherwise).
+// Inputs of the per-parameter arithmetic for up to 4 consecutive parameters,
+// loaded ahead of it so that a thread can keep many groups in flight.  Which
+// slots hold what depends on the mode (see param_load).
+struct ParamIn {
+  float x[3][4];
+};
+
+// The arrays whose values the arithmetic of this mode needs, by input slot
+// (null: slot unused).
 template <typename T>
-__device__ __forceinline__ void param_apply(const ParamArgs<T>& P, long idx, int cnt,
-                                            const float* g, const float* hv, float* cv) {
+__device__ __forceinline__ void param_sources(const ParamArgs<T>& P, const float* (&src)[3]) {
+  src[0] = src[1] = src[2] = nullptr;
+  switch (P.mode) {
+    case P_UPD_SGD_PP: src[0] = P.theta; src[1] = P.eta; return;
+    case P_UPD_SGD_FIXED: src[0] = P.theta; return;
+    case P_UPD_ADAM: src[0] = P.theta; src[1] = P.m_in; src[2] = P.v_in; return;
+    case P_SEED_SGD_PP: src[1] = P.eta; return;
+    case P_REV_SGD_PP: src[0] = P.thetabar; src[1] = P.eta; src[2] = P.first ? nullptr : P.etabar; return;
+    case P_REV_SGD_FIXED:
+    case P_REV_ADAM: src[0] = P.thetabar; return;
+    default: return;
+  }
+}
+
+// Loads the inputs of cnt (1..4) consecutive parameters starting at flat index idx.
+template <typename T>
+__device__ __forceinline__ void param_load(const ParamArgs<T>& P, long idx, int cnt, ParamIn& in) {
   const bool vec = cnt == 4 && (idx & 3) == 0;
-  float a[4], b[4], c[4];
+  const float* src[3];
+  param_sources(P, src);
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    if (src[s]) ld4(src[s], idx, cnt, vec, in.x[s]);
+}
+
+// The arithmetic and stores for cnt (1..4) consecutive parameters at flat index
+// idx, given their inputs.  cv receives the values for the operand copies (new
+// theta for the update modes, the next tangent for the SGD seed/reverse modes,
+// 0 otherwise).
+template <typename T>
+__device__ __forceinline__ void param_finish(const ParamArgs<T>& P, long idx, int cnt,
+                                             const ParamIn& in, const float* g, const float* hv,
+                                             float* cv) {
+  const bool vec = cnt == 4 && (idx & 3) == 0;
   switch (P.mode) {
     case P_UPD_SGD_PP:
     case P_UPD_SGD_FIXED: {
-      ld4(P.theta, idx, cnt, vec, a);
-      if (P.mode == P_UPD_SGD_PP) ld4(P.eta, idx, cnt, vec, b);
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const float lam = P.mode == P_UPD_SGD_PP ? expf(b[k]) : P.lr;
-        cv[k] = a[k] - lam * g[k];
+        const float lam = P.mode == P_UPD_SGD_PP ? expf(in.x[1][k]) : P.lr;
+        cv[k] = in.x[0][k] - lam * g[k];
       }
       st4(P.theta_next, idx, cnt, vec, cv);
       if (P.grad_out) st4(P.grad_out, idx, cnt, vec, g);
       return;
     }
     case P_UPD_ADAM: {
-      ld4(P.theta, idx, cnt, vec, a);
-      float m[4] = {0.f, 0.f, 0.f, 0.f}, v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (P.m_in) ld4(P.m_in, idx, cnt, vec, m);
-      if (P.v_in) ld4(P.v_in, idx, cnt, vec, v);
+      float m[4], v[4];
       const float lam = expf(P.eta[P.layer]);
       const float om = P.eta[P.n_layers];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        m[k] = P.b1 * m[k] + (1.0f - P.b1) * g[k];
-        v[k] = P.b2 * v[k] + (1.0f - P.b2) * g[k] * g[k];
+        const float m0 = P.m_in ? in.x[1][k] : 0.0f, v0 = P.v_in ? in.x[2][k] : 0.0f;
+        m[k] = P.b1 * m0 + (1.0f - P.b1) * g[k];
+        v[k] = P.b2 * v0 + (1.0f - P.b2) * g[k] * g[k];
         const float u = (m[k] / P.k1) / (sqrtf(v[k] / P.k2) + P.eps);
-        cv[k] = a[k] - lam * (u + om * a[k]);
+        cv[k] = in.x[0][k] - lam * (u + om * in.x[0][k]);
       }
       st4(P.theta_next, idx, cnt, vec, cv);
       st4(P.m_out, idx, cnt, vec, m);
@@ -90,39 +122,36 @@ __device__ __forceinline__ void param_apply(const ParamArgs<T>& P, long idx, int
     case P_SEED_SGD_PP:
     case P_SEED_SGD_FIXED:
     case P_SEED_ADAM: {
-      if (P.mode == P_SEED_SGD_PP) ld4(P.eta, idx, cnt, vec, b);
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        cv[k] = P.mode == P_SEED_SGD_PP ? -expf(b[k]) * g[k]
+        cv[k] = P.mode == P_SEED_SGD_PP ? -expf(in.x[1][k]) * g[k]
                 : P.mode == P_SEED_SGD_FIXED ? -P.lr * g[k] : 0.0f;
       st4(P.thetabar, idx, cnt, vec, g);
       return;
     }
     case P_REV_SGD_PP: {
-      ld4(P.thetabar, idx, cnt, vec, a);
-      ld4(P.eta, idx, cnt, vec, b);
-      if (!P.first) ld4(P.etabar, idx, cnt, vec, c);
+      float tb[4], eb[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const float lam = expf(b[k]);
-        const float eb = -lam * g[k] * a[k];
-        c[k] = P.first ? eb : c[k] + eb;
-        a[k] = a[k] + hv[k];
-        cv[k] = -lam * a[k];
+        const float lam = expf(in.x[1][k]);
+        const float e = -lam * g[k] * in.x[0][k];
+        eb[k] = P.first ? e : in.x[2][k] + e;
+        tb[k] = in.x[0][k] + hv[k];
+        cv[k] = -lam * tb[k];
       }
-      st4(P.etabar, idx, cnt, vec, c);
-      st4(P.thetabar, idx, cnt, vec, a);
+      st4(P.etabar, idx, cnt, vec, eb);
+      st4(P.thetabar, idx, cnt, vec, tb);
       return;
     }
     case P_REV_SGD_FIXED:
     case P_REV_ADAM: {
-      ld4(P.thetabar, idx, cnt, vec, a);
+      float tb[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        a[k] = a[k] + hv[k];
-        cv[k] = P.mode == P_REV_SGD_FIXED ? -P.lr * a[k] : 0.0f;
+        tb[k] = in.x[0][k] + hv[k];
+        cv[k] = P.mode == P_REV_SGD_FIXED ? -P.lr * tb[k] : 0.0f;
       }
-      st4(P.thetabar, idx, cnt, vec, a);
+      st4(P.thetabar, idx, cnt, vec, tb);
       return;
     }
     case P_HVP: {
@@ -139,6 +168,15 @@ __device__ __forceinline__ void param_apply(const ParamArgs<T>& P, long idx, int
       return;
     }
   }
+}
+
+// Loads, arithmetic and stores of cnt (1..4) consecutive parameters.
+template <typename T>
+__device__ __forceinline__ void param_apply(const ParamArgs<T>& P, long idx, int cnt,
+                                            const float* g, const float* hv, float* cv) {
+  ParamIn in;
+  param_load(P, idx, cnt, in);
+  param_finish(P, idx, cnt, in, g, hv, cv);
 }
 
 // One parameter (the bias reductions).
