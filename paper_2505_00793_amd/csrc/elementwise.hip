@@ -45,9 +45,22 @@ __global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ 
 // ------------------------------------------------------------------------------------
 // Bias entries: column sums of dZ (and its tangent) over the batch rows, read
 // from the transposed copies (one wavefront per column, contiguous reads),
-// then the per-parameter epilogue.
+// then the per-parameter epilogue.  VEC: rows start 16-byte aligned, so each
+// lane reads 16 bytes at a time; the rows % (elements per 16 bytes) tail is
+// read element by element.
 // ------------------------------------------------------------------------------------
-template <typename T>
+__device__ __forceinline__ float chunk_sum(uint4 u, const bf16_t*) {
+  const unsigned w[4] = {u.x, u.y, u.z, u.w};
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) s += __uint_as_float(w[k] << 16) + __uint_as_float(w[k] & 0xffff0000u);
+  return s;
+}
+__device__ __forceinline__ float chunk_sum(uint4 u, const float*) {
+  return (__uint_as_float(u.x) + __uint_as_float(u.y)) + (__uint_as_float(u.z) + __uint_as_float(u.w));
+}
+
+template <typename T, bool VEC>
 __global__ void __launch_bounds__(256) bias_kernel(const T* __restrict__ dZT,
                                                    const T* __restrict__ dZdT, int ld, int rows,
                                                    ParamArgs<T> P) {
@@ -55,7 +68,19 @@ __global__ void __launch_bounds__(256) bias_kernel(const T* __restrict__ dZT,
   const int lane = threadIdx.x & 63;
   if (n >= P.nout) return;
   float g = 0.0f, hv = 0.0f;
-  for (int r = lane; r < rows; r += 64) {
+  int r0 = 0;
+  if constexpr (VEC) {
+    constexpr int VE = Elem<T>::VE;
+    const int full = rows / VE * VE;
+    const T* a = dZT + (long)n * ld;
+    const T* b = dZdT ? dZdT + (long)n * ld : nullptr;
+    for (int r = lane * VE; r < full; r += 64 * VE) {
+      g += chunk_sum(*reinterpret_cast<const uint4*>(a + r), a);
+      if (b) hv += chunk_sum(*reinterpret_cast<const uint4*>(b + r), b);
+    }
+    r0 = full;
+  }
+  for (int r = r0 + lane; r < rows; r += 64) {
     g += Elem<T>::to_float(dZT[(long)n * ld + r]);
     if (dZdT) hv += Elem<T>::to_float(dZdT[(long)n * ld + r]);
   }
@@ -419,8 +444,14 @@ template <typename T>
 hipError_t bias_reduce(const T* dZT, const T* dZdT, int ld, int rows, const ParamArgs<T>& P,
                        hipStream_t s) {
   if (P.nout <= 0) return hipSuccess;
-  hipLaunchKernelGGL(bias_kernel<T>, dim3(cdiv(P.nout, 4)), dim3(256), 0, s, dZT, dZdT, ld, rows,
-                     P);
+  const bool vec = (ld % Elem<T>::VE) == 0 && (reinterpret_cast<uintptr_t>(dZT) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(dZdT) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL((bias_kernel<T, true>), dim3(cdiv(P.nout, 4)), dim3(256), 0, s, dZT, dZdT, ld,
+                       rows, P);
+  else
+    hipLaunchKernelGGL((bias_kernel<T, false>), dim3(cdiv(P.nout, 4)), dim3(256), 0, s, dZT, dZdT,
+                       ld, rows, P);
   return hipGetLastError();
 }
 

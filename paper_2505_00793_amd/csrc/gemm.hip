@@ -702,6 +702,7 @@ struct DmaSmem {
   static constexpr int OFF_B = OFF_AD + (LAD ? BM : 0) * ROWB;
   static constexpr int OFF_BD = OFF_B + (LB ? BN : 0) * ROWB;
   static constexpr int STAGE_BYTES = OFF_BD + (LBD ? BN : 0) * ROWB;
+  static constexpr int NOPS = (LA ? 1 : 0) + (LAD ? 1 : 0) + (LB ? 1 : 0) + (LBD ? 1 : 0);
   static constexpr int CPR = BK / 8;
   static constexpr int LPW = STAGE_BYTES / 1024 / 4;         // load instructions per wave
   static constexpr int PIPE_BYTES = NST * STAGE_BYTES;
@@ -835,29 +836,38 @@ __global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi e
       const char* Ads = st + SM::OFF_AD;
       const char* Bs = st + SM::OFF_B;
       const char* Bds = st + SM::OFF_BD;
+      // Fragments of NF chunks are read before the first chunk's MFMAs, so the
+      // later chunks' LDS reads overlap them: all chunks of the step for two
+      // operand tiles, one at a time for the dual products (registers).
+      constexpr int NF = SM::NOPS <= 2 ? NCH : 1;
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        bf16x8 a[TM], ad[TM], b[TN], bd[TN];
+      for (int c0 = 0; c0 < NCH; c0 += NF) {
+        bf16x8 a[NF][TM], ad[NF][TM], b[NF][TN], bd[NF][TN];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int r0 = (wm * WTM + i * 16) * ROWB + foff[c];
-          if constexpr (SM::LA) a[i] = *reinterpret_cast<const bf16x8*>(As + r0);
-          if constexpr (HAD) ad[i] = *reinterpret_cast<const bf16x8*>(Ads + r0);
-        }
+        for (int f = 0; f < NF; ++f) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int r0 = (wn * WTN + j * 16) * ROWB + foff[c];
-          if constexpr (SM::LB) b[j] = *reinterpret_cast<const bf16x8*>(Bs + r0);
-          if constexpr (HBD) bd[j] = *reinterpret_cast<const bf16x8*>(Bds + r0);
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
+          for (int i = 0; i < TM; ++i) {
+            const int r0 = (wm * WTM + i * 16) * ROWB + foff[c0 + f];
+            if constexpr (SM::LA) a[f][i] = *reinterpret_cast<const bf16x8*>(As + r0);
+            if constexpr (HAD) ad[f][i] = *reinterpret_cast<const bf16x8*>(Ads + r0);
+          }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
-            if constexpr (HC1) mma(acc1[i][j], a[i], b[j]);
-            if constexpr (HAD) mma(acc2[i][j], ad[i], b[j]);
-            if constexpr (HBD) mma(acc2[i][j], a[i], bd[j]);
+            const int r0 = (wn * WTN + j * 16) * ROWB + foff[c0 + f];
+            if constexpr (SM::LB) b[f][j] = *reinterpret_cast<const bf16x8*>(Bs + r0);
+            if constexpr (HBD) bd[f][j] = *reinterpret_cast<const bf16x8*>(Bds + r0);
           }
+        }
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              if constexpr (HC1) mma(acc1[i][j], a[f][i], b[f][j]);
+              if constexpr (HAD) mma(acc2[i][j], ad[f][i], b[f][j]);
+              if constexpr (HBD) mma(acc2[i][j], a[f][i], bd[f][j]);
+            }
       }
     }
     wait_vm_lgkm<0>();
@@ -895,15 +905,16 @@ struct KDepth<G_BD, ParamOp<T>> {
   static constexpr int value = 32;
 };
 
-// Direct-to-LDS pipeline shape: k depth and stages, sized to about 128 KB of
-// LDS.  One operand pair: 64 deep x 4 stages; three or four operand tiles:
-// 32 deep x 4 stages.
+// Direct-to-LDS pipeline shape.  The k depth is 64 (128-byte rows): each 1 KB
+// load then covers 8 whole 128-byte lines, where 64-byte rows make it touch 16
+// half lines and halve the load unit's throughput.  Stages: as many 32 KB
+// (two tiles), 48 KB (three) or 64 KB (four) stages as fit in 144 KB.
 template <int FLAGS>
 struct DmaShape {
   static constexpr int NOPS = ((FLAGS & (G_C1 | G_BD)) ? 1 : 0) + ((FLAGS & G_AD) ? 1 : 0) +
                               ((FLAGS & (G_C1 | G_AD)) ? 1 : 0) + ((FLAGS & G_BD) ? 1 : 0);
-  static constexpr int BK = NOPS <= 2 ? 64 : 32;
-  static constexpr int NST = 4;
+  static constexpr int BK = 64;
+  static constexpr int NST = NOPS <= 2 ? 4 : NOPS == 3 ? 3 : 2;
 };
 
 template <typename T>

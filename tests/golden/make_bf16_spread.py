@@ -32,9 +32,13 @@ FP32_CASES = [("c3_mlp_gelu_adam", 16)]
 
 
 def groups(cfg):
+    """The eta groups of the parity gates: each per-layer lr and the decay of
+    Adam separately, each meta-model tensor separately, else all of eta."""
     n = W.n_eta(cfg)
     if cfg.meta == W.META_LOGLR_PER_LAYER_WD:
         return [[i] for i in range(n)]
+    if cfg.meta == W.META_TOKEN_WEIGHT_MLP:
+        return [list(range(off, off + int(np.prod(shape)))) for _, off, shape in W.meta_layout(cfg)]
     return [list(range(n))]
 
 

@@ -1,6 +1,9 @@
 """Shared test helpers: workload config -> ABI description, device upload, error metrics."""
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 
 import workloads as W
@@ -62,3 +65,10 @@ def to_device(inp: dict, device="cuda"):
         "xs": [t(x) for x in inp["train_x"]], "ys": [t(y) for y in inp["train_y"]],
         "vx": t(inp["val_x"]), "vy": t(inp["val_y"]),
     }
+
+
+def spread_of(key):
+    """Per-eta-group distance between the oracle's float32- and
+    float64-accumulated bf16 emulations, stored by tests/golden/make_bf16_spread.py."""
+    with open(os.path.join(os.path.dirname(__file__), "golden", "bf16_spread.json")) as f:
+        return json.load(f)[key]["emu32_vs_emu64"]

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import workloads as W
-from helpers import desc_of, eta_groups, group_errors, relerr, to_device, tol_of
+from helpers import desc_of, eta_groups, group_errors, relerr, spread_of, to_device, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -189,11 +189,6 @@ def test_meta_grad_deterministic_and_workspace_reuse():
     run_meta(other, inp2)
     b, Vb, _ = run_meta(cfg, inp)
     assert np.array_equal(a, b) and Va == Vb
-
-
-def spread_of(key):
-    with open(os.path.join(os.path.dirname(__file__), "golden", "bf16_spread.json")) as f:
-        return json.load(f)[key]["emu32_vs_emu64"]
 
 
 @pytest.mark.parametrize("name,T", [("c5_mlp_relu_8x4096", 2), ("c5_mlp_relu_8x4096", 4),

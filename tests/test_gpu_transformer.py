@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import workloads as W
-from helpers import desc_of, group_errors, relerr, to_device, tol_of
+from helpers import desc_of, group_errors, relerr, spread_of, to_device, tol_of
 from oracle import models as OM
 
 pytestmark = pytest.mark.gpu
@@ -32,6 +32,8 @@ def c(a):
 
 SMALL = W.SMALL["c4_small"]
 CASES = {"fp32": SMALL.with_(precision=W.PREC_FP32), "bf16": SMALL}
+# the full transformer workload: d 512, 8 heads, 4 blocks, vocab 8192, 16 x 256 tokens
+FULL = {"fp32": W.C4.with_(precision=W.PREC_FP32), "bf16": W.C4}
 
 
 def token_alpha(cfg, theta, eta, tokens):
@@ -45,13 +47,21 @@ def token_alpha(cfg, theta, eta, tokens):
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_tf_inner_step(prec):
-    cfg = CASES[prec]
-    inp = W.make_inputs(cfg)
+    check_inner_step(CASES[prec], prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_tf_inner_step_full_size(prec):
+    check_inner_step(FULL[prec], prec)
+
+
+def check_inner_step(cfg, prec):
+    inp = W.make_inputs(cfg, T=1)
     n = W.n_theta(cfg)
     theta = inp["theta0"] + 0.02 * W.random_direction(n, 51)
     tok = inp["train_x"][0]
     alpha = token_alpha(cfg, theta, inp["eta"], tok)
-    print(f"\n[tf inner_step] {prec}", flush=True)
+    print(f"\n[tf inner_step] {cfg.name} {prec}", flush=True)
     th1_ref, _, g_ref, L_ref = oracle.inner_step(cfg, theta, None, inp["eta"], tok, None, 0,
                                                  alpha=alpha, bf16=prec == "bf16")
     P = M().Problem(desc_of(cfg))
@@ -77,15 +87,22 @@ def test_tf_inner_step(prec):
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_tf_hvp(prec):
-    cfg = CASES[prec]
-    inp = W.make_inputs(cfg)
+    check_hvp(CASES[prec], prec)
+
+
+def test_tf_hvp_full_size_fp32():
+    check_hvp(FULL["fp32"], "fp32")
+
+
+def check_hvp(cfg, prec):
+    inp = W.make_inputs(cfg, T=1)
     n = W.n_theta(cfg)
     theta = inp["theta0"] + 0.02 * W.random_direction(n, 52)
     v = 0.1 * W.random_direction(n, 53)
     tok = inp["train_x"][0]
     alpha = token_alpha(cfg, theta, inp["eta"], tok)
     bf16 = prec == "bf16"
-    print(f"\n[tf hvp] {prec}", flush=True)
+    print(f"\n[tf hvp] {cfg.name} {prec}", flush=True)
     hv_ref = oracle.hvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
     mv_ref = oracle.mvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
     g_ref, _ = oracle.grad_and_loss(cfg, theta, tok, None, alpha=alpha, bf16=bf16)
@@ -131,4 +148,23 @@ def test_tf_meta_grad(prec):
     print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
     assert np.all(np.isfinite(got))
     assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
+def test_tf_meta_grad_full_size_bf16():
+    """The full transformer workload at T=2 with bf16 operands against the
+    oracle's float64-accumulated bf16 emulation, each meta-model tensor gated at
+    max(2e-2, 1.5 x the stored spread between two valid emulations)."""
+    cfg = W.C4.with_(T=2)
+    inp = W.make_inputs(cfg, T=2)
+    print("\n[tf meta_grad full bf16] T=2", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=True)
+    spread = spread_of(f"{cfg.name}/T2")
+    errs = group_errors(cfg, got, ref)
+    print(f"  errors {['%.2e' % e for e in errs]} spread {['%.2e' % e for e in spread]} "
+          f"V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    for e, sp in zip(errs, spread):
+        assert e <= max(tol_of(cfg), 1.5 * sp)
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
