@@ -42,6 +42,84 @@ __global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ 
   }
 }
 
+// The same with 16-byte accesses: each thread converts 4 consecutive columns of a
+// row (float4 in, 4 elements out) and writes the transposed copy 4 consecutive
+// rows at a time.  Requires lds, ldd, lddT and the batch strides to be
+// multiples of 4 and the arrays aligned to their 4-element width.
+template <typename T>
+__global__ void __launch_bounds__(256) convert_vec_kernel(const float* __restrict__ src, int rows,
+                                                          int cols, int lds, T* dst, int ldd,
+                                                          T* dstT, int lddT, long s_src,
+                                                          long s_dst, long s_dstT) {
+  __shared__ __attribute__((aligned(16))) float tile[64][68];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  src += blockIdx.z * s_src;
+  if (dst) dst += blockIdx.z * s_dst;
+  if (dstT) dstT += blockIdx.z * s_dstT;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int c = c0 + tx * 4;
+  for (int i = ty; i < 64; i += 16) {
+    const int r = r0 + i;
+    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (r < rows) {
+      if (c + 4 <= cols) {
+        const float4 x = *reinterpret_cast<const float4*>(src + (long)r * lds + c);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+        if (dst) store4(dst + (long)r * ldd + c, v[0], v[1], v[2], v[3]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (c + k < cols) {
+            v[k] = src[(long)r * lds + c + k];
+            if (dst) dst[(long)r * ldd + c + k] = Elem<T>::from_float(v[k]);
+          }
+      }
+    }
+    *reinterpret_cast<float4*>(&tile[i][tx * 4]) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  if (!dstT) return;
+  __syncthreads();
+  const int r = r0 + tx * 4;
+  for (int j = ty; j < 64; j += 16) {
+    const int cc = c0 + j;
+    if (cc >= cols || r >= rows) continue;
+    const float w0 = tile[tx * 4][j], w1 = tile[tx * 4 + 1][j], w2 = tile[tx * 4 + 2][j],
+                w3 = tile[tx * 4 + 3][j];
+    if (r + 4 <= rows) {
+      store4(dstT + (long)cc * lddT + r, w0, w1, w2, w3);
+    } else {
+      const float w[4] = {w0, w1, w2, w3};
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (r + k < rows) dstT[(long)cc * lddT + r + k] = Elem<T>::from_float(w[k]);
+    }
+  }
+}
+
+// bf16 / float [rows][ld] -> its transpose [cols][ldT], through a 64x64 LDS tile;
+// the transposed copies of the loss head's outputs.  Two matrices per launch
+// (z = 0, 1; the second may be null).
+template <typename T>
+__global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ a0,
+                                                        const T* __restrict__ a1, int rows,
+                                                        int cols, int ld, T* t0, T* t1, int ldT) {
+  __shared__ float tile[64][65];
+  const T* src = blockIdx.z ? a1 : a0;
+  T* dst = blockIdx.z ? t1 : t0;
+  if (!src || !dst) return;
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < rows && c < cols) ? Elem<T>::to_float(src[(long)r * ld + c]) : 0.0f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) dst[(long)c * ldT + r] = Elem<T>::from_float(tile[tx][i]);
+  }
+}
+
 // ------------------------------------------------------------------------------------
 // Bias entries: column sums of dZ (and its tangent) over the batch rows, read
 // from the transposed copies (one wavefront per column, contiguous reads),
@@ -138,11 +216,9 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
       const float p = expf(z[c] - lse);
       const float d = scale * (p - (c == y ? 1.0f : 0.0f));
       a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
-      a.dT[(long)c * a.ldT + row] = Elem<T>::from_float(d);
       if (a.dual) {
         const float dd = scale * p * (zd[c] - s);
         a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
-        a.ddT[(long)c * a.ldT + row] = Elem<T>::from_float(dd);
       }
     }
   } else {
@@ -152,12 +228,10 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
       loss += r * r;
       const float d = 2.0f * scale * r;
       a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
-      a.dT[(long)c * a.ldT + row] = Elem<T>::from_float(d);
       if (a.dual) {
         ldot += 2.0f * r * zd[c];
         const float dd = 2.0f * scale * zd[c];
         a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
-        a.ddT[(long)c * a.ldT + row] = Elem<T>::from_float(dd);
       }
     }
     loss = wave_sum(loss);
@@ -435,8 +509,17 @@ hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst,
                           long s_dstT) {
   if (rows <= 0 || cols <= 0 || batch <= 0) return hipSuccess;
   dim3 grid(cdiv(cols, 64), cdiv(rows, 64), batch);
-  hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
-                     dstT, lddT, s_src, s_dst, s_dstT);
+  const auto al = [](const void* q, uintptr_t a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+  const uintptr_t aw = 4 * sizeof(T);  // alignment of 4 elements
+  const bool vec = (lds % 4) == 0 && (s_src % 4) == 0 && al(src, 16) &&
+                   (!dst || ((ldd % 4) == 0 && (s_dst % 4) == 0 && al(dst, aw))) &&
+                   (!dstT || ((lddT % 4) == 0 && (s_dstT % 4) == 0 && al(dstT, aw)));
+  if (vec)
+    hipLaunchKernelGGL(convert_vec_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
+                       dstT, lddT, s_src, s_dst, s_dstT);
+  else
+    hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
+                       dstT, lddT, s_src, s_dst, s_dstT);
   return hipGetLastError();
 }
 
@@ -458,6 +541,11 @@ hipError_t bias_reduce(const T* dZT, const T* dZdT, int ld, int rows, const Para
 template <typename T>
 hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
   hipLaunchKernelGGL(loss_kernel<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // transposed copies of dL/dz (and its tangent), coalesced through LDS
+  hipLaunchKernelGGL(transpose_kernel<T>, dim3(cdiv(a.C, 64), cdiv(a.rows, 64), 2), dim3(256), 0, s,
+                     a.d, a.dual ? a.dd : nullptr, a.rows, a.C, a.ld, a.dT, a.ddT, a.ldT);
   return hipGetLastError();
 }
 
