@@ -105,11 +105,12 @@ def algorithmic_bytes(cfg: W.Config, T: int):
 
 # Kernel instantiation that makes up each kernel class in the c5 run (bf16,
 # 128 x 128 tiles on the direct-to-LDS path), for matching counter records.
+# (Regular expressions over the kernel name: flags, tile and epilogue; any k depth and stages.)
 CLASS_KERNEL = {
-    "dual_bwd_weight_gemm_reverse": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ParamOp",
-    "bwd_weight_gemm_update": "gemm_nt_ws<1, 128, 128, 64, 4, mfmg::(anonymous namespace)::ParamOp",
-    "dual_fwd_gemm": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ActFwdOp",
-    "dual_bwd_data_gemm": "gemm_nt_ws<7, 128, 128, 32, 4, mfmg::(anonymous namespace)::ActBwdOp",
+    "dual_bwd_weight_gemm_reverse": r"gemm_nt_ws<7, 128, 128, \d+, \d+, mfmg::\(anonymous namespace\)::ParamOp",
+    "bwd_weight_gemm_update": r"gemm_nt_ws<1, 128, 128, \d+, \d+, mfmg::\(anonymous namespace\)::ParamOp",
+    "dual_fwd_gemm": r"gemm_nt_ws<7, 128, 128, \d+, \d+, mfmg::\(anonymous namespace\)::ActFwdOp",
+    "dual_bwd_data_gemm": r"gemm_nt_ws<7, 128, 128, \d+, \d+, mfmg::\(anonymous namespace\)::ActBwdOp",
 }
 KERNEL_SOURCES = ["paper_2505_00793_amd/csrc/gemm.hip", "paper_2505_00793_amd/csrc/param_epi.h",
                   "paper_2505_00793_amd/csrc/kernels.h", "paper_2505_00793_amd/csrc/common.h"]
@@ -150,6 +151,7 @@ def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, comma
     dispatch) of `bench.py --copy-bytes N` into per-launch HBM bytes of one
     kernel class, each counter scaled by what it reads for the plain N-byte copy."""
     import csv
+    import re
 
     def load(path, counter):
         per = {}
@@ -164,12 +166,16 @@ def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, comma
         rows = load(path, counter)
         copies = sorted((v for n, v in rows if "copyBuffer" in n), reverse=True)[:3]
         factor = (copy_bytes / 1024.0) / (sum(copies) / len(copies))
-        ks = [v for n, v in rows if CLASS_KERNEL[cls] in n]
+        ks = [v for n, v in rows if re.search(CLASS_KERNEL[cls], n)]
+        names = sorted({n for n, _ in rows if re.search(CLASS_KERNEL[cls], n)})
+        if not ks:
+            raise SystemExit(f"no dispatch of {cls} ({CLASS_KERNEL[cls]}) in {path}")
         out[counter] = {"copy_kib_per_dispatch": round(sum(copies) / len(copies), 1),
                         "scale": round(factor, 4), "dispatches": len(ks),
                         "kib_per_dispatch": round(sum(ks) / len(ks), 1),
                         "bytes_per_launch": sum(ks) / len(ks) * 1024.0 * factor}
-    rec = {"kernel_class": cls, "kernel": CLASS_KERNEL[cls], "copy_bytes": copy_bytes,
+    kname = re.sub(r"^void |\(mfmg::GemmOperands.*$", "", names[0])
+    rec = {"kernel_class": cls, "kernel": kname, "copy_bytes": copy_bytes,
            "fetch": out["FETCH_SIZE"], "write": out["WRITE_SIZE"],
            "hbm_bytes_per_launch": round(out["FETCH_SIZE"]["bytes_per_launch"]
                                          + out["WRITE_SIZE"]["bytes_per_launch"]),
@@ -184,7 +190,7 @@ def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, comma
             f"Each counter is scaled by its reading for a plain device copy of {copy_bytes} bytes "
             f"(`__amd_rocclr_copyBuffer`, which reads and writes exactly that many bytes), then "
             f"averaged over the {out['FETCH_SIZE']['dispatches']} dispatches of "
-            f"`{CLASS_KERNEL[cls]}>`.", "",
+            f"`{kname}`.", "",
             "| counter | copy reads (KiB) | scale | kernel (KiB/dispatch) | bytes per launch |",
             "|---|---:|---:|---:|---:|"]
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
