@@ -211,6 +211,13 @@ def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, comma
 
 def desc_of(cfg: W.Config):
     from paper_2505_00793_amd import _lib as M
+    if cfg.kind == W.KIND_TRANSFORMER:
+        return M.make_desc(kind=1, widths=(1, 1), loss=cfg.loss, optimizer=cfg.optimizer,
+                           meta=cfg.meta, precision=cfg.precision, has_bias=False,
+                           rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
+                           d_model=cfg.d_model, n_heads=cfg.n_heads, d_ff=cfg.d_ff,
+                           vocab=cfg.vocab, seq=cfg.seq, n_blocks=cfg.n_blocks,
+                           meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps, rope_base=cfg.rope_base)
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
@@ -245,6 +252,72 @@ def cpu_baseline(cfg: W.Config, inp: dict, T: int):
                        f"{per:.1f} s per meta-gradient")}
 
 
+WORKLOADS = {
+    "c1_linreg": "linear regression 64 features, 256 rows, per-parameter log learning rates, fp32",
+    "c2_mlp_tanh_lossweights": ("MLP 784-256-10 tanh, CE, 128 rows, SGD lr 0.1, per-example loss "
+                                "weights, fp32"),
+    "c3_mlp_gelu_adam": ("MLP 1024-(1024x3)-100 GELU, CE, 512 rows, Adam with per-layer log "
+                         "learning rates and weight decay, bf16 GEMM operands"),
+    "c4_transformer_tokenweights": ("decoder 4 blocks d 512, 8 heads, FF 2048, vocab 8192, RoPE, "
+                                    "16x256 tokens, SGD lr 0.1, per-token loss weights from a "
+                                    "512-128-1 meta-model, bf16 GEMM operands"),
+}
+
+
+def bench_config(name: str, args):
+    """meta-gradients/s of one of the other workloads at its own T, same timing
+    protocol as the main line (inputs resident, warm-up calls, HIP-event timing
+    on the stream); no roofline, sweep or CPU baseline."""
+    import torch
+    from paper_2505_00793_amd import _lib as M
+    cfg = W.CONFIGS[name]
+    T = cfg.T
+    log(f"[bench] {name}: generating inputs (T={T})")
+    inp = W.make_inputs(cfg)
+    dev = torch.device("cuda")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    theta0, eta = up(inp["theta0"]), up(inp["eta"])
+    xs = [up(x) for x in inp["train_x"]]
+    vx = up(inp["val_x"])
+    if cfg.kind == W.KIND_TRANSFORMER:   # next-token targets come from the token rows
+        dummy = torch.zeros(1, dtype=torch.int32, device=dev)
+        ys, vy = [dummy] * T, dummy
+    else:
+        ys, vy = [up(y) for y in inp["train_y"]], up(inp["val_y"])
+    P = M.Problem(desc_of(cfg))
+    d_eta = torch.empty(W.n_eta(cfg), device=dev)
+    vloss = torch.empty(1, device=dev)
+    ws = P.workspace(P.mfmg_query_sizes(T).workspace_bytes)
+    stream = torch.cuda.current_stream()
+
+    def call():
+        return P.mfmg_meta_grad(theta0, None, eta, xs, ys, vx, vy, d_eta, vloss, ws=ws)
+
+    for _ in range(args.warmup):
+        peak = call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        peak = call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] {name}: {ms:.3f} ms per meta-gradient")
+    print(json.dumps({
+        "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
+        "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.PREC_BF16 else "f32",
+        "data": "synthetic (seeded, see workloads/)",
+        "config": {"workload": WORKLOADS[name], "name": name, "T": T},
+        "peak_bytes": peak, "roofline": None, "cpu_baseline": None,
+        "d_eta_finite": bool(torch.isfinite(d_eta).all().item())}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -261,6 +334,9 @@ def main():
                     help="write the HBM counter summary of --pmc-class from two rocprofv3 "
                          "--pmc runs (made with --copy-bytes) and exit; no GPU needed")
     ap.add_argument("--pmc-class", default="dual_bwd_weight_gemm_reverse")
+    ap.add_argument("--config", default="c5_mlp_relu_8x4096", choices=list(W.CONFIGS),
+                    help="workload; the default (c5) line carries the roofline, the memory "
+                         "sweep and the CPU baseline, the others throughput only")
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
     args = ap.parse_args()
     if args.pmc_summary:
@@ -271,6 +347,9 @@ def main():
         print(f"bench.py measures one GPU: the meta-gradient path is single-device "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
+    if args.config != W.C5.name:
+        bench_config(args.config, args)
+        return
 
     import torch
     from paper_2505_00793_amd import _lib as M

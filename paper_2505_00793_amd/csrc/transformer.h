@@ -5,7 +5,7 @@
 
 namespace mfmg {
 
-constexpr int LN_ROWS_PER_WAVE = 8;
+constexpr int LN_CHUNK = 64;  // rows per partial column sum of the LayerNorm backward
 constexpr int LN_MAX_D = 1024;
 constexpr int TOKEN_SORT_MAX = 8192;
 constexpr int META_ROWS_PER_BLOCK = 128;
@@ -29,7 +29,7 @@ struct LnBwdArgs {
   const float* g;  const float* gd;
   const float* dh_in; const float* dhd_in;   // residual-stream gradient entering
   float* dh_out; float* dhd_out;             // dh_in + dx (may alias dh_in)
-  float* partial;                            // [ln_bwd_parts(N)][4][d]
+  float* partial;                            // [ln_bwd_parts(N)][4][d] column-sum partials
   int N, d, dual;
 };
 

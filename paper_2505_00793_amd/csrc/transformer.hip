@@ -108,95 +108,115 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(LnArgs a) {
 //   qd = gd dy + g dyd,
 //   Ad = qd - mean(qd) - xhd mean(xh q) - xh (mean(xhd q) + mean(xh qd)),
 //   dxd = rstd' A + rstd Ad.
-// Per-block partial column sums of dy xh, dy and their tangents
-// (dyd xh + dy xhd, dyd) feed the parameter epilogue of g and b.
+// The column sums of dy xh, dy and their tangents (dyd xh + dy xhd, dyd), the
+// gradients of g and b, come from ln_colsum_kernel.
 // ------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) ln_bwd_kernel(LnBwdArgs a) {
-  const int wave = threadIdx.x >> 6;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  if (row >= a.N) return;
   const int d = a.d;
-  // each block: 4 waves x LN_ROWS rows; partial sums per block in a.partial
-  float pg[LN_MAXPL], pb[LN_MAXPL], pgd[LN_MAXPL], pbd[LN_MAXPL];
-  int cnt = 0;
+  const long base = (long)row * d;
+  const float rstd = a.rstd[row];
+  float xh[LN_MAXPL], dy[LN_MAXPL], q[LN_MAXPL];
+  float mq = 0.f, mxq = 0.f;
   for (int j = lane, k = 0; j < d; j += 64, ++k) {
-    pg[k] = pb[k] = pgd[k] = pbd[k] = 0.f;
-    cnt = k + 1;
+    xh[k] = a.xh[base + j];
+    dy[k] = a.dy[base + j];
+    q[k] = a.g[j] * dy[k];
+    mq += q[k];
+    mxq += xh[k] * q[k];
   }
-  for (int rr = 0; rr < LN_ROWS_PER_WAVE; ++rr) {
-    const int row = (blockIdx.x * 4 + wave) * LN_ROWS_PER_WAVE + rr;
-    if (row >= a.N) break;
-    const long base = (long)row * d;
-    const float rstd = a.rstd[row];
-    float xh[LN_MAXPL], dy[LN_MAXPL], q[LN_MAXPL];
-    float mq = 0.f, mxq = 0.f;
+  mq = wave_sum(mq) / d;
+  mxq = wave_sum(mxq) / d;
+  float xhd[LN_MAXPL], qd[LN_MAXPL];
+  float mqd = 0.f, mxdq = 0.f, mxqd = 0.f;
+  if (a.dual) {
     for (int j = lane, k = 0; j < d; j += 64, ++k) {
-      xh[k] = a.xh[base + j];
-      dy[k] = a.dy[base + j];
-      q[k] = a.g[j] * dy[k];
-      mq += q[k];
-      mxq += xh[k] * q[k];
+      xhd[k] = a.xhd[base + j];
+      qd[k] = a.gd[j] * dy[k] + a.g[j] * a.dyd[base + j];
+      mqd += qd[k];
+      mxdq += xhd[k] * q[k];
+      mxqd += xh[k] * qd[k];
     }
-    mq = wave_sum(mq) / d;
-    mxq = wave_sum(mxq) / d;
-    float xhd[LN_MAXPL], dyd[LN_MAXPL], qd[LN_MAXPL];
-    float mqd = 0.f, mxdq = 0.f, mxqd = 0.f;
+    mqd = wave_sum(mqd) / d;
+    mxdq = wave_sum(mxdq) / d;
+    mxqd = wave_sum(mxqd) / d;
+  }
+  const float rstdd = a.dual ? -rstd * rstd * a.c[row] : 0.f;
+  for (int j = lane, k = 0; j < d; j += 64, ++k) {
+    const float A = q[k] - mq - xh[k] * mxq;
+    a.dh_out[base + j] = (a.dh_in ? a.dh_in[base + j] : 0.f) + rstd * A;
     if (a.dual) {
-      for (int j = lane, k = 0; j < d; j += 64, ++k) {
-        xhd[k] = a.xhd[base + j];
-        dyd[k] = a.dyd[base + j];
-        qd[k] = a.gd[j] * dy[k] + a.g[j] * dyd[k];
-        mqd += qd[k];
-        mxdq += xhd[k] * q[k];
-        mxqd += xh[k] * qd[k];
-      }
-      mqd = wave_sum(mqd) / d;
-      mxdq = wave_sum(mxdq) / d;
-      mxqd = wave_sum(mxqd) / d;
-    }
-    const float rstdd = a.dual ? -rstd * rstd * a.c[row] : 0.f;
-    for (int j = lane, k = 0; j < d; j += 64, ++k) {
-      const float A = q[k] - mq - xh[k] * mxq;
-      a.dh_out[base + j] = (a.dh_in ? a.dh_in[base + j] : 0.f) + rstd * A;
-      pg[k] += dy[k] * xh[k];
-      pb[k] += dy[k];
-      if (a.dual) {
-        const float Ad = qd[k] - mqd - xhd[k] * mxq - xh[k] * (mxdq + mxqd);
-        a.dhd_out[base + j] = (a.dhd_in ? a.dhd_in[base + j] : 0.f) + rstdd * A + rstd * Ad;
-        pgd[k] += dyd[k] * xh[k] + dy[k] * xhd[k];
-        pbd[k] += dyd[k];
-      }
+      const float Ad = qd[k] - mqd - xhd[k] * mxq - xh[k] * (mxdq + mxqd);
+      a.dhd_out[base + j] = (a.dhd_in ? a.dhd_in[base + j] : 0.f) + rstdd * A + rstd * Ad;
     }
   }
-  // partial[(block * 4 + wave)][4][d]
-  float* P = a.partial + (long)(blockIdx.x * 4 + wave) * 4 * d;
-  for (int j = lane, k = 0; j < d; j += 64, ++k) {
-    P[j] = pg[k];
-    P[d + j] = pb[k];
-    P[2 * d + j] = pgd[k];
-    P[3 * d + j] = pbd[k];
-  }
-  (void)cnt;
 }
 
-// Column sums of the per-wave partials in a fixed order, then the parameter
+// Column sums over a chunk of LN_CHUNK rows: partial[chunk][4][d] = sums of
+// dy xh, dy, dyd xh + dy xhd, dyd.  Block: 64 columns x 4 row phases; each
+// phase sums every fourth row of the chunk, then the four are added in order.
+__global__ void __launch_bounds__(256) ln_colsum_kernel(LnBwdArgs a) {
+  __shared__ float red[4][4][64];
+  const int c = threadIdx.x & 63, ph = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + c;
+  const int r0 = blockIdx.y * LN_CHUNK;
+  const int r1 = min(a.N, r0 + LN_CHUNK);
+  float sg = 0.f, sb = 0.f, sgd = 0.f, sbd = 0.f;
+  if (j < a.d) {
+    for (int r = r0 + ph; r < r1; r += 4) {
+      const long o = (long)r * a.d + j;
+      const float dy = a.dy[o], xh = a.xh[o];
+      sg += dy * xh;
+      sb += dy;
+      if (a.dual) {
+        const float dyd = a.dyd[o];
+        sgd += dyd * xh + dy * a.xhd[o];
+        sbd += dyd;
+      }
+    }
+  }
+  red[ph][0][c] = sg;
+  red[ph][1][c] = sb;
+  red[ph][2][c] = sgd;
+  red[ph][3][c] = sbd;
+  __syncthreads();
+  if (ph == 0 && j < a.d) {
+    float* P = a.partial + (long)blockIdx.y * 4 * a.d;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) P[k * a.d + j] = ((red[0][k][c] + red[1][k][c]) + red[2][k][c]) + red[3][k][c];
+  }
+}
+
+// Column sums of the chunk partials in a fixed order (chunk phase p sums chunks
+// p, p + 4, ...; the four phases are added in order), then the parameter
 // epilogue on g (offset g_off) and b (offset b_off).
 template <typename T>
 __global__ void __launch_bounds__(256) ln_param_kernel(const float* __restrict__ partial,
                                                        int nparts, int d, long g_off, long b_off,
                                                        ParamArgs<T> P, float* out_g,
                                                        float* out_b) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= d) return;
-  float sg = 0.f, sb = 0.f, sgd = 0.f, sbd = 0.f;
-  for (int p = 0; p < nparts; ++p) {
-    const float* Pp = partial + (long)p * 4 * d;
-    sg += Pp[j];
-    sb += Pp[d + j];
-    sgd += Pp[2 * d + j];
-    sbd += Pp[3 * d + j];
+  __shared__ float red[4][4][64];
+  const int c = threadIdx.x & 63, ph = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + c;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < d) {
+    for (int p = ph; p < nparts; p += 4) {
+      const float* Pp = partial + (long)p * 4 * d;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) s[k] += Pp[k * d + j];
+    }
   }
-  const float cg = param_elem(P, g_off + j, sg, sgd);
-  const float cb = param_elem(P, b_off + j, sb, sbd);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) red[ph][k][c] = s[k];
+  __syncthreads();
+  if (ph != 0 || j >= d) return;
+  float t[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) t[k] = ((red[0][k][c] + red[1][k][c]) + red[2][k][c]) + red[3][k][c];
+  const float cg = param_elem(P, g_off + j, t[0], t[2]);
+  const float cb = param_elem(P, b_off + j, t[1], t[3]);
   if (out_g) out_g[j] = cg;
   if (out_b) out_b[j] = cb;
 }
@@ -481,15 +501,20 @@ hipError_t ln_fwd(const LnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-int ln_bwd_parts(int N) { return cdivl(N, 4 * LN_ROWS_PER_WAVE) * 4; }
+int ln_bwd_parts(int N) { return cdivl(N, LN_CHUNK); }
 
 template <typename T>
 hipError_t ln_bwd(const LnBwdArgs& a, long g_off, long b_off, const ParamArgs<T>& P,
                   float* out_g, float* out_b, hipStream_t s) {
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdivl(a.N, 4 * LN_ROWS_PER_WAVE)), dim3(256), 0, s, a);
+  if (a.N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ln_param_kernel<T>, dim3(cdivl(a.d, 256)), dim3(256), 0, s, a.partial,
+  hipLaunchKernelGGL(ln_colsum_kernel, dim3(cdivl(a.d, 64), ln_bwd_parts(a.N)), dim3(256), 0, s,
+                     a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(ln_param_kernel<T>, dim3(cdivl(a.d, 64)), dim3(256), 0, s, a.partial,
                      ln_bwd_parts(a.N), a.d, g_off, b_off, P, out_g, out_b);
   return hipGetLastError();
 }
