@@ -132,6 +132,10 @@ SMALL: Dict[str, Config] = {
                       val_rows=136, T=3),
     "c5_mid_r8": C5.with_(name="c5_mid_r8", cfg_id=111, widths=(1544, 2056, 1032, 40), rows=1544,
                           val_rows=520, T=2),
+    # more 128 x 128 output tiles than compute units (two tiles for some
+    # persistent workgroups), ragged rows, columns and k
+    "c5_rag2": C5.with_(name="c5_rag2", cfg_id=112, widths=(2056, 2312, 40), rows=520,
+                        val_rows=264, T=2),
     "c4_small": C4.with_(name="c4_small", cfg_id=104, d_model=64, n_heads=4, d_ff=128, vocab=97,
                          seq=24, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2),
 }
