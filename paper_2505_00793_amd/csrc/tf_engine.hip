@@ -149,7 +149,8 @@ struct Act {  // one inner step at up to maxB sequences (the dynamic memory)
   T *dZ1, *dZ1T, *dZ1d, *dZ1dT;
   T *dOh, *dOhT, *dOdh, *dOdhT;
   float *lnpart;
-  int *perm, *run_start, *run_len, *tok2run;
+  TokenSegs ts;
+  float* epart;
   float* loss_rows;
   float *cs, *sn;
 };
@@ -212,10 +213,13 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
   a.dOh = OPT(BH * hrow); a.dOhT = OPT(BH * hcol);
   a.dOdh = OPT(BH * hrow); a.dOdhT = OPT(BH * hcol);
   a.lnpart = F32((long)ln_bwd_parts((int)N) * 4 * d);
-  a.perm = c.take<int>(N);
-  a.run_start = c.take<int>(N);
-  a.run_len = c.take<int>(N);
-  a.tok2run = c.take<int>(y.V);
+  const long nsm = embed_segments_max((int)N);
+  a.ts.perm = c.take<int>(N);
+  a.ts.seg_start = c.take<int>(nsm + 1);
+  a.ts.seg_tok = c.take<int>(nsm);
+  a.ts.nseg = c.take<int>(1);
+  a.ts.tok2seg = c.take<int>(y.V);
+  a.epart = F32(nsm * 2 * d);
   a.loss_rows = F32(N);
   a.cs = F32((long)S * y.dh / 2);
   a.sn = F32((long)S * y.dh / 2);
@@ -646,11 +650,11 @@ struct TfEng {
                      out ? out->ln[b][0] : nullptr, out ? out->ln[b][1] : nullptr));
     }
     // embedding rows
-    HC(sort_tokens(a.ids, N, y.V, a.perm, a.run_start, a.run_len, a.tok2run, s));
+    HC(sort_tokens(a.ids, N, y.V, a.ts, s));
     EmbedGradArgs eg;
-    eg.dh = a.dh; eg.dhd = dual ? a.dhd : nullptr; eg.perm = a.perm; eg.run_len = a.run_len;
-    eg.tok2run = a.tok2run; eg.emb_off = y.emb; eg.outE = out ? out->emb : nullptr;
-    eg.V = y.V; eg.d = d;
+    eg.dh = a.dh; eg.dhd = dual ? a.dhd : nullptr; eg.ts = a.ts; eg.part = a.epart;
+    eg.emb_off = y.emb; eg.outE = out ? out->emb : nullptr;
+    eg.V = y.V; eg.d = d; eg.N = N;
     return embed_grad<T>(eg, P, s);
   }
 };

@@ -8,6 +8,7 @@ namespace mfmg {
 constexpr int LN_CHUNK = 64;  // rows per partial column sum of the LayerNorm backward
 constexpr int LN_MAX_D = 1024;
 constexpr int TOKEN_SORT_MAX = 8192;
+constexpr int EMB_SEG = 32;   // positions per embedding-gradient segment
 constexpr int META_ROWS_PER_BLOCK = 128;
 constexpr int META_MAX_HIDDEN = 256;
 
@@ -52,12 +53,24 @@ struct SoftmaxArgs {
   float scale;
 };
 
+// Token positions sorted by id are cut into segments: maximal runs of one id,
+// split further at every multiple of EMB_SEG in the sorted order, so that a
+// segment holds at most EMB_SEG positions of one token.
+struct TokenSegs {
+  int* perm;       // [N] positions in ascending (id, position) order
+  int* seg_start;  // [embed_segments_max(N) + 1] first sorted index of each segment; sentinel
+  int* seg_tok;    // [embed_segments_max(N)] token id of each segment
+  int* nseg;       // [1] number of segments
+  int* tok2seg;    // [V] first segment of each token, -1 if absent
+};
+
 struct EmbedGradArgs {
   const float* dh; const float* dhd;         // [N][d] gradient at the embedding output
-  const int* perm; const int* run_len; const int* tok2run;
+  TokenSegs ts;
+  float* part;                               // [embed_segments_max(N)][2][d] segment sums
   long emb_off;
   float* outE;                               // operand copy of the new rows (fp32 [V][d]) or null
-  int V, d;
+  int V, d, N;
 };
 
 hipError_t split_tokens(const int* tok, int B, int S, int V, int* ids, int* labels,
@@ -75,8 +88,8 @@ hipError_t rope_merge(const RopeArgs& a, hipStream_t s);
 hipError_t softmax_fwd(const SoftmaxArgs& a, hipStream_t s);
 hipError_t softmax_bwd(const SoftmaxArgs& a, hipStream_t s);
 bool sort_tokens_fits(int N);
-hipError_t sort_tokens(const int* ids, int N, int V, int* perm, int* run_start, int* run_len,
-                       int* tok2run, hipStream_t s);
+int embed_segments_max(int N);
+hipError_t sort_tokens(const int* ids, int N, int V, const TokenSegs& ts, hipStream_t s);
 template <typename T>
 hipError_t embed_grad(const EmbedGradArgs& a, const ParamArgs<T>& P, hipStream_t s);
 hipError_t meta_out(const float* hid, int rows, int hdim, const float* w2, const float* b2,

@@ -339,27 +339,32 @@ __global__ void __launch_bounds__(256) softmax_bwd_kernel(SoftmaxArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// Embedding gradient.  The token ids of a batch are sorted once (bitonic sort of
-// (id, position) pairs in one workgroup), giving runs of equal ids; each
-// vocabulary row then sums the rows of its run in position order, which keeps
-// the scatter-add deterministic even for the Zipf-hot ids.
+// Embedding gradient.  The token ids of a batch are sorted (bitonic sort of
+// (id, position) pairs in one workgroup) and the sorted positions cut into
+// segments of at most EMB_SEG positions of one id.  One wave sums each
+// segment's rows, and each vocabulary row then adds its segments' sums in
+// order: a deterministic scatter-add whose work is spread evenly even for the
+// Zipf-hot ids.
 // ------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(1024) sort_tokens_kernel(const int* __restrict__ ids, int N,
-                                                           int V, int* perm, int* run_start,
-                                                           int* run_len, int* tok2run) {
+                                                           int V, TokenSegs ts) {
   extern __shared__ unsigned long long key[];
   int P2 = 1;
   while (P2 < N) P2 <<= 1;
-  for (int i = threadIdx.x; i < P2; i += blockDim.x) {
+  int* scan = reinterpret_cast<int*>(key + P2);   // [1024] per-thread segment counts
+  __shared__ int n_valid;
+  const int t = threadIdx.x;
+  for (int i = t; i < P2; i += blockDim.x) {
     const unsigned long long id = i < N ? (unsigned long long)(unsigned)(ids[i] < 0 ? V : ids[i])
                                         : 0xffffffffull;
     key[i] = (id << 32) | (unsigned)i;
   }
-  for (int v = threadIdx.x; v < V; v += blockDim.x) tok2run[v] = -1;
+  for (int v = t; v < V; v += blockDim.x) ts.tok2seg[v] = -1;
+  if (t == 0) n_valid = 0;
   __syncthreads();
   for (int k = 2; k <= P2; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = threadIdx.x; i < P2; i += blockDim.x) {
+      for (int i = t; i < P2; i += blockDim.x) {
         const int ixj = i ^ j;
         if (ixj > i) {
           const bool up = (i & k) == 0;
@@ -373,24 +378,84 @@ __global__ void __launch_bounds__(1024) sort_tokens_kernel(const int* __restrict
       __syncthreads();
     }
   }
-  for (int i = threadIdx.x; i < N; i += blockDim.x) perm[i] = (int)(key[i] & 0xffffffffu);
-  // run heads
-  for (int i = threadIdx.x; i < N; i += blockDim.x) {
-    const unsigned id = (unsigned)(key[i] >> 32);
-    if (id >= (unsigned)V) continue;
-    if (i == 0 || (unsigned)(key[i - 1] >> 32) != id) {
-      int e = i + 1;
-      while (e < N && (unsigned)(key[e] >> 32) == id) ++e;
-      tok2run[id] = i;
-      run_start[i] = i;
-      run_len[i] = e - i;
+  for (int i = t; i < N; i += blockDim.x) ts.perm[i] = (int)(key[i] & 0xffffffffu);
+  // Segment heads: the first sorted index of a run of one id, and every
+  // multiple of EMB_SEG inside a run.  Ids >= V (ignored positions) sort last.
+  auto tok = [&](int i) { return (unsigned)(key[i] >> 32); };
+  auto head = [&](int i) {
+    return i < N && tok(i) < (unsigned)V &&
+           (i == 0 || tok(i - 1) != tok(i) || i % EMB_SEG == 0);
+  };
+  const int C = (P2 + 1023) / 1024;   // sorted indices per thread
+  int cnt = 0;
+  for (int c = 0; c < C; ++c) {
+    const int i = t * C + c;
+    if (head(i)) ++cnt;
+    if (i < N && tok(i) < (unsigned)V && (i + 1 == N || tok(i + 1) >= (unsigned)V)) n_valid = i + 1;
+  }
+  scan[t] = cnt;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {   // inclusive scan of the counts
+    const int add = t >= off ? scan[t - off] : 0;
+    __syncthreads();
+    scan[t] += add;
+    __syncthreads();
+  }
+  int idx = scan[t] - cnt;
+  for (int c = 0; c < C; ++c) {
+    const int i = t * C + c;
+    if (head(i)) {
+      ts.seg_start[idx] = i;
+      ts.seg_tok[idx] = (int)tok(i);
+      if (i == 0 || tok(i - 1) != tok(i)) ts.tok2seg[tok(i)] = idx;
+      ++idx;
+    }
+  }
+  if (t == 0) {
+    ts.nseg[0] = scan[1023];
+    ts.seg_start[scan[1023]] = n_valid;   // end of the last segment
+  }
+}
+
+// Sum of dh (and dhd) over the positions of one segment per wave:
+// part[s][0][:] and part[s][1][:].
+__global__ void __launch_bounds__(256) embed_seg_kernel(EmbedGradArgs a) {
+  const int sg = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (sg >= a.ts.nseg[0]) return;
+  const int p0 = a.ts.seg_start[sg], p1 = a.ts.seg_start[sg + 1];
+  const int d = a.d;
+  const bool vec = (d & 3) == 0;
+  for (int j = lane * 4; j < d; j += 256) {
+    const int cnt = min(4, d - j);
+    float g[4] = {0.f, 0.f, 0.f, 0.f}, h[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int p = p0; p < p1; ++p) {
+      const long off = (long)a.ts.perm[p] * d + j;
+      if (vec) {
+        const float4 x = *reinterpret_cast<const float4*>(a.dh + off);
+        g[0] += x.x; g[1] += x.y; g[2] += x.z; g[3] += x.w;
+        if (a.dhd) {
+          const float4 y = *reinterpret_cast<const float4*>(a.dhd + off);
+          h[0] += y.x; h[1] += y.y; h[2] += y.z; h[3] += y.w;
+        }
+      } else {
+        for (int k = 0; k < cnt; ++k) {
+          g[k] += a.dh[off + k];
+          if (a.dhd) h[k] += a.dhd[off + k];
+        }
+      }
+    }
+    float* out = a.part + (long)sg * 2 * d + j;
+    for (int k = 0; k < cnt; ++k) {
+      out[k] = g[k];
+      out[d + k] = h[k];
     }
   }
 }
 
-// g[v][j] = sum over positions n with ids[n] == v of dh[n][j] (tangent too), then
-// the parameter epilogue over every vocabulary row (rows without occurrences
-// get g = 0).
+// g[v][j] = sum over positions n with ids[n] == v of dh[n][j] (tangent too),
+// added up from the token's segment sums in order, then the parameter
+// epilogue over every vocabulary row (rows without occurrences get g = 0).
 template <typename T>
 __global__ void __launch_bounds__(256) embed_grad_kernel(EmbedGradArgs a, ParamArgs<T> P) {
   const long e4 = ((long)blockIdx.x * 256 + threadIdx.x) * 4;  // 4 consecutive j
@@ -399,14 +464,14 @@ __global__ void __launch_bounds__(256) embed_grad_kernel(EmbedGradArgs a, ParamA
   const int v = (int)(e4 / d), j = (int)(e4 % d);
   float g[4] = {0.f, 0.f, 0.f, 0.f}, hv[4] = {0.f, 0.f, 0.f, 0.f}, cv[4];
   const int cnt = min(4, d - j);
-  const int r = a.tok2run[v];
-  if (r >= 0) {
-    const int len = a.run_len[r];
-    for (int i = 0; i < len; ++i) {
-      const long n = a.perm[r + i];
+  const int s0 = a.ts.tok2seg[v];
+  if (s0 >= 0) {
+    const int ns = a.ts.nseg[0];
+    for (int sg = s0; sg < ns && a.ts.seg_tok[sg] == v; ++sg) {
+      const float* in = a.part + (long)sg * 2 * d + j;
       for (int k = 0; k < cnt; ++k) {
-        g[k] += a.dh[n * d + j + k];
-        if (a.dhd) hv[k] += a.dhd[n * d + j + k];
+        g[k] += in[k];
+        hv[k] += in[d + k];
       }
     }
   }
@@ -549,17 +614,22 @@ hipError_t softmax_bwd(const SoftmaxArgs& a, hipStream_t s) {
 
 bool sort_tokens_fits(int N) { return N >= 1 && N <= TOKEN_SORT_MAX; }
 
-hipError_t sort_tokens(const int* ids, int N, int V, int* perm, int* run_start, int* run_len,
-                       int* tok2run, hipStream_t s) {
+int embed_segments_max(int N) { return N + (N + EMB_SEG - 1) / EMB_SEG; }
+
+hipError_t sort_tokens(const int* ids, int N, int V, const TokenSegs& ts, hipStream_t s) {
+  if (!sort_tokens_fits(N)) return hipErrorInvalidValue;
   int P2 = 1;
   while (P2 < N) P2 <<= 1;
-  hipLaunchKernelGGL(sort_tokens_kernel, dim3(1), dim3(1024), P2 * sizeof(unsigned long long), s,
-                     ids, N, V, perm, run_start, run_len, tok2run);
+  hipLaunchKernelGGL(sort_tokens_kernel, dim3(1), dim3(1024),
+                     P2 * sizeof(unsigned long long) + 1024 * sizeof(int), s, ids, N, V, ts);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t embed_grad(const EmbedGradArgs& a, const ParamArgs<T>& P, hipStream_t s) {
+  hipLaunchKernelGGL(embed_seg_kernel, dim3(cdivl(embed_segments_max(a.N), 4)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(embed_grad_kernel<T>, dim3(cdivl((long)a.V * a.d / 4 + 1, 256)), dim3(256), 0,
                      s, a, P);
   return hipGetLastError();
