@@ -191,7 +191,63 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
   if (a.alpha_logits) w = 1.0f / (1.0f + expf(-a.alpha_logits[row]));
   const float scale = w * a.inv_n;
   float loss = 0.0f, ldot = 0.0f;
-  if (a.loss == 1) {
+  const bool vec = (C & 3) == 0 && (a.ld & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(a.Z) & 15) == 0 &&
+                   (!a.dual || ((reinterpret_cast<uintptr_t>(a.Zd) & 15) == 0));
+  if (a.loss == 1 && vec) {
+    // One pass for the log-sum-exp and the tangent dot: per lane a running max
+    // m with se = sum exp(z - m) and sd = sum exp(z - m) zd, rescaled when m
+    // grows; lanes are then combined at the wave's max.
+    float m = -INFINITY, se = 0.0f, sd = 0.0f;
+    for (int c = lane * 4; c < C; c += 256) {
+      const float4 x = *reinterpret_cast<const float4*>(z + c);
+      const float mn = fmaxf(m, fmaxf(fmaxf(x.x, x.y), fmaxf(x.z, x.w)));
+      if (mn == -INFINITY) continue;
+      const float r = m == mn ? 1.0f : expf(m - mn);
+      const float e0 = expf(x.x - mn), e1 = expf(x.y - mn), e2 = expf(x.z - mn),
+                  e3 = expf(x.w - mn);
+      se = se * r + ((e0 + e1) + (e2 + e3));
+      if (a.dual) {
+        const float4 xd = *reinterpret_cast<const float4*>(zd + c);
+        sd = sd * r + ((e0 * xd.x + e1 * xd.y) + (e2 * xd.z + e3 * xd.w));
+      }
+      m = mn;
+    }
+    const float M = wave_max(m);
+    const float f = m == -INFINITY ? 0.0f : expf(m - M);
+    const float SE = wave_sum(se * f);
+    const float lse = M + logf(SE);
+    int y = a.labels[row];
+    if (y < 0 || y >= C) {  // invalid label: NaN loss, no target term
+      y = -1;
+      loss = NAN;
+    } else {
+      loss = lse - z[y];
+    }
+    float sdot = 0.0f;
+    if (a.dual) {
+      sdot = wave_sum(sd * f) / SE;   // sum_c p_c zd_c
+      ldot = y >= 0 ? sdot - zd[y] : NAN;
+    }
+    for (int c = lane * 4; c < C; c += 256) {
+      const float4 x = *reinterpret_cast<const float4*>(z + c);
+      const float xs[4] = {x.x, x.y, x.z, x.w};
+      float dv[4], ddv[4];
+      float xds[4] = {0.f, 0.f, 0.f, 0.f};
+      if (a.dual) {
+        const float4 xd = *reinterpret_cast<const float4*>(zd + c);
+        xds[0] = xd.x; xds[1] = xd.y; xds[2] = xd.z; xds[3] = xd.w;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float p = expf(xs[k] - lse);
+        dv[k] = scale * (p - (c + k == y ? 1.0f : 0.0f));
+        ddv[k] = scale * p * (xds[k] - sdot);
+      }
+      store4(a.d + (long)row * a.ld + c, dv[0], dv[1], dv[2], dv[3]);
+      if (a.dual) store4(a.dd + (long)row * a.ld + c, ddv[0], ddv[1], ddv[2], ddv[3]);
+    }
+  } else if (a.loss == 1) {
     float mx = -INFINITY;
     for (int c = lane; c < C; c += 64) mx = fmaxf(mx, z[c]);
     mx = wave_max(mx);
