@@ -14,16 +14,34 @@ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 // ------------------------------------------------------------------------------------
 // float32 [rows][cols] -> operand copies in both layouts, through a 64x64 LDS tile.
 // ------------------------------------------------------------------------------------
+// Several matrices of one shape per launch: z = job * batch + batch index.
 template <typename T>
-__global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ src, int rows,
-                                                      int cols, int lds, T* dst, int ldd, T* dstT,
-                                                      int lddT, long s_src, long s_dst,
-                                                      long s_dstT) {
+struct ConvPtrs {
+  const float* src;
+  T* dst;
+  T* dstT;
+};
+template <typename T>
+__device__ __forceinline__ ConvPtrs<T> conv_ptrs(const ConvJobs<T>& J, int batch, long s_src,
+                                                 long s_dst, long s_dstT) {
+  const int job = blockIdx.z / batch, bz = blockIdx.z - job * batch;
+  ConvPtrs<T> p;
+  p.src = J.src[job] + bz * s_src;
+  p.dst = J.dst[job] ? J.dst[job] + bz * s_dst : nullptr;
+  p.dstT = J.dstT[job] ? J.dstT[job] + bz * s_dstT : nullptr;
+  return p;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) convert_kernel(ConvJobs<T> J, int batch, int rows,
+                                                      int cols, int lds, int ldd, int lddT,
+                                                      long s_src, long s_dst, long s_dstT) {
   __shared__ float tile[64][65];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  src += blockIdx.z * s_src;
-  if (dst) dst += blockIdx.z * s_dst;
-  if (dstT) dstT += blockIdx.z * s_dstT;
+  const ConvPtrs<T> P = conv_ptrs(J, batch, s_src, s_dst, s_dstT);
+  const float* src = P.src;
+  T* dst = P.dst;
+  T* dstT = P.dstT;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tx;
@@ -47,15 +65,15 @@ __global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ 
 // rows at a time.  Requires lds, ldd, lddT and the batch strides to be
 // multiples of 4 and the arrays aligned to their 4-element width.
 template <typename T>
-__global__ void __launch_bounds__(256) convert_vec_kernel(const float* __restrict__ src, int rows,
-                                                          int cols, int lds, T* dst, int ldd,
-                                                          T* dstT, int lddT, long s_src,
-                                                          long s_dst, long s_dstT) {
+__global__ void __launch_bounds__(256) convert_vec_kernel(ConvJobs<T> J, int batch, int rows,
+                                                          int cols, int lds, int ldd, int lddT,
+                                                          long s_src, long s_dst, long s_dstT) {
   __shared__ __attribute__((aligned(16))) float tile[64][68];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  src += blockIdx.z * s_src;
-  if (dst) dst += blockIdx.z * s_dst;
-  if (dstT) dstT += blockIdx.z * s_dstT;
+  const ConvPtrs<T> P = conv_ptrs(J, batch, s_src, s_dst, s_dstT);
+  const float* src = P.src;
+  T* dst = P.dst;
+  T* dstT = P.dstT;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int c = c0 + tx * 4;
   for (int i = ty; i < 64; i += 16) {
@@ -560,23 +578,39 @@ hipError_t copy(const float* src, float* dst, long n, hipStream_t s) {
 }
 
 template <typename T>
+hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, int ldd, int lddT,
+                            hipStream_t s, int batch, long s_src, long s_dst, long s_dstT) {
+  if (J.n < 0 || J.n > CONV_MAX_JOBS) return hipErrorInvalidValue;
+  if (rows <= 0 || cols <= 0 || batch <= 0 || J.n == 0) return hipSuccess;
+  for (int k = 0; k < J.n; ++k)
+    if (!J.src[k]) return hipErrorInvalidValue;
+  dim3 grid(cdiv(cols, 64), cdiv(rows, 64), batch * J.n);
+  const auto al = [](const void* q, uintptr_t a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+  const uintptr_t aw = 4 * sizeof(T);  // alignment of 4 elements
+  bool vec = (lds % 4) == 0 && (s_src % 4) == 0;
+  for (int k = 0; k < J.n; ++k)
+    vec = vec && al(J.src[k], 16) &&
+          (!J.dst[k] || ((ldd % 4) == 0 && (s_dst % 4) == 0 && al(J.dst[k], aw))) &&
+          (!J.dstT[k] || ((lddT % 4) == 0 && (s_dstT % 4) == 0 && al(J.dstT[k], aw)));
+  if (vec)
+    hipLaunchKernelGGL(convert_vec_kernel<T>, grid, dim3(256), 0, s, J, batch, rows, cols, lds, ldd,
+                       lddT, s_src, s_dst, s_dstT);
+  else
+    hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, J, batch, rows, cols, lds, ldd,
+                       lddT, s_src, s_dst, s_dstT);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
                           T* dstT, int lddT, hipStream_t s, int batch, long s_src, long s_dst,
                           long s_dstT) {
-  if (rows <= 0 || cols <= 0 || batch <= 0) return hipSuccess;
-  dim3 grid(cdiv(cols, 64), cdiv(rows, 64), batch);
-  const auto al = [](const void* q, uintptr_t a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
-  const uintptr_t aw = 4 * sizeof(T);  // alignment of 4 elements
-  const bool vec = (lds % 4) == 0 && (s_src % 4) == 0 && al(src, 16) &&
-                   (!dst || ((ldd % 4) == 0 && (s_dst % 4) == 0 && al(dst, aw))) &&
-                   (!dstT || ((lddT % 4) == 0 && (s_dstT % 4) == 0 && al(dstT, aw)));
-  if (vec)
-    hipLaunchKernelGGL(convert_vec_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
-                       dstT, lddT, s_src, s_dst, s_dstT);
-  else
-    hipLaunchKernelGGL(convert_kernel<T>, grid, dim3(256), 0, s, src, rows, cols, lds, dst, ldd,
-                       dstT, lddT, s_src, s_dst, s_dstT);
-  return hipGetLastError();
+  ConvJobs<T> J;
+  J.n = 1;
+  J.src[0] = src;
+  J.dst[0] = dst;
+  J.dstT[0] = dstT;
+  return convert_matrices<T>(J, rows, cols, lds, ldd, lddT, s, batch, s_src, s_dst, s_dstT);
 }
 
 template <typename T>
@@ -659,6 +693,8 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   return hipGetLastError();
 }
 
+template hipError_t convert_matrices<bf16_t>(const ConvJobs<bf16_t>&, int, int, int, int, int, hipStream_t, int, long, long, long);
+template hipError_t convert_matrices<float>(const ConvJobs<float>&, int, int, int, int, int, hipStream_t, int, long, long, long);
 template hipError_t convert_matrix<bf16_t>(const float*, int, int, int, bf16_t*, int, bf16_t*, int, hipStream_t, int, long, long, long);
 template hipError_t convert_matrix<float>(const float*, int, int, int, float*, int, float*, int, hipStream_t, int, long, long, long);
 template hipError_t bias_reduce<bf16_t>(const bf16_t*, const bf16_t*, int, int, const ParamArgs<bf16_t>&, hipStream_t);

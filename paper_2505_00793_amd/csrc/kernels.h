@@ -188,6 +188,21 @@ hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst,
                           T* dstT, int lddT, hipStream_t s, int batch = 1, long s_src = 0,
                           long s_dst = 0, long s_dstT = 0);
 
+// The same for up to CONV_MAX_JOBS matrices of one shape and layout in one
+// launch (job k: src[k] -> dst[k], dstT[k]; src[k] non-null).
+constexpr int CONV_MAX_JOBS = 6;
+template <typename T>
+struct ConvJobs {
+  int n = 0;
+  const float* src[CONV_MAX_JOBS] = {};
+  T* dst[CONV_MAX_JOBS] = {};
+  T* dstT[CONV_MAX_JOBS] = {};
+};
+template <typename T>
+hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, int ldd, int lddT,
+                            hipStream_t s, int batch = 1, long s_src = 0, long s_dst = 0,
+                            long s_dstT = 0);
+
 // Column sums over rows of dZT [nout][ld] (and dZdT) -> per-parameter epilogue
 // on the bias entries of layer P.layer.
 template <typename T>

@@ -19,6 +19,8 @@
 #include <cstring>
 #include <vector>
 
+#include <initializer_list>
+
 #include "kernels.h"
 #include "tf_engine.h"
 #include "transformer.h"
@@ -317,10 +319,23 @@ struct TfEng {
   static int fl(bool dual, bool ad = true) {
     return G_C1 | (dual ? (G_BD | (ad ? G_AD : 0)) : 0);
   }
-  hipError_t conv(const float* src, int rows, int cols, T* dst, T* dstT, int batch = 1,
-                  long ss = 0, long sd = 0, long sdT = 0) const {
-    return convert_matrix<T>(src, rows, cols, cols, dst, (int)y.ld(cols), dstT, (int)y.ld(rows), s,
-                             batch, ss, sd, sdT);
+  // Up to six matrices of one shape in one launch; jobs with a null source are skipped.
+  struct Job {
+    const float* src;
+    T* dst;
+    T* dstT;
+  };
+  hipError_t convs(std::initializer_list<Job> js, int rows, int cols, int batch = 1, long ss = 0,
+                   long sd = 0, long sdT = 0) const {
+    ConvJobs<T> J;
+    for (const Job& j : js) {
+      if (!j.src) continue;
+      if (J.n == CONV_MAX_JOBS) return hipErrorInvalidValue;
+      J.src[J.n] = j.src; J.dst[J.n] = j.dst; J.dstT[J.n] = j.dstT;
+      ++J.n;
+    }
+    return convert_matrices<T>(J, rows, cols, cols, (int)y.ld(cols), (int)y.ld(rows), s, batch, ss,
+                               sd, sdT);
   }
   hipError_t store(const GemmOperands<T>& o, int flags, float* C, float* Cd, int ldc, long sC,
                    float scale, bool dual) const {
@@ -409,8 +424,8 @@ struct TfEng {
       ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xh1[b]; ln.xhd = a.xhd1[b];
       ln.rstd = a.rs1[b]; ln.c = a.c1[b]; ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
       HC(ln_fwd(ln, s));
-      HC(conv(a.y32, N, d, a.a1[b], a.a1T[b]));
-      if (dual) HC(conv(a.yd32, N, d, a.a1d[b], a.a1dT[b]));
+      HC(convs({{a.y32, a.a1[b], a.a1T[b]}, {dual ? a.yd32 : nullptr, a.a1d[b], a.a1dT[b]}}, N,
+               d));
       // qkv = a1 Wqkv
       HC(store(op(a.a1[b], dual ? a.a1d[b] : nullptr, th.WT[b][0], dual ? v->WT[b][0] : nullptr,
                   (int)y.ld(d), (int)y.ld(d), N, 3 * d, d),
@@ -422,14 +437,11 @@ struct TfEng {
       r.cs = a.cs; r.sn = a.sn; r.N = N; r.S = S; r.H = H; r.dh = dh; r.dual = dual;
       HC(rope_split(r, s));
       const long sh = (long)S * dh;
-      HC(conv(a.Qh, S, dh, a.Q[b], a.QT[b], BH, sh, hrow, hcol));
-      HC(conv(a.Kh, S, dh, a.K[b], a.KT[b], BH, sh, hrow, hcol));
-      HC(conv(a.Vh, S, dh, a.Vv[b], a.VT[b], BH, sh, hrow, hcol));
-      if (dual) {
-        HC(conv(a.Qdh, S, dh, a.Qd[b], a.QdT[b], BH, sh, hrow, hcol));
-        HC(conv(a.Kdh, S, dh, a.Kd[b], a.KdT[b], BH, sh, hrow, hcol));
-        HC(conv(a.Vdh, S, dh, a.Vd[b], a.VdT[b], BH, sh, hrow, hcol));
-      }
+      HC(convs({{a.Qh, a.Q[b], a.QT[b]}, {a.Kh, a.K[b], a.KT[b]}, {a.Vh, a.Vv[b], a.VT[b]},
+                {dual ? a.Qdh : nullptr, a.Qd[b], a.QdT[b]},
+                {dual ? a.Kdh : nullptr, a.Kd[b], a.KdT[b]},
+                {dual ? a.Vdh : nullptr, a.Vd[b], a.VdT[b]}},
+               S, dh, BH, sh, hrow, hcol));
       // scores S = scale Q K^T (per head), softmax
       {
         GemmOperands<T> o = op(a.Q[b], dual ? a.Qd[b] : nullptr, a.K[b], dual ? a.Kd[b] : nullptr,
@@ -442,8 +454,8 @@ struct TfEng {
       sm.Sc = a.S32; sm.Scd = a.Sd32; sm.P = a.P32[b]; sm.Pd = a.Pd32[b];
       sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
       HC(softmax_fwd(sm, s));
-      HC(conv(a.P32[b], S, S, a.Pb[b], a.PbT[b], BH, (long)S * S, pS, pS));
-      if (dual) HC(conv(a.Pd32[b], S, S, a.Pdb[b], a.PdbT[b], BH, (long)S * S, pS, pS));
+      HC(convs({{a.P32[b], a.Pb[b], a.PbT[b]}, {dual ? a.Pd32[b] : nullptr, a.Pdb[b], a.PdbT[b]}},
+               S, S, BH, (long)S * S, pS, pS));
       // O = P V (per head) -> token-major operands
       {
         GemmOperands<T> o = op(a.Pb[b], dual ? a.Pdb[b] : nullptr, a.VT[b], dual ? a.VdT[b] : nullptr,
@@ -470,8 +482,8 @@ struct TfEng {
       ln.gd = dual ? v->ln[b][2] : nullptr; ln.bd = dual ? v->ln[b][3] : nullptr;
       ln.xh = a.xh2[b]; ln.xhd = a.xhd2[b]; ln.rstd = a.rs2[b]; ln.c = a.c2[b];
       HC(ln_fwd(ln, s));
-      HC(conv(a.y32, N, d, a.a2[b], a.a2T[b]));
-      if (dual) HC(conv(a.yd32, N, d, a.a2d[b], a.a2dT[b]));
+      HC(convs({{a.y32, a.a2[b], a.a2T[b]}, {dual ? a.yd32 : nullptr, a.a2d[b], a.a2dT[b]}}, N,
+               d));
       // A1 = GELU(a2 W1)
       {
         EpiActFwd<T> e;
@@ -501,8 +513,7 @@ struct TfEng {
     ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xhf; ln.xhd = a.xhdf; ln.rstd = a.rsf; ln.c = a.cf;
     ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
     HC(ln_fwd(ln, s));
-    HC(conv(a.y32, N, d, a.af, a.afT));
-    if (dual) HC(conv(a.yd32, N, d, a.afd, a.afdT));
+    HC(convs({{a.y32, a.af, a.afT}, {dual ? a.yd32 : nullptr, a.afd, a.afdT}}, N, d));
     HC(store(op(a.af, dual ? a.afd : nullptr, th.UT, dual ? v->UT : nullptr, (int)y.ld(d),
                 (int)y.ld(d), N, y.V, d),
              fl(dual), a.logits, a.logitsd, y.V, 0, 1.0f, dual));
@@ -560,8 +571,7 @@ struct TfEng {
                    out ? out->lnf[1] : nullptr));
     for (int b = y.L - 1; b >= 0; --b) {
       // ---- MLP: h_out = h_mid + GELU(a2 W1) W2
-      HC(conv(a.dh, N, d, a.dhb, a.dhbT));
-      if (dual) HC(conv(a.dhd, N, d, a.dhdb, a.dhdbT));
+      HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
       HC(gemm_param<T>(op(a.A1T[b], dual ? a.A1dT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), F, d, N),
                        fl(dual), matP(y.w2[b], F, d, out ? out->W[b][3] : nullptr, out ? out->WT[b][3] : nullptr), s));
@@ -584,8 +594,7 @@ struct TfEng {
                      dual ? v->ln[b][2] : nullptr, a.dh, dual ? a.dhd : nullptr, y.ln2g[b], y.ln2b[b],
                      out ? out->ln[b][2] : nullptr, out ? out->ln[b][3] : nullptr));
       // ---- attention: h_mid = h + Attn(LN1(h)) Wo
-      HC(conv(a.dh, N, d, a.dhb, a.dhbT));
-      if (dual) HC(conv(a.dhd, N, d, a.dhdb, a.dhdbT));
+      HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
       HC(gemm_param<T>(op(a.OT[b], dual ? a.OdT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), d, d, N),
                        fl(dual), matP(y.wo[b], d, d, out ? out->W[b][1] : nullptr, out ? out->WT[b][1] : nullptr), s));
@@ -616,8 +625,8 @@ struct TfEng {
       sm.dS = a.dS32; sm.dSd = a.dSd32; sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
       sm.scale = scale;
       HC(softmax_bwd(sm, s));
-      HC(conv(a.dS32, S, S, a.dS, a.dST, BH, (long)S * S, pS, pS));
-      if (dual) HC(conv(a.dSd32, S, S, a.dSd, a.dSdT, BH, (long)S * S, pS, pS));
+      HC(convs({{a.dS32, a.dS, a.dST}, {dual ? a.dSd32 : nullptr, a.dSd, a.dSdT}}, S, S, BH,
+               (long)S * S, pS, pS));
       {  // dQ = dS K
         GemmOperands<T> o = op(a.dS, dual ? a.dSd : nullptr, a.KT[b], dual ? a.KdT[b] : nullptr,
                                (int)y.ld(S), (int)y.ld(S), S, dh, S);
@@ -637,8 +646,8 @@ struct TfEng {
       r.cs = a.cs; r.sn = a.sn; r.N = N; r.S = S; r.H = H; r.dh = dh; r.dual = dual;
       HC(rope_merge(r, s));
       // dqkv operands in the dZ1 buffers (sized for max(F, 3d))
-      HC(conv(a.qkv32, N, 3 * d, a.dZ1, a.dZ1T));
-      if (dual) HC(conv(a.qkvd32, N, 3 * d, a.dZ1d, a.dZ1dT));
+      HC(convs({{a.qkv32, a.dZ1, a.dZ1T}, {dual ? a.qkvd32 : nullptr, a.dZ1d, a.dZ1dT}}, N,
+               3 * d));
       HC(gemm_param<T>(op(a.a1T[b], dual ? a.a1dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), d, 3 * d, N),
                        fl(dual), matP(y.wqkv[b], d, 3 * d, out ? out->W[b][0] : nullptr, out ? out->WT[b][0] : nullptr), s));
