@@ -22,6 +22,8 @@
 //   gemm_nt     everything else (float32, ragged k): register-staged,
 //               double-buffered LDS, 256 threads.
 // Both end in the same staged epilogue.
+#include <type_traits>
+
 #include "kernels.h"
 #include "param_epi.h"
 
@@ -950,9 +952,119 @@ hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------
+// Split-K for backward-weight products with few output tiles and a long k (the
+// token dimension of a transformer's weight gradients): S batched products over
+// k slices write float32 partial sums C1, C2 to the workspace, then a second
+// kernel adds the S slices in order and applies the epilogue (row-major
+// outputs through epi.row, transposed ones through epi.trans).
+// ------------------------------------------------------------------------------------
+int splitk_count(int M, int N, int K) {
+  const int tiles = cdiv(M, 128) * cdiv(N, 128);
+  if (M <= 0 || N <= 0 || tiles >= 192 || K < 1024) return 1;
+  int S = (256 + tiles - 1) / tiles;
+  if (S > 8) S = 8;
+  if (S > K / 256) S = K / 256;
+  while (S > 1 && K % (S * 64) != 0) --S;
+  return S;
+}
+
+// One workgroup per 16 x 64 output tile, one thread per 4 columns of a row;
+// the transposed outputs go through an LDS copy of the tile.
+template <class Epi>
+__global__ void __launch_bounds__(256) splitk_epilogue(const float* __restrict__ P1,
+                                                       const float* __restrict__ P2, int S, int M,
+                                                       int N, Epi epi) {
+  __shared__ float T1[16][68], T2[16][68];
+  const int tiles_n = (N + 63) / 64;
+  const int m0 = (blockIdx.x / tiles_n) * 16, n0 = (blockIdx.x % tiles_n) * 64;
+  const int r = threadIdx.x >> 4, c = (threadIdx.x & 15) * 4;
+  const int m = m0 + r, n = n0 + c;
+  const int cn = min(4, N - n);
+  const long MN = (long)M * N;
+  float c1[4] = {0.f, 0.f, 0.f, 0.f}, c2[4] = {0.f, 0.f, 0.f, 0.f};
+  float t1[4] = {0.f, 0.f, 0.f, 0.f}, t2[4] = {0.f, 0.f, 0.f, 0.f};
+  if (m < M && cn > 0) {
+    const bool vec = cn == 4 && (N & 3) == 0;
+    for (int sp = 0; sp < S; ++sp) {
+      const long off = sp * MN + (long)m * N + n;
+      if (vec) {
+        const float4 x = *reinterpret_cast<const float4*>(P1 + off);
+        c1[0] += x.x; c1[1] += x.y; c1[2] += x.z; c1[3] += x.w;
+        if (P2) {
+          const float4 y = *reinterpret_cast<const float4*>(P2 + off);
+          c2[0] += y.x; c2[1] += y.y; c2[2] += y.z; c2[3] += y.w;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (k < cn) {
+            c1[k] += P1[off + k];
+            if (P2) c2[k] += P2[off + k];
+          }
+      }
+    }
+    epi.row(0, m, n, cn, c1, c2, t1, t2);
+  }
+  const int nT = epi.n_trans();
+  if (nT == 0) return;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    T1[r][c + k] = t1[k];
+    T2[r][c + k] = t2[k];
+  }
+  __syncthreads();
+  // thread: column cc of the tile, rows 4 q .. 4 q + 3
+  const int cc = threadIdx.x >> 2, q = threadIdx.x & 3;
+  const int nn = n0 + cc, mm = m0 + 4 * q;
+  const int cm = min(4, M - mm);
+  if (nn >= N || cm <= 0) return;
+  float v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) v[k] = T1[4 * q + k][cc];
+  epi.trans(0, 0, nn, mm, cm, v);
+  if (nT > 1) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = T2[4 * q + k][cc];
+    epi.trans(1, 0, nn, mm, cm, v);
+  }
+}
+
+template <class E> struct IsParamOp : std::false_type {};
+template <typename T> struct IsParamOp<ParamOp<T>> : std::true_type {};
+
+template <typename T, int FLAGS, class Epi>
+hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipStream_t s) {
+  constexpr bool HC2 = (FLAGS & (G_AD | G_BD)) != 0;
+  const long MN = (long)op.M * op.N;
+  GemmOperands<T> p = op;
+  p.K = op.K / S;
+  p.batch = S;
+  p.sA = p.K;
+  p.sB = p.K;
+  p.ws = nullptr;
+  p.ws_floats = 0;
+  EpiStore e;
+  e.C = op.ws; e.Cd = op.ws + S * MN; e.ldc = op.N; e.sC = MN; e.scale = 1.0f;
+  e.M = op.M; e.N = op.N; e.dual = HC2 ? 1 : 0;
+  hipError_t r = launch<T, FLAGS, 128, 128>(p, StoreOp{e, op.M, op.N}, s);
+  if (r != hipSuccess) return r;
+  const int nb = cdiv(op.M, 16) * cdiv(op.N, 64);
+  hipLaunchKernelGGL((splitk_epilogue<Epi>), dim3(nb), dim3(256), 0, s, op.ws,
+                     HC2 ? op.ws + S * MN : nullptr, S, op.M, op.N, epi);
+  return hipGetLastError();
+}
+
 template <typename T, int FLAGS, class Epi>
 hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   if (op.M <= 0 || op.N <= 0) return hipSuccess;
+  if constexpr (sizeof(T) == 2 && IsParamOp<Epi>::value) {
+    if (op.ws && op.batch == 1) {
+      const int S = splitk_count(op.M, op.N, op.K);
+      if (S > 1 && op.ws_floats >= 2L * S * op.M * op.N)
+        return launch_splitk<T, FLAGS>(op, epi, S, s);
+    }
+  }
   if constexpr (sizeof(T) == 2) {
     // 128 x 128 tiles once they alone fill most of the 256 compute units.
     if (cdiv(op.M, 128) * cdiv(op.N, 128) * op.batch >= 192)
@@ -974,6 +1086,11 @@ hipError_t dispatch(const GemmOperands<T>& op, int flags, const Epi& epi, hipStr
 }
 
 }  // namespace
+
+long gemm_splitk_floats(int M, int N, int K) {
+  const int S = splitk_count(M, N, K);
+  return S > 1 ? 2L * S * M * N : 0;
+}
 
 template <typename T>
 hipError_t gemm_act_fwd(const GemmOperands<T>& op, int flags, const EpiActFwd<T>& epi,

@@ -28,7 +28,16 @@ struct GemmOperands {
   int M, N, K;
   int batch = 1;      // independent products (grid.y); operand z starts at A + z * sA
   long sA = 0, sB = 0;
+  // Optional float32 workspace for split-K (products with few output tiles and
+  // a long k): null, or ws_floats >= gemm_splitk_floats(M, N, K).
+  float* ws = nullptr;
+  long ws_floats = 0;
 };
+
+// Workspace (floats) that the backward-weight product of an M x N output over K
+// uses for split-K when given it; 0 when it runs without (bf16 operands, one
+// batch).
+long gemm_splitk_floats(int M, int N, int K);
 
 // Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
 // ad = act'(z) zd.  Hidden layers store z (and zd) in float32 for the

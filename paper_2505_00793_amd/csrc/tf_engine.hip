@@ -153,6 +153,8 @@ struct Act {  // one inner step at up to maxB sequences (the dynamic memory)
   float *lnpart;
   TokenSegs ts;
   float* epart;
+  float* skws;   // split-K workspace of the weight-gradient products
+  long skws_n;
   float* loss_rows;
   float *cs, *sn;
 };
@@ -222,6 +224,10 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
   a.ts.nseg = c.take<int>(1);
   a.ts.tok2seg = c.take<int>(y.V);
   a.epart = F32(nsm * 2 * d);
+  a.skws_n = std::max({gemm_splitk_floats(F, d, (int)N), gemm_splitk_floats(d, F, (int)N),
+                       gemm_splitk_floats(d, d, (int)N), gemm_splitk_floats(d, 3 * d, (int)N),
+                       gemm_splitk_floats(d, y.V, (int)N)});
+  a.skws = F32(a.skws_n);
   a.loss_rows = F32(N);
   a.cs = F32((long)S * y.dh / 2);
   a.sn = F32((long)S * y.dh / 2);
@@ -314,6 +320,12 @@ struct TfEng {
     o.A = A; o.Ad = Ad; o.B = B; o.Bd = Bd;
     o.lda = lda; o.ldb = ldb;
     o.M = M; o.N = N; o.K = K;
+    return o;
+  }
+  // the split-K workspace for a weight-gradient product
+  GemmOperands<T> wsk(GemmOperands<T> o, const Act<T>& a) const {
+    o.ws = a.skws;
+    o.ws_floats = a.skws_n;
     return o;
   }
   static int fl(bool dual, bool ad = true) {
@@ -560,8 +572,8 @@ struct TfEng {
       return ln_bwd<T>(l, goff, boff, P, og, ob, s);
     };
     // unembedding
-    HC(gemm_param<T>(op(a.afT, dual ? a.afdT : nullptr, a.dzT, dual ? a.dzdT : nullptr,
-                        (int)y.ld(N), (int)y.ld(N), d, y.V, N),
+    HC(gemm_param<T>(wsk(op(a.afT, dual ? a.afdT : nullptr, a.dzT, dual ? a.dzdT : nullptr,
+                        (int)y.ld(N), (int)y.ld(N), d, y.V, N), a),
                      fl(dual), matP(y.unemb, d, y.V, out ? out->U : nullptr, out ? out->UT : nullptr), s));
     HC(store(op(a.dz, dual ? a.dzd : nullptr, th.U, dual ? v->U : nullptr, (int)y.ld(y.V),
                 (int)y.ld(y.V), N, d, y.V),
@@ -572,8 +584,8 @@ struct TfEng {
     for (int b = y.L - 1; b >= 0; --b) {
       // ---- MLP: h_out = h_mid + GELU(a2 W1) W2
       HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
-      HC(gemm_param<T>(op(a.A1T[b], dual ? a.A1dT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
-                          (int)y.ld(N), (int)y.ld(N), F, d, N),
+      HC(gemm_param<T>(wsk(op(a.A1T[b], dual ? a.A1dT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
+                          (int)y.ld(N), (int)y.ld(N), F, d, N), a),
                        fl(dual), matP(y.w2[b], F, d, out ? out->W[b][3] : nullptr, out ? out->WT[b][3] : nullptr), s));
       {
         EpiActBwd<T> e;
@@ -584,8 +596,8 @@ struct TfEng {
                               (int)y.ld(d), (int)y.ld(d), N, F, d),
                            fl(dual), e, s));
       }
-      HC(gemm_param<T>(op(a.a2T[b], dual ? a.a2dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
-                          (int)y.ld(N), (int)y.ld(N), d, F, N),
+      HC(gemm_param<T>(wsk(op(a.a2T[b], dual ? a.a2dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
+                          (int)y.ld(N), (int)y.ld(N), d, F, N), a),
                        fl(dual), matP(y.w1[b], d, F, out ? out->W[b][2] : nullptr, out ? out->WT[b][2] : nullptr), s));
       HC(store(op(a.dZ1, dual ? a.dZ1d : nullptr, th.W[b][2], dual ? v->W[b][2] : nullptr,
                   (int)y.ld(F), (int)y.ld(F), N, d, F),
@@ -595,8 +607,8 @@ struct TfEng {
                      out ? out->ln[b][2] : nullptr, out ? out->ln[b][3] : nullptr));
       // ---- attention: h_mid = h + Attn(LN1(h)) Wo
       HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
-      HC(gemm_param<T>(op(a.OT[b], dual ? a.OdT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
-                          (int)y.ld(N), (int)y.ld(N), d, d, N),
+      HC(gemm_param<T>(wsk(op(a.OT[b], dual ? a.OdT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
+                          (int)y.ld(N), (int)y.ld(N), d, d, N), a),
                        fl(dual), matP(y.wo[b], d, d, out ? out->W[b][1] : nullptr, out ? out->WT[b][1] : nullptr), s));
       {
         EpiHeadSplit<T> e;
@@ -648,8 +660,8 @@ struct TfEng {
       // dqkv operands in the dZ1 buffers (sized for max(F, 3d))
       HC(convs({{a.qkv32, a.dZ1, a.dZ1T}, {dual ? a.qkvd32 : nullptr, a.dZ1d, a.dZ1dT}}, N,
                3 * d));
-      HC(gemm_param<T>(op(a.a1T[b], dual ? a.a1dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
-                          (int)y.ld(N), (int)y.ld(N), d, 3 * d, N),
+      HC(gemm_param<T>(wsk(op(a.a1T[b], dual ? a.a1dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
+                          (int)y.ld(N), (int)y.ld(N), d, 3 * d, N), a),
                        fl(dual), matP(y.wqkv[b], d, 3 * d, out ? out->W[b][0] : nullptr, out ? out->WT[b][0] : nullptr), s));
       HC(store(op(a.dZ1, dual ? a.dZ1d : nullptr, th.W[b][0], dual ? v->W[b][0] : nullptr,
                   (int)y.ld(3 * d), (int)y.ld(3 * d), N, d, 3 * d),
