@@ -151,6 +151,22 @@ def test_tf_meta_grad(prec):
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
 
 
+def test_tf_meta_grad_mid_bf16():
+    """8 x 160 tokens: the weight-gradient products over the token dimension take
+    the split-K path (5 slices), the unembedding with an odd vocabulary (301)
+    its scalar edge; bf16 operands against the oracle's bf16 emulation."""
+    cfg = W.SMALL["c4_mid"]
+    inp = W.make_inputs(cfg)
+    print(f"\n[tf meta_grad] c4_mid bf16 T={cfg.T}", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=True)
+    errs = group_errors(cfg, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
 def test_tf_meta_grad_full_size_bf16():
     """The full transformer workload at T=2 with bf16 operands against the
     oracle's float64-accumulated bf16 emulation, each meta-model tensor gated at

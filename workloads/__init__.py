@@ -138,6 +138,9 @@ SMALL: Dict[str, Config] = {
                         val_rows=264, T=2),
     "c4_small": C4.with_(name="c4_small", cfg_id=104, d_model=64, n_heads=4, d_ff=128, vocab=97,
                          seq=24, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2),
+    # enough tokens (8 x 160) for the split-K weight gradients, an odd vocabulary
+    "c4_mid": C4.with_(name="c4_mid", cfg_id=113, d_model=128, n_heads=4, d_ff=256, vocab=301,
+                       seq=160, rows=8, val_rows=4, n_blocks=2, meta_hidden=32, T=2),
 }
 
 
