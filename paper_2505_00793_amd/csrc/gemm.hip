@@ -17,11 +17,14 @@
 // v_mfma_f32_16x16x4_f32 (float32 operands), 64-lane wavefronts, four
 // computing waves per workgroup in a 2 x 2 arrangement.  Two main loops:
 //   gemm_nt_ws  bf16 operands with k, leading dimensions and strides multiples
-//               of 8: a 4-stage LDS ring filled by buffer_load ... lds from
-//               four loader waves while four waves multiply (512 threads);
+//               of 8: a 2- to 4-stage LDS ring of 64-deep k steps filled by
+//               buffer_load ... lds from four loader waves while four waves
+//               multiply (512 threads);
 //   gemm_nt     everything else (float32, ragged k): register-staged,
 //               double-buffered LDS, 256 threads.
-// Both end in the same staged epilogue.
+// Both end in the same staged epilogue.  Backward-weight products with few
+// output tiles and a long k can run split-K (batched partial products into a
+// caller workspace, then an ordered sum with the epilogue).
 #include <type_traits>
 
 #include "kernels.h"
