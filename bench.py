@@ -261,7 +261,10 @@ WORKLOADS = {
     "c4_transformer_tokenweights": ("decoder 4 blocks d 512, 8 heads, FF 2048, vocab 8192, RoPE, "
                                     "16x256 tokens, SGD lr 0.1, per-token loss weights from a "
                                     "512-128-1 meta-model, bf16 GEMM operands"),
+    "maml_mlp_relu_8x4096": ("MLP 4096-(4096x7)-1000 ReLU, CE, batch 1024, T=8, MAML (eta = "
+                             "theta_0), SGD lr 0.05, bf16 GEMM operands"),
 }
+BENCH_CONFIGS = {**W.CONFIGS, W.MAML5.name: W.MAML5}
 
 
 def bench_config(name: str, args):
@@ -270,7 +273,7 @@ def bench_config(name: str, args):
     on the stream); no roofline, sweep or CPU baseline."""
     import torch
     from paper_2505_00793_amd import _lib as M
-    cfg = W.CONFIGS[name]
+    cfg = BENCH_CONFIGS[name]
     T = cfg.T
     log(f"[bench] {name}: generating inputs (T={T})")
     inp = W.make_inputs(cfg)
@@ -334,7 +337,7 @@ def main():
                     help="write the HBM counter summary of --pmc-class from two rocprofv3 "
                          "--pmc runs (made with --copy-bytes) and exit; no GPU needed")
     ap.add_argument("--pmc-class", default="dual_bwd_weight_gemm_reverse")
-    ap.add_argument("--config", default="c5_mlp_relu_8x4096", choices=list(W.CONFIGS),
+    ap.add_argument("--config", default="c5_mlp_relu_8x4096", choices=list(BENCH_CONFIGS),
                     help="workload; the default (c5) line carries the roofline, the memory "
                          "sweep and the CPU baseline, the others throughput only")
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")

@@ -50,6 +50,12 @@
  *                                  decoupled weight decay omega (Adam).
  *   MFMG_META_EXAMPLE_WEIGHT_LOGITS [T][rows] logits; example n of inner step
  *                                  t has loss weight sigmoid(eta[t][n]).
+ *   MFMG_META_MAML                 n_theta floats, theta layout: the starting
+ *                                  point theta_0 itself (MAML, the task list of
+ *                                  Section 5.2); SGD with the fixed rate sgd_lr,
+ *                                  unweighted loss.  dV/deta = bar theta_0;
+ *                                  mfmg_meta_grad ignores its theta0 argument
+ *                                  (which may be null).  MLP kind only.
  *  The inner loss is L = (1/N) sum_n alpha_n l_n over the N rows of a batch,
  *  alpha_n = 1 unless the loss is weighted; the outer loss V is the unweighted
  *  mean over the validation rows.  l_n is softmax cross-entropy (CE) or the
@@ -86,7 +92,8 @@ enum {
   MFMG_META_LOGLR_PER_PARAM = 0,
   MFMG_META_LOGLR_PER_LAYER_WD = 1,
   MFMG_META_EXAMPLE_WEIGHT_LOGITS = 2,
-  MFMG_META_TOKEN_WEIGHT_MLP = 3
+  MFMG_META_TOKEN_WEIGHT_MLP = 3,
+  MFMG_META_MAML = 4
 };
 /* FP32: float32 GEMM operands.  BF16: bfloat16 GEMM operands (round to nearest
  * even) with float32 accumulation; parameters, optimiser state, adjoints and

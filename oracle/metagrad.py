@@ -20,7 +20,7 @@ from typing import List, Optional, Tuple
 import numpy as np
 import torch
 
-from workloads import Config, KIND_TRANSFORMER, META_TOKEN_WEIGHT_MLP, theta_layout
+from workloads import Config, KIND_TRANSFORMER, META_MAML, META_TOKEN_WEIGHT_MLP, theta_layout
 
 from .models import alpha_of, inner_loss, outer_loss, unpack
 from .optim import upsilon
@@ -56,8 +56,10 @@ class _Inputs:
 
     def __init__(self, cfg: Config, inputs: dict):
         self.cfg = cfg
-        self.theta0 = _t(inputs["theta0"])
         self.eta = _t(inputs["eta"])
+        # MAML (the task list of Section 5.2, 'Sweeping over Bilevel Optimisation
+        # Tasks'): the meta-parameters are the initial point theta_0
+        self.theta0 = self.eta.clone() if cfg.meta == META_MAML else _t(inputs["theta0"])
         self.opt0 = _t(inputs.get("opt_state0"))
         self.xs = [_t(x) for x in inputs["train_x"]]
         self.ys = [_t(y) for y in inputs["train_y"]]
@@ -73,7 +75,7 @@ def val_loss_of_eta(cfg: Config, inputs: dict, eta: torch.Tensor, bf16: bool = F
                     create_graph: bool = True) -> torch.Tensor:
     """ValLoss of Algorithm 1 as a differentiable function of eta."""
     I = _Inputs(cfg, inputs)
-    theta = I.theta0.clone().requires_grad_(True)
+    theta = eta if cfg.meta == META_MAML else I.theta0.clone().requires_grad_(True)
     opt = I.opt0
     for i in range(I.T):
         alpha = alpha_of(cfg, eta, i, I.xs[i], I.emb0)
@@ -154,6 +156,8 @@ def meta_grad_checkpointed(cfg: Config, inputs: dict, bf16: bool = False
     for i in reversed(range(I.T)):
         thbar, obar, d = reverse_step(cfg, I, i, thetas[i], opts[i], thbar, obar, bf16)
         etabar = etabar + d
+    if cfg.meta == META_MAML:   # theta_0 = eta: its adjoint is the rest of dV/deta
+        etabar = etabar + thbar
     return etabar.double().numpy(), float(V.detach())
 
 

@@ -478,8 +478,10 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
   const Act<T>& a = mp.act;
   const bool adam = p->adam();
   const bool wlog = p->d.meta == MFMG_META_EXAMPLE_WEIGHT_LOGITS;
+  const bool maml = p->d.meta == MFMG_META_MAML;
   const int R = p->d.rows;
   const long n = p->n_theta;
+  if (maml) theta0 = eta;   // the meta-parameters are the starting point
 
   // prologue
   TRY(E.to_ops(theta0, mp.slot[0]));
@@ -607,6 +609,8 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
                    a));
     if (!adam) vc ^= 1;
   }
+  // MAML: nothing else depends on eta = theta_0, so dV/deta = bar theta_0
+  if (maml) HIPCHK(copy(mp.thetabar, d_eta, n, s));
   return MFMG_OK;
 }
 
@@ -671,6 +675,7 @@ long n_eta_of(const mfmg_problem* p, int T) {
   if (p->tf) return tf_n_eta(p->d);
   switch (p->d.meta) {
     case MFMG_META_LOGLR_PER_PARAM: return p->n_theta;
+    case MFMG_META_MAML: return p->n_theta;
     case MFMG_META_LOGLR_PER_LAYER_WD: return p->L + 1;
     case MFMG_META_EXAMPLE_WEIGHT_LOGITS: return (long)T * p->d.rows;
     default: return 0;
@@ -831,6 +836,12 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
       break;
     case MFMG_META_TOKEN_WEIGHT_MLP:
       return fail(MFMG_ERR_UNSUPPORTED, "token-weight meta-MLP needs the transformer kind");
+    case MFMG_META_MAML:
+      if (d.optimizer != MFMG_OPT_SGD)
+        return fail(MFMG_ERR_UNSUPPORTED, "MAML is implemented for SGD");
+      if (!std::isfinite(d.sgd_lr))
+        return fail(MFMG_ERR_INVALID_ARGUMENT, "sgd_lr must be finite");
+      break;
     default:
       return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown meta kind %d", d.meta);
   }
@@ -951,7 +962,7 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
                            size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream) {
   if (!p) return fail(MFMG_ERR_INVALID_ARGUMENT, "null problem");
   if (T < 1) return fail(MFMG_ERR_INVALID_ARGUMENT, "T = %d, must be >= 1", T);
-  if (!theta0 || !eta || !d_eta_out)
+  if ((!theta0 && p->d.meta != MFMG_META_MAML) || !eta || !d_eta_out)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "null theta0, eta or d_eta_out");
   if (!train_batches) return fail(MFMG_ERR_INVALID_ARGUMENT, "null train_batches");
   for (int t = 0; t < T; ++t) TRY(check_batch(p, &train_batches[t], p->d.rows, "train_batches", t));

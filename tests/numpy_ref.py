@@ -107,7 +107,10 @@ def _layer_index(cfg):
 
 def val_loss(cfg, inp, eta):
     """V(eta): T inner updates then the unweighted validation loss (any dtype)."""
-    theta = inp["theta0"].astype(np.float64) + 0 * eta.reshape(-1)[0]
+    if cfg.meta == W.META_MAML:   # eta is the starting point theta_0
+        theta = eta.reshape(-1).astype(np.result_type(eta.dtype, np.float64)).copy()
+    else:
+        theta = inp["theta0"].astype(np.float64) + 0 * eta.reshape(-1)[0]
     n = theta.size
     m = np.zeros(n, dtype=theta.dtype)
     v = np.zeros(n, dtype=theta.dtype)

@@ -47,6 +47,13 @@ TINY = {
     "adam_tanh": W.C3.with_(name="t_adam_tanh", cfg_id=208, widths=(3, 4, 2), act=W.ACT_TANH,
                             precision=W.PREC_FP32, rows=5, val_rows=4, T=4,
                             loglr_init=math.log(0.02), wd_init=0.05),
+    "maml_tanh_ce": W.C5.with_(name="t_maml_ce", cfg_id=209, widths=(4, 5, 3), act=W.ACT_TANH,
+                               precision=W.PREC_FP32, meta=W.META_MAML, sgd_lr=0.4, rows=6,
+                               val_rows=5, T=3),
+    "maml_gelu_mse": W.C5.with_(name="t_maml_mse", cfg_id=210, widths=(3, 4, 1),
+                                act=W.ACT_GELU, loss=W.LOSS_MSE, has_bias=True,
+                                precision=W.PREC_FP32, meta=W.META_MAML, sgd_lr=0.2, rows=6,
+                                val_rows=5, T=2),
 }
 
 
@@ -83,6 +90,46 @@ def linreg_closed_form(inp):
         d += -D * gs[i] * a
         a = a - As[i] @ (D * a)
     return d
+
+
+def maml_linreg_closed_form(inp, lr):
+    """MAML on the squared loss: theta_{i+1} = (I - lr A_i) theta_i + lr b_i, so with
+    a_T = grad V(theta_T) and a_i = (I - lr A_i) a_{i+1} (A_i symmetric), dV/dtheta_0 = a_0."""
+    th = inp["eta"].astype(np.float64)
+    As = []
+    for X, y in zip(inp["train_x"], inp["train_y"]):
+        X = X.astype(np.float64)
+        y = y.astype(np.float64).reshape(-1)
+        N = X.shape[0]
+        A = 2.0 / N * X.T @ X
+        th = th - lr * (A @ th - 2.0 / N * X.T @ y)
+        As.append(A)
+    Xv = inp["val_x"].astype(np.float64)
+    yv = inp["val_y"].astype(np.float64).reshape(-1)
+    a = 2.0 / Xv.shape[0] * Xv.T @ (Xv @ th - yv)
+    for A in reversed(As):
+        a = a - lr * (A @ a)
+    return a
+
+
+@pytest.mark.parametrize("T", [1, 3])
+def test_maml_linreg_closed_form(T):
+    cfg = W.C1.with_(name="t_maml_lin", cfg_id=211, meta=W.META_MAML, sgd_lr=0.05, T=T,
+                     widths=(6, 1), rows=9, val_rows=7)
+    inp = W.make_inputs(cfg)
+    assert not np.any(inp["theta0"])   # the starting point comes from eta alone
+    d_cf = maml_linreg_closed_form(inp, cfg.sgd_lr)
+    assert relerr(oracle.meta_grad(cfg, inp)[0], d_cf) < 1e-12
+    assert relerr(oracle.meta_grad_checkpointed(cfg, inp)[0], d_cf) < 1e-12
+
+
+def test_maml_zero_lr_is_the_validation_gradient():
+    """With a zero inner learning rate theta_T = theta_0 = eta, so dV/deta = grad V(eta)."""
+    cfg = TINY["maml_tanh_ce"].with_(sgd_lr=0.0)
+    inp = W.make_inputs(cfg)
+    _, g = R.loss_and_grad(cfg, inp["eta"].astype(np.float64), inp["val_x"].astype(np.float64),
+                           inp["val_y"])
+    assert relerr(oracle.meta_grad_checkpointed(cfg, inp)[0], g) < 1e-12
 
 
 @pytest.mark.parametrize("cfg", [W.C1, W.SMALL["c1_small"], TINY["linreg"]], ids=lambda c: c.name)

@@ -31,6 +31,7 @@ ACT_TANH, ACT_GELU, ACT_RELU, ACT_NONE = 0, 1, 2, 3
 LOSS_MSE, LOSS_CE = 0, 1
 OPT_SGD, OPT_ADAM = 0, 1
 META_LOGLR_PER_PARAM, META_LOGLR_PER_LAYER_WD, META_EXAMPLE_WEIGHT_LOGITS, META_TOKEN_WEIGHT_MLP = 0, 1, 2, 3
+META_MAML = 4   # eta is the initial parameter vector theta_0 (SGD, fixed inner lr)
 PREC_FP32, PREC_BF16 = 0, 1
 KIND_MLP, KIND_TRANSFORMER = 0, 1
 
@@ -108,6 +109,9 @@ C5_TS = (4, 8, 16, 32)
 
 CONFIGS: Dict[str, Config] = {c.name: c for c in (C1, C2, C3, C4, C5)}
 
+# MAML on the config-5 network: eta = theta_0, SGD at a fixed rate
+MAML5 = C5.with_(name="maml_mlp_relu_8x4096", cfg_id=6, meta=META_MAML, sgd_lr=0.05)
+
 # Reduced variants for parity tests: same structure, sizes the oracle finishes in
 # seconds, each spanning several GEMM tiles plus a ragged tail.
 SMALL: Dict[str, Config] = {
@@ -132,6 +136,15 @@ SMALL: Dict[str, Config] = {
                       val_rows=136, T=3),
     "c5_mid_r8": C5.with_(name="c5_mid_r8", cfg_id=111, widths=(1544, 2056, 1032, 40), rows=1544,
                           val_rows=520, T=2),
+    # MAML: eta is theta_0 (fixed-rate SGD inside)
+    "c5_maml_fp32": C5.with_(name="c5_maml_fp32", cfg_id=114, widths=(40, 50, 30, 7),
+                             act=ACT_TANH, precision=PREC_FP32, meta=META_MAML, sgd_lr=0.1,
+                             has_bias=True, rows=33, val_rows=20, T=3),
+    "c5_maml": C5.with_(name="c5_maml", cfg_id=115, widths=(200, 264, 136, 40), meta=META_MAML,
+                        sgd_lr=0.1, rows=200, val_rows=136, T=3),
+    "c5_maml_r8_fp32": C5.with_(name="c5_maml_r8_fp32", cfg_id=116, widths=(200, 264, 136, 40),
+                                meta=META_MAML, sgd_lr=0.1, precision=PREC_FP32, rows=200,
+                                val_rows=136, T=3),
     # more 128 x 128 output tiles than compute units (two tiles for some
     # persistent workgroups), ragged rows, columns and k
     "c5_rag2": C5.with_(name="c5_rag2", cfg_id=112, widths=(2056, 2312, 40), rows=520,
@@ -193,7 +206,7 @@ def n_theta(cfg: Config) -> int:
 
 def meta_layout(cfg: Config) -> List[Tuple[str, int, Tuple[int, ...]]]:
     """Layout of the flat eta array."""
-    if cfg.meta == META_LOGLR_PER_PARAM:
+    if cfg.meta in (META_LOGLR_PER_PARAM, META_MAML):
         return theta_layout(cfg)
     if cfg.meta == META_LOGLR_PER_LAYER_WD:
         return [(f"loglr{l}", l, ()) for l in range(cfg.n_layers)] + [("wd", cfg.n_layers, ())]
@@ -207,7 +220,7 @@ def meta_layout(cfg: Config) -> List[Tuple[str, int, Tuple[int, ...]]]:
 
 
 def n_eta(cfg: Config) -> int:
-    if cfg.meta == META_LOGLR_PER_PARAM:
+    if cfg.meta in (META_LOGLR_PER_PARAM, META_MAML):
         return n_theta(cfg)
     if cfg.meta == META_LOGLR_PER_LAYER_WD:
         return cfg.n_layers + 1
@@ -257,6 +270,8 @@ def make_theta0(cfg: Config) -> np.ndarray:
 
 
 def make_eta(cfg: Config) -> np.ndarray:
+    if cfg.meta == META_MAML:
+        return make_theta0(cfg)
     if cfg.meta == META_LOGLR_PER_PARAM:
         return np.full(n_theta(cfg), cfg.loglr_init, dtype=np.float32)
     if cfg.meta == META_LOGLR_PER_LAYER_WD:
@@ -320,7 +335,9 @@ def make_inputs(cfg: Config, T: Optional[int] = None) -> dict:
     batches = [make_train_batch(cfg, t) for t in range(T)]
     vx, vy = make_val_batch(cfg)
     return {
-        "theta0": make_theta0(cfg),
+        # with MAML the starting point is eta; theta0 is then unused (zeros)
+        "theta0": (np.zeros(n_theta(cfg), dtype=np.float32) if cfg.meta == META_MAML
+                   else make_theta0(cfg)),
         "eta": make_eta(cfg),
         "opt_state0": (np.zeros(n_opt_state(cfg), dtype=np.float32)
                        if cfg.optimizer == OPT_ADAM else None),
