@@ -221,7 +221,8 @@ def desc_of(cfg: W.Config):
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
-                       adam_b1=cfg.adam_b1, adam_b2=cfg.adam_b2, adam_eps=cfg.adam_eps)
+                       adam_b1=cfg.adam_b1, adam_b2=cfg.adam_b2, adam_eps=cfg.adam_eps,
+                       map_steps=cfg.map_steps)
 
 
 def cpu_baseline(cfg: W.Config, inp: dict, T: int):
@@ -263,17 +264,58 @@ WORKLOADS = {
                                     "512-128-1 meta-model, bf16 GEMM operands"),
     "maml_mlp_relu_8x4096": ("MLP 4096-(4096x7)-1000 ReLU, CE, batch 1024, T=8, MAML (eta = "
                              "theta_0), SGD lr 0.05, bf16 GEMM operands"),
+    "toy_mstep_map": ("motivating example: y_0 = x w (1024 x 4096, w 4096 x 4096), M map steps "
+                      "y_i = i (2 + sin y)^cos y, mean squared error, MAML, T=2, SGD lr 1e-3, "
+                      "fp32"),
 }
-BENCH_CONFIGS = {**W.CONFIGS, W.MAML5.name: W.MAML5}
+BENCH_CONFIGS = {**W.CONFIGS, W.MAML5.name: W.MAML5, W.TOY.name: W.TOY}
 
 
 def bench_config(name: str, args):
     """meta-gradients/s of one of the other workloads at its own T, same timing
     protocol as the main line (inputs resident, warm-up calls, HIP-event timing
     on the stream); no roofline, sweep or CPU baseline."""
+    cfg = BENCH_CONFIGS[name]
+    ms, peak, finite = time_config(cfg, args)
+    print(json.dumps({
+        "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
+        "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.PREC_BF16 else "f32",
+        "data": "synthetic (seeded, see workloads/)",
+        "config": {"workload": WORKLOADS[name], "name": name, "T": cfg.T},
+        "peak_bytes": peak, "roofline": None, "cpu_baseline": None, "d_eta_finite": finite}))
+
+
+def bench_toy(args):
+    """The motivating example of Section 3.3 (B = 1024, D = 4096, T = 2, MAML) over
+    the number of map steps M: time and peak device bytes per meta-gradient.
+    The map's derivatives are carried in registers, so memory does not grow with
+    M.  The map's derivative grows roughly like M!, so in float32 the meta-gradient
+    itself overflows for the larger M (from M = 16 at this size); d_eta_finite
+    records it per M."""
+    rows = {}
+    for m in W.TOY_MS:
+        ms, peak, finite = time_config(W.TOY.with_(map_steps=m), args)
+        rows[str(m)] = {"ms_per_meta_grad": round(ms, 4), "peak_bytes": peak,
+                        "d_eta_finite": finite}
+    ref = rows[str(W.TOY.map_steps)]
+    print(json.dumps({
+        "metric": "meta-gradients/sec on 1 MI355X",
+        "value": round(1e3 / ref["ms_per_meta_grad"], 4),
+        "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ref["ms_per_meta_grad"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded, see workloads/)",
+        "config": {"workload": WORKLOADS[W.TOY.name], "name": W.TOY.name, "T": W.TOY.T,
+                   "M": W.TOY.map_steps},
+        "vs_M": rows, "roofline": None, "cpu_baseline": None}))
+
+
+def time_config(cfg: W.Config, args):
+    """(ms per meta-gradient, peak device bytes, dV/deta finite) for one workload."""
     import torch
     from paper_2505_00793_amd import _lib as M
-    cfg = BENCH_CONFIGS[name]
+    name = cfg.name
     T = cfg.T
     log(f"[bench] {name}: generating inputs (T={T})")
     inp = W.make_inputs(cfg)
@@ -309,16 +351,8 @@ def bench_config(name: str, args):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
-    log(f"[bench] {name}: {ms:.3f} ms per meta-gradient")
-    print(json.dumps({
-        "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
-        "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.PREC_BF16 else "f32",
-        "data": "synthetic (seeded, see workloads/)",
-        "config": {"workload": WORKLOADS[name], "name": name, "T": T},
-        "peak_bytes": peak, "roofline": None, "cpu_baseline": None,
-        "d_eta_finite": bool(torch.isfinite(d_eta).all().item())}))
+    log(f"[bench] {name} (M={cfg.map_steps}): {ms:.3f} ms per meta-gradient")
+    return ms, peak, bool(torch.isfinite(d_eta).all().item())
 
 
 def main():
@@ -350,6 +384,9 @@ def main():
         print(f"bench.py measures one GPU: the meta-gradient path is single-device "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
+    if args.config == W.TOY.name:
+        bench_toy(args)
+        return
     if args.config != W.C5.name:
         bench_config(args.config, args)
         return

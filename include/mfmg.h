@@ -59,7 +59,11 @@
  *  The inner loss is L = (1/N) sum_n alpha_n l_n over the N rows of a batch,
  *  alpha_n = 1 unless the loss is weighted; the outer loss V is the unweighted
  *  mean over the validation rows.  l_n is softmax cross-entropy (CE) or the
- *  squared error sum_j (z_nj - y_nj)^2 (MSE).
+ *  squared error sum_j (z_nj - y_nj)^2 (MSE), or for MAPMSE the mean over the
+ *  outputs j of (y_M,nj - y_nj)^2, where y_0 = z and y_i = i (2 + sin y_{i-1})^
+ *  cos(y_{i-1}) elementwise for i = 1..M (the map of Section 3.3, eq.
+ *  motivational_example; with one D x D layer and MAML this is the paper's
+ *  motivating example).  MAPMSE targets are float32 like MSE ones.
  *
  * Batches (mfmg_batch)
  * --------------------
@@ -86,7 +90,7 @@ typedef enum {
 
 enum { MFMG_KIND_MLP = 0, MFMG_KIND_TRANSFORMER = 1 };
 enum { MFMG_ACT_TANH = 0, MFMG_ACT_GELU = 1, MFMG_ACT_RELU = 2, MFMG_ACT_NONE = 3 };
-enum { MFMG_LOSS_MSE = 0, MFMG_LOSS_CE = 1 };
+enum { MFMG_LOSS_MSE = 0, MFMG_LOSS_CE = 1, MFMG_LOSS_MAPMSE = 2 };
 enum { MFMG_OPT_SGD = 0, MFMG_OPT_ADAM = 1 };
 enum {
   MFMG_META_LOGLR_PER_PARAM = 0,
@@ -120,6 +124,7 @@ typedef struct {
   /* transformer fields (reserved) */
   int d_model, n_heads, d_ff, vocab, seq, n_blocks, meta_hidden;
   float ln_eps, rope_base;
+  int map_steps;                       /* MFMG_LOSS_MAPMSE: M, 1..1024 */
 } mfmg_problem_desc;
 
 typedef struct mfmg_problem* mfmg_problem_t;

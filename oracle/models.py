@@ -15,7 +15,7 @@ from typing import Dict, Optional
 
 import torch
 
-from workloads import (Config, KIND_MLP, KIND_TRANSFORMER, LOSS_CE, LOSS_MSE,
+from workloads import (Config, KIND_MLP, KIND_TRANSFORMER, LOSS_CE, LOSS_MAPMSE, LOSS_MSE,
                        META_EXAMPLE_WEIGHT_LOGITS, META_TOKEN_WEIGHT_MLP, ACT_NONE,
                        theta_layout, meta_layout)
 
@@ -53,7 +53,17 @@ def per_example_loss(cfg: Config, out: torch.Tensor, y: torch.Tensor) -> torch.T
         return cross_entropy_rows(out, y)
     if cfg.loss == LOSS_MSE:
         return ((out - y.reshape(out.shape)) ** 2).sum(-1)
+    if cfg.loss == LOSS_MAPMSE:
+        return ((toy_map(out, cfg.map_steps) - y.reshape(out.shape)) ** 2).mean(-1)
     raise ValueError(cfg.loss)
+
+
+def toy_map(y: torch.Tensor, M: int) -> torch.Tensor:
+    """The M-step recursive map of Section 3.3 (eq. motivational_example),
+    elementwise: y_i = i * (2 + sin y_{i-1}) ** cos y_{i-1}, i = 1..M."""
+    for i in range(1, M + 1):
+        y = i * (2.0 + torch.sin(y)) ** torch.cos(y)
+    return y
 
 
 # ---------------------------------------------------------------------------------------

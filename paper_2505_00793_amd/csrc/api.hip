@@ -345,6 +345,7 @@ struct Eng {
     const int C = p->w[p->L];
     LossArgs<T> la;
     la.loss = p->d.loss;
+    la.map_M = p->d.map_steps;
     la.rows = R;
     la.C = C;
     la.dual = dual;
@@ -352,7 +353,7 @@ struct Eng {
     la.Z = a.Z[p->L - 1];
     la.Zd = a.Zd[p->L - 1];
     la.labels = p->d.loss == MFMG_LOSS_CE ? static_cast<const int*>(b.y) : nullptr;
-    la.targets = p->d.loss == MFMG_LOSS_MSE ? static_cast<const float*>(b.y) : nullptr;
+    la.targets = p->d.loss != MFMG_LOSS_CE ? static_cast<const float*>(b.y) : nullptr;
     la.alpha_logits = alpha_logits;
     la.d = a.dZ[0];
     la.dT = a.dZT[0];
@@ -806,8 +807,10 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
       return fail(MFMG_ERR_INVALID_ARGUMENT, "widths[%d] = %d outside [1, 2^20]", l, d.widths[l]);
   if (d.act < MFMG_ACT_TANH || d.act > MFMG_ACT_NONE)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown activation %d", d.act);
-  if (d.loss != MFMG_LOSS_MSE && d.loss != MFMG_LOSS_CE)
+  if (d.loss != MFMG_LOSS_MSE && d.loss != MFMG_LOSS_CE && d.loss != MFMG_LOSS_MAPMSE)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown loss %d", d.loss);
+  if (d.loss == MFMG_LOSS_MAPMSE && (d.map_steps < 1 || d.map_steps > 1024))
+    return fail(MFMG_ERR_INVALID_ARGUMENT, "map_steps = %d outside [1, 1024]", d.map_steps);
   if (d.optimizer != MFMG_OPT_SGD && d.optimizer != MFMG_OPT_ADAM)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown optimizer %d", d.optimizer);
   if (d.precision != MFMG_PREC_FP32 && d.precision != MFMG_PREC_BF16)

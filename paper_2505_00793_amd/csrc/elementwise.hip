@@ -265,6 +265,40 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
       store4(a.d + (long)row * a.ld + c, dv[0], dv[1], dv[2], dv[3]);
       if (a.dual) store4(a.dd + (long)row * a.ld + c, ddv[0], ddv[1], ddv[2], ddv[3]);
     }
+  } else if (a.loss == 2) {
+    // Squared error after the M-step map y_i = i (2 + sin y_{i-1})^cos y_{i-1},
+    // mean over the C outputs.  Per element the map's value y_M and its first
+    // and second derivatives in z are carried through the M steps in registers
+    // (with h = d/dy ln f_i = cos^2 y / (2 + sin y) - sin y ln(2 + sin y):
+    // f_i' = f_i h, f_i'' = f_i (h^2 + h')), so no step is stored.
+    const float* t = a.targets + (long)row * C;
+    const float invC = 1.0f / (float)C;
+    for (int c = lane; c < C; c += 64) {
+      float g = z[c], g1 = 1.0f, g2 = 0.0f;
+      for (int i = 1; i <= a.map_M; ++i) {
+        float sn, cs;
+        sincosf(g, &sn, &cs);
+        const float u = 2.0f + sn, lu = logf(u), iu = 1.0f / u;
+        const float f = (float)i * expf(cs * lu);
+        const float h = cs * cs * iu - sn * lu;
+        const float hp = -cs * lu - 3.0f * sn * cs * iu - cs * cs * cs * iu * iu;
+        const float f1 = f * h, f2 = f * (h * h + hp);
+        g2 = f2 * g1 * g1 + f1 * g2;
+        g1 = f1 * g1;
+        g = f;
+      }
+      const float r = g - t[c];
+      loss += r * r * invC;
+      a.d[(long)row * a.ld + c] = Elem<T>::from_float(2.0f * scale * invC * r * g1);
+      if (a.dual) {
+        const float zdc = zd[c];
+        ldot += 2.0f * invC * r * g1 * zdc;
+        a.dd[(long)row * a.ld + c] =
+            Elem<T>::from_float(2.0f * scale * invC * zdc * (g1 * g1 + r * g2));
+      }
+    }
+    loss = wave_sum(loss);
+    ldot = wave_sum(ldot);
   } else if (a.loss == 1) {
     float mx = -INFINITY;
     for (int c = lane; c < C; c += 64) mx = fmaxf(mx, z[c]);

@@ -154,7 +154,8 @@ struct ParamArgs {
 
 template <typename T>
 struct LossArgs {
-  int loss;                 // 0 MSE, 1 CE
+  int loss;                 // 0 MSE, 1 CE, 2 MSE after the M-step map (mean over outputs)
+  int map_M;                // M of that map
   int rows, C, dual;
   float inv_n;
   const float* Z;           // [rows][C] outputs

@@ -73,6 +73,20 @@ def loss_and_grad(cfg, theta, x, y, alpha=None):
         ln = lse - out[np.arange(N), y]
         dout = e / s
         dout[np.arange(N), y] -= 1.0
+    elif cfg.loss == W.LOSS_MAPMSE:
+        # forward through the map keeping each step's input, then the chain rule
+        # back through d/dy [i (2 + sin y)^cos y] = y_i (cos^2 y / (2 + sin y) - sin y ln(2 + sin y))
+        ys = [out]
+        for i in range(1, cfg.map_steps + 1):
+            ys.append(i * (2.0 + np.sin(ys[-1])) ** np.cos(ys[-1]))
+        r = ys[-1] - y.reshape(out.shape)
+        D = out.shape[1]
+        ln = (r * r).sum(axis=1) / D
+        dout = 2.0 * r / D
+        for i in range(cfg.map_steps, 0, -1):
+            yp = ys[i - 1]
+            s, c = np.sin(yp), np.cos(yp)
+            dout = dout * ys[i] * (c * c / (2.0 + s) - s * np.log(2.0 + s))
     else:
         r = out - y.reshape(out.shape)
         ln = (r * r).sum(axis=1)

@@ -55,7 +55,13 @@ def run_meta(cfg, inp):
 
 META_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small",
               "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml",
-              "c5_maml_r8_fp32", "c1_linreg", "c2_mlp_tanh_lossweights"]
+              "c5_maml_r8_fp32", "toy_small", "toy_mid", "c1_linreg",
+              "c2_mlp_tanh_lossweights"]
+
+
+def start_of(cfg, inp):
+    """The parameters the single-step tests start from (with MAML: eta)."""
+    return inp["eta"] if cfg.meta == W.META_MAML else inp["theta0"]
 
 
 def cfg_of(name):
@@ -83,7 +89,7 @@ def test_meta_grad_parity(name):
 
 
 INNER_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_small", "c3_small", "c5_r8",
-               "c5_mid_r8"]
+               "c5_mid_r8", "toy_small"]
 
 
 @pytest.mark.parametrize("name", INNER_CASES)
@@ -92,7 +98,7 @@ def test_inner_step_parity(name):
     inp = W.make_inputs(cfg)
     step = 1
     n = W.n_theta(cfg)
-    theta = inp["theta0"] + 0.01 * W.random_direction(n, 11)
+    theta = start_of(cfg, inp) + 0.01 * W.random_direction(n, 11)
     opt = None
     if cfg.optimizer == W.OPT_ADAM:
         m = 0.01 * W.random_direction(n, 12)
@@ -123,8 +129,8 @@ def test_inner_step_parity(name):
         assert relerr(opt1.cpu().numpy()[n:], opt1_ref[n:]) <= tol
 
 
-HVP_CASES = ["c1_small", "c2_small", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c3_small",
-             "c5_mid", "c5_r8", "c5_mid_r8"]
+HVP_CASES = ["toy_small", "c1_small", "c2_small", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small",
+             "c3_small", "c5_mid", "c5_r8", "c5_mid_r8"]
 
 
 @pytest.mark.parametrize("name", HVP_CASES)
@@ -133,7 +139,7 @@ def test_hvp_parity(name):
     inp = W.make_inputs(cfg)
     n = W.n_theta(cfg)
     step = 0
-    theta = inp["theta0"]
+    theta = start_of(cfg, inp)
     v = W.random_direction(n, 21)
     x, y = inp["train_x"][step], inp["train_y"][step]
     bf16 = cfg.precision == W.PREC_BF16

@@ -50,6 +50,10 @@ TINY = {
     "maml_tanh_ce": W.C5.with_(name="t_maml_ce", cfg_id=209, widths=(4, 5, 3), act=W.ACT_TANH,
                                precision=W.PREC_FP32, meta=W.META_MAML, sgd_lr=0.4, rows=6,
                                val_rows=5, T=3),
+    "toy_map": W.TOY.with_(name="t_toy", cfg_id=212, widths=(6, 5), rows=7, val_rows=4,
+                           map_steps=3, sgd_lr=0.05),
+    "toy_map_m1": W.TOY.with_(name="t_toy1", cfg_id=213, widths=(4, 3), rows=5, val_rows=3,
+                              map_steps=1, sgd_lr=0.2, T=3),
     "maml_gelu_mse": W.C5.with_(name="t_maml_mse", cfg_id=210, widths=(3, 4, 1),
                                 act=W.ACT_GELU, loss=W.LOSS_MSE, has_bias=True,
                                 precision=W.PREC_FP32, meta=W.META_MAML, sgd_lr=0.2, rows=6,

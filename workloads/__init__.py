@@ -29,6 +29,9 @@ ROOT_SEED = 250500793
 # enum values shared with include/mfmg.h (plain integers, no arithmetic)
 ACT_TANH, ACT_GELU, ACT_RELU, ACT_NONE = 0, 1, 2, 3
 LOSS_MSE, LOSS_CE = 0, 1
+# squared error after the M-step map y_i = i (2 + sin y_{i-1})^cos y_{i-1} of Section 3.3
+# (eq. motivational_example), averaged over the outputs
+LOSS_MAPMSE = 2
 OPT_SGD, OPT_ADAM = 0, 1
 META_LOGLR_PER_PARAM, META_LOGLR_PER_LAYER_WD, META_EXAMPLE_WEIGHT_LOGITS, META_TOKEN_WEIGHT_MLP = 0, 1, 2, 3
 META_MAML = 4   # eta is the initial parameter vector theta_0 (SGD, fixed inner lr)
@@ -62,6 +65,7 @@ class Config:
     adam_eps: float = 1e-8
     loglr_init: float = math.log(0.01)
     wd_init: float = 1e-4
+    map_steps: int = 0                     # M of the toy map (LOSS_MAPMSE)
     # transformer
     d_model: int = 0
     n_heads: int = 0
@@ -112,6 +116,19 @@ CONFIGS: Dict[str, Config] = {c.name: c for c in (C1, C2, C3, C4, C5)}
 # MAML on the config-5 network: eta = theta_0, SGD at a fixed rate
 MAML5 = C5.with_(name="maml_mlp_relu_8x4096", cfg_id=6, meta=META_MAML, sgd_lr=0.05)
 
+# The paper's motivating example (Section 3.3): y_0 = x w with x of B x D and
+# w of D x D, M map steps, mean squared error against standard normal targets,
+# MAML (w_0 = eta), T = 2 inner SGD steps at rate 1e-3, B = 1024, D = 4096.
+TOY = Config(name="toy_mstep_map", cfg_id=7, widths=(4096, 4096), act=ACT_NONE,
+             loss=LOSS_MAPMSE, optimizer=OPT_SGD, meta=META_MAML, precision=PREC_FP32,
+             has_bias=False, rows=1024, val_rows=1024, T=2, init="normal1", sgd_lr=1e-3,
+             map_steps=8)
+TOY_MS = (1, 2, 4, 8, 16, 32, 64)
+
+TOY_SMALL_BASE = Config(name="toy", cfg_id=0, act=ACT_NONE, loss=LOSS_MAPMSE, optimizer=OPT_SGD,
+                        meta=META_MAML, precision=PREC_FP32, has_bias=False, T=2,
+                        init="normal0.1")
+
 # Reduced variants for parity tests: same structure, sizes the oracle finishes in
 # seconds, each spanning several GEMM tiles plus a ragged tail.
 SMALL: Dict[str, Config] = {
@@ -145,6 +162,11 @@ SMALL: Dict[str, Config] = {
     "c5_maml_r8_fp32": C5.with_(name="c5_maml_r8_fp32", cfg_id=116, widths=(200, 264, 136, 40),
                                 meta=META_MAML, sgd_lr=0.1, precision=PREC_FP32, rows=200,
                                 val_rows=136, T=3),
+    # the motivating example (one D x D layer, the M-step map, MAML), small
+    "toy_small": TOY_SMALL_BASE.with_(name="toy_small", cfg_id=117, widths=(64, 48), rows=24,
+                                      val_rows=16, map_steps=3, sgd_lr=0.05),
+    "toy_mid": TOY_SMALL_BASE.with_(name="toy_mid", cfg_id=118, widths=(200, 136), rows=100,
+                                    val_rows=40, map_steps=2, sgd_lr=0.02),
     # more 128 x 128 output tiles than compute units (two tiles for some
     # persistent workgroups), ragged rows, columns and k
     "c5_rag2": C5.with_(name="c5_rag2", cfg_id=112, widths=(2056, 2312, 40), rows=520,
@@ -247,6 +269,8 @@ def _init_std(cfg: Config, shape) -> float:
         return 0.1
     if cfg.init == "normal0.02":
         return 0.02
+    if cfg.init == "normal1":
+        return 1.0
     fan_in, fan_out = shape[0], shape[1]
     if cfg.init == "xavier":
         return math.sqrt(2.0 / (fan_in + fan_out))
@@ -307,6 +331,8 @@ def _draw_batch(cfg: Config, rng, rows: int):
     if cfg.kind == KIND_TRANSFORMER:
         return _zipf_tokens(rng, cfg, (rows, cfg.seq + 1)), None
     x = rng.standard_normal((rows, cfg.widths[0])).astype(np.float32)
+    if cfg.loss == LOSS_MAPMSE:   # the toy task: standard normal inputs and targets
+        return x, rng.standard_normal((rows, cfg.widths[-1])).astype(np.float32)
     if cfg.loss == LOSS_MSE:
         noise = rng.standard_normal((rows, cfg.widths[-1]))
         y = (x.astype(np.float64) @ _wstar(cfg).reshape(-1, 1) + 0.1 * noise).astype(np.float32)
