@@ -222,7 +222,7 @@ def desc_of(cfg: W.Config):
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
                        adam_b1=cfg.adam_b1, adam_b2=cfg.adam_b2, adam_eps=cfg.adam_eps,
-                       map_steps=cfg.map_steps)
+                       map_steps=cfg.map_steps, ckpt_segment=cfg.ckpt_segment)
 
 
 def cpu_baseline(cfg: W.Config, inp: dict, T: int):

@@ -125,6 +125,16 @@ typedef struct {
   int d_model, n_heads, d_ff, vocab, seq, n_blocks, meta_hidden;
   float ln_eps, rope_base;
   int map_steps;                       /* MFMG_LOSS_MAPMSE: M, 1..1024 */
+  /* Static-memory reduction for SGD (MLP kind): 0 keeps the operand
+   * checkpoint of every theta_t (memory linear in T).  k >= 1 keeps float32
+   * theta only at t = k, 2k, .. and a ring of k + 1 operand checkpoints, and
+   * recomputes each segment's states (the same kernels on the same inputs, so
+   * the result is bit-identical) when the reverse sweep enters it: static
+   * memory ~ (T/k + k) parameter copies, one extra forward inner step per
+   * recomputed state.  A two-level form of the rematerialisation schedules
+   * the appendix on static device memory proposes (whose logarithmic form
+   * needs a recursive schedule).  Ignored for Adam and when k >= T. */
+  int ckpt_segment;
 } mfmg_problem_desc;
 
 typedef struct mfmg_problem* mfmg_problem_t;

@@ -159,7 +159,9 @@ void carve_act(const mfmg_problem* p, Carver& c, Act<T>& a, int R, bool dual) {
 
 template <typename T>
 struct MetaPlan {
-  std::vector<OperandSet<T>> slot;  // T + 1 operand checkpoints
+  int seg;                          // 0, or the segment length k of recomputed checkpoints
+  std::vector<OperandSet<T>> slot;  // T + 1 operand checkpoints, or a ring of k + 1
+  std::vector<float*> ck;           // segments: theta_{s k} (float32), s = 1 .. ceil(T/k) - 1
   float* run[2];                    // SGD: theta_{t+1} (float32), ping-pong
   float* thetabar;
   OperandSet<T> v[2];               // tangent operand copies, ping-pong
@@ -178,6 +180,13 @@ int adam_blocks(const mfmg_problem* p, int l) {
   return (int)((n + 255) / 256);
 }
 
+// Segment length of the recomputed checkpoints for T inner steps (0: every
+// step's operands are kept).  SGD only: Adam's reverse step reads m_t, v_t, g_t.
+int seg_of(const mfmg_problem* p, int T) {
+  const int k = p->d.ckpt_segment;
+  return (k > 0 && k < T && !p->adam()) ? k : 0;
+}
+
 template <typename T>
 void plan_meta(const mfmg_problem* p, int T_, char* base, MetaPlan<T>& mp) {
   Carver c{base};
@@ -190,8 +199,16 @@ void plan_meta(const mfmg_problem* p, int T_, char* base, MetaPlan<T>& mp) {
     return;
   }
   const size_t n = p->n_theta;
-  mp.slot.resize(T_ + 1);
-  for (int t = 0; t <= T_; ++t) carve_opset(p, c, mp.slot[t]);
+  mp.seg = seg_of(p, T_);
+  const int nslot = mp.seg ? mp.seg + 1 : T_ + 1;
+  mp.slot.resize(nslot);
+  for (int t = 0; t < nslot; ++t) carve_opset(p, c, mp.slot[t]);
+  mp.ck.clear();
+  if (mp.seg) {
+    const int nseg = (T_ + mp.seg - 1) / mp.seg;
+    mp.ck.assign(nseg, nullptr);
+    for (int q = 1; q < nseg; ++q) mp.ck[q] = c.take<float>(n);
+  }
   mp.run[0] = mp.run[1] = nullptr;
   if (!p->adam()) {
     mp.run[0] = c.take<float>(n);
@@ -484,8 +501,13 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
   const long n = p->n_theta;
   if (maml) theta0 = eta;   // the meta-parameters are the starting point
 
+  // Operand checkpoint of theta_t: slot t, or with segments the ring entry
+  // t mod (k + 1), which holds one segment's states plus theta_T at once.
+  const int k = mp.seg;
+  auto sl = [&](int t) -> const OperandSet<T>& { return mp.slot[k ? t % (k + 1) : t]; };
+
   // prologue
-  TRY(E.to_ops(theta0, mp.slot[0]));
+  TRY(E.to_ops(theta0, sl(0)));
   if (adam) {
     if (opt0) {
       HIPCHK(copy(opt0, mp.m[0], n, s));
@@ -496,10 +518,11 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
     }
   }
 
-  // forward unroll with checkpoints
-  for (int t = 0; t < T_; ++t) {
+  // One forward inner step t from the float32 theta_t at th: the update writes
+  // theta_{t+1} to th_next and its operand copies to checkpoint t + 1.
+  auto fwd_step = [&](int t, const float* th, float* th_next) -> mfmg_status {
     TRY(E.load_x(static_cast<const float*>(batches[t].x), R, a));
-    TRY(E.forward(mp.slot[t], nullptr, R, a));
+    TRY(E.forward(sl(t), nullptr, R, a));
     const float* alpha = wlog ? eta + (long)t * R : nullptr;
     TRY(E.head(batches[t], R, false, alpha, nullptr, nullptr, a));
     ParamArgs<T> P = param_base<T>(p, mode_of(p, 0), eta);
@@ -513,30 +536,45 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
       P.g_save = mp.g[t];
       bias_corr(p, t, &P.k1, &P.k2);
     } else {
-      P.theta = t == 0 ? theta0 : mp.run[(t - 1) & 1];
-      P.theta_next = mp.run[t & 1];
+      P.theta = th;
+      P.theta_next = th_next;
     }
-    const OperandSet<T>& nxt = mp.slot[t + 1];
-    TRY(E.backward(mp.slot[t], nullptr, R, true, P,
+    const OperandSet<T>& nxt = sl(t + 1);
+    TRY(E.backward(sl(t), nullptr, R, true, P,
                    [&](ParamArgs<T>& Q, int l) {
                      Q.outW = nxt.W[l];
                      Q.outWT = nxt.WT[l];
                      Q.outb = nxt.b[l];
                    },
                    a));
+    return MFMG_OK;
+  };
+  // SGD keeps theta in the run ping-pong; with segments theta at a segment
+  // start goes to its float32 checkpoint instead.
+  auto other = [&](const float* th) { return th == mp.run[0] ? mp.run[1] : mp.run[0]; };
+
+  // forward unroll with checkpoints
+  {
+    const float* th = theta0;
+    for (int t = 0; t < T_; ++t) {
+      float* nx = nullptr;
+      if (!adam) nx = (k && (t + 1) % k == 0 && t + 1 < T_) ? mp.ck[(t + 1) / k] : other(th);
+      TRY(fwd_step(t, th, nx));
+      th = nx;
+    }
   }
 
   // outer loss V at theta_T and its gradient: the seed of the reverse sweep
   {
     const int Rv = p->d.val_rows;
     TRY(E.load_x(static_cast<const float*>(val->x), Rv, a));
-    TRY(E.forward(mp.slot[T_], nullptr, Rv, a));
+    TRY(E.forward(sl(T_), nullptr, Rv, a));
     TRY(E.head(*val, Rv, false, nullptr, nullptr, nullptr, a));
     if (val_loss) HIPCHK(loss_reduce(a.loss_rows, nullptr, Rv, 1.0f / (float)Rv, val_loss, s));
     ParamArgs<T> P = param_base<T>(p, mode_of(p, 1), eta);
     P.thetabar = mp.thetabar;
     const OperandSet<T>& v0 = mp.v[0];
-    TRY(E.backward(mp.slot[T_], nullptr, Rv, true, P,
+    TRY(E.backward(sl(T_), nullptr, Rv, true, P,
                    [&](ParamArgs<T>& Q, int l) {
                      if (!adam) {
                        Q.outW = v0.W[l];
@@ -551,6 +589,19 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
   int vc = 0;
   for (int i = T_ - 1; i >= 0; --i) {
     const bool first = i == T_ - 1;
+    // entering a segment other than the last: recompute theta_{s0} .. theta_i
+    // from the segment's float32 checkpoint (the same kernels on the same
+    // inputs, so the operand copies are bit-identical to the unroll's)
+    if (k && (i + 1) % k == 0 && i + 1 < T_) {
+      const int s0 = i + 1 - k;
+      const float* th = s0 == 0 ? theta0 : mp.ck[s0 / k];
+      TRY(E.to_ops(th, sl(s0)));
+      for (int t = s0; t < i; ++t) {
+        float* nx = other(th);
+        TRY(fwd_step(t, th, nx));
+        th = nx;
+      }
+    }
     if (adam) {
       float k1, k2;
       bias_corr(p, i, &k1, &k2);
@@ -590,7 +641,7 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
       HIPCHK(adam_reduce(mp.partial, mp.part_off, p->L, first, d_eta, s));
     }
     TRY(E.load_x(static_cast<const float*>(batches[i].x), R, a));
-    TRY(E.forward(mp.slot[i], &mp.v[vc], R, a));
+    TRY(E.forward(sl(i), &mp.v[vc], R, a));
     const float* alpha = wlog ? eta + (long)i * R : nullptr;
     TRY(E.head(batches[i], R, true, alpha, nullptr, wlog ? d_eta + (long)i * R : nullptr, a));
     ParamArgs<T> P = param_base<T>(p, mode_of(p, 2), eta);
@@ -599,7 +650,7 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
     P.first = first;
     const OperandSet<T>& vn = mp.v[vc ^ 1];
     const bool write_next = !adam && i > 0;
-    TRY(E.backward(mp.slot[i], &mp.v[vc], R, !adam, P,
+    TRY(E.backward(sl(i), &mp.v[vc], R, !adam, P,
                    [&](ParamArgs<T>& Q, int l) {
                      if (write_next) {
                        Q.outW = vn.W[l];
@@ -811,6 +862,9 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown loss %d", d.loss);
   if (d.loss == MFMG_LOSS_MAPMSE && (d.map_steps < 1 || d.map_steps > 1024))
     return fail(MFMG_ERR_INVALID_ARGUMENT, "map_steps = %d outside [1, 1024]", d.map_steps);
+  if (d.ckpt_segment < 0 || d.ckpt_segment > (1 << 20))
+    return fail(MFMG_ERR_INVALID_ARGUMENT, "ckpt_segment = %d outside [0, 2^20]",
+                d.ckpt_segment);
   if (d.optimizer != MFMG_OPT_SGD && d.optimizer != MFMG_OPT_ADAM)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown optimizer %d", d.optimizer);
   if (d.precision != MFMG_PREC_FP32 && d.precision != MFMG_PREC_BF16)

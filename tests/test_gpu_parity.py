@@ -92,6 +92,26 @@ INNER_CASES = ["c1_small", "c2_small", "c3_fp32", "c5_tanh_fp32", "c5_small", "c
                "c5_mid_r8", "toy_small"]
 
 
+@pytest.mark.parametrize("name,k", [("c5_small", 1), ("c5_small", 3), ("c5_r8", 2),
+                                    ("c5_tanh_fp32", 3), ("c2_small", 2), ("c5_maml", 3),
+                                    ("toy_small", 1)])
+def test_segment_checkpoints_bit_identical(name, k):
+    """Keeping float32 theta only at segment starts and recomputing each segment
+    in the reverse sweep gives the same bits as keeping every step, with less
+    static memory."""
+    base = cfg_of(name).with_(T=7)
+    inp = W.make_inputs(base)
+    print(f"\n[segments] {name} T=7 k={k}", flush=True)
+    d0, V0, _ = run_meta(base, inp)
+    seg = base.with_(ckpt_segment=k)
+    d1, V1, _ = run_meta(seg, inp)
+    st0 = M().Problem(desc_of(base)).mfmg_query_sizes(7).static_bytes
+    st1 = M().Problem(desc_of(seg)).mfmg_query_sizes(7).static_bytes
+    print(f"  static bytes {st0} -> {st1}", flush=True)
+    assert np.array_equal(d0, d1) and V0 == V1
+    assert st1 < st0
+
+
 @pytest.mark.parametrize("name", INNER_CASES)
 def test_inner_step_parity(name):
     cfg = cfg_of(name)

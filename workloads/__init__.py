@@ -66,6 +66,7 @@ class Config:
     loglr_init: float = math.log(0.01)
     wd_init: float = 1e-4
     map_steps: int = 0                     # M of the toy map (LOSS_MAPMSE)
+    ckpt_segment: int = 0                  # GPU static-memory segments (0: keep every step)
     # transformer
     d_model: int = 0
     n_heads: int = 0
