@@ -15,6 +15,7 @@ runs on) and the float64 CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import math
 import json
 import os
 import sys
@@ -490,20 +491,23 @@ def main():
                  "floor_us": {"mfma": round(t_mfma * 1e6, 2), "hbm": round(t_hbm * 1e6, 2)}})
     finite = bool(torch.isfinite(d_eta).all().item())
 
-    sweep = {}
-    for Ts in W.C5_TS:
-        s = P.mfmg_query_sizes(Ts)
+    def sweep_entry(Pq, Ts, label):
+        s = Pq.mfmg_query_sizes(Ts)
         entry = {"peak_bytes": None, "static_bytes": s.static_bytes, "dynamic_bytes": s.dynamic_bytes,
                  "workspace_bytes": s.workspace_bytes}
         if args.sweep_steps > 0:
-            log(f"[bench] sweep T={Ts}")
-            wss = ws if s.workspace_bytes <= ws.numel() else P.workspace(s.workspace_bytes)
-            entry["peak_bytes"] = call(Ts, wss)
+            log(f"[bench] sweep T={Ts}{label}")
+            wss = ws if s.workspace_bytes <= ws.numel() else Pq.workspace(s.workspace_bytes)
+
+            def callq():
+                return Pq.mfmg_meta_grad(theta0, None, eta, xs[:Ts], ys[:Ts], vx, vy, d_eta, vloss,
+                                         ws=wss)
+            entry["peak_bytes"] = callq()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             for _ in range(args.sweep_steps):
-                call(Ts, wss)
+                callq()
             e1.record(stream)
             torch.cuda.synchronize()
             entry["ms_per_meta_grad"] = round(e0.elapsed_time(e1) / args.sweep_steps, 3)
@@ -511,7 +515,17 @@ def main():
             if wss is not ws:
                 del wss
                 torch.cuda.empty_cache()
-        sweep[str(Ts)] = entry
+        return entry
+
+    sweep = {str(Ts): sweep_entry(P, Ts, "") for Ts in W.C5_TS}
+    # the same with segment checkpoints of length round(sqrt(T)) (static memory
+    # ~ 2 sqrt(T) parameter copies instead of T + 1, bit-identical results)
+    sweep_seg = {}
+    for Ts in W.C5_TS:
+        k = max(1, int(round(math.sqrt(Ts))))
+        Pk = M.Problem(desc_of(cfg.with_(ckpt_segment=k)))
+        sweep_seg[str(Ts)] = {"segment": k, **sweep_entry(Pk, Ts, f" segments of {k}")}
+        del Pk
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -530,6 +544,7 @@ def main():
                    "parallelism": "single GPU"},
         "peak_bytes": peak, "static_bytes": sizes.static_bytes,
         "dynamic_bytes": sizes.dynamic_bytes, "memory_vs_T": sweep,
+        "memory_vs_T_segment_checkpoints": sweep_seg,
         "roofline": roof, "kernels": kern,
         "kernel_timing": "HIP events around each launch on the library stream, separate pass of the same calls",
         "cpu_baseline": cpu, "d_eta_finite": finite,
