@@ -1069,9 +1069,14 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
     }
   }
   if constexpr (sizeof(T) == 2) {
-    // 128 x 128 tiles once they alone fill most of the 256 compute units.
+    // 128 x 128 tiles once they alone fill most of the 256 compute units, else
+    // 128 x 64 on the direct-to-LDS path (each compute unit then loads 128 + 64
+    // rows per k step for 8192 outputs against 2 x 128 for two 64 x 64 tiles),
+    // else 64 x 64.
     if (cdiv(op.M, 128) * cdiv(op.N, 128) * op.batch >= 192)
       return launch<T, FLAGS, 128, 128>(op, epi, s);
+    if (cdiv(op.M, 128) * cdiv(op.N, 64) * op.batch >= 192 && dma_ok(op))
+      return launch<T, FLAGS, 128, 64>(op, epi, s);
   }
   return launch<T, FLAGS, 64, 64>(op, epi, s);
 }
