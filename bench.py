@@ -265,11 +265,19 @@ WORKLOADS = {
                                     "512-128-1 meta-model, bf16 GEMM operands"),
     "maml_mlp_relu_8x4096": ("MLP 4096-(4096x7)-1000 ReLU, CE, batch 1024, T=8, MAML (eta = "
                              "theta_0), SGD lr 0.05, bf16 GEMM operands"),
+    "c4_long_context": ("decoder 4 blocks d 512, 8 heads, FF 2048, vocab 8192, 8192 tokens per "
+                        "batch as S x 8192/S sequences for S = 2048, 4096, 8192, T=2, per-token "
+                        "loss weights, bf16 GEMM operands, attention materialised"),
     "toy_mstep_map": ("motivating example: y_0 = x w (1024 x 4096, w 4096 x 4096), M map steps "
                       "y_i = i (2 + sin y)^cos y, mean squared error, MAML, T=2, SGD lr 1e-3, "
                       "fp32"),
 }
-BENCH_CONFIGS = {**W.CONFIGS, W.MAML5.name: W.MAML5, W.TOY.name: W.TOY}
+BENCH_CONFIGS = {**W.CONFIGS, W.MAML5.name: W.MAML5, W.TOY.name: W.TOY,
+                 "c4_long_context": W.C4}
+
+
+def c4_long(S: int) -> W.Config:
+    return W.C4.with_(name=f"c4_S{S}", seq=S, rows=8192 // S, val_rows=8192 // S, T=2)
 
 
 def bench_config(name: str, args):
@@ -312,6 +320,26 @@ def bench_toy(args):
         "vs_M": rows, "roofline": None, "cpu_baseline": None}))
 
 
+def bench_long_context(args):
+    """The config-4 decoder at long contexts: time and peak device bytes per
+    meta-gradient for each S in C4_LONG_S (8192 tokens per batch, T = 2)."""
+    rows = {}
+    for S in W.C4_LONG_S:
+        ms, peak, finite = time_config(c4_long(S), args)
+        rows[str(S)] = {"ms_per_meta_grad": round(ms, 4), "peak_bytes": peak,
+                        "d_eta_finite": finite}
+    ref = rows[str(W.C4_LONG_S[-1])]
+    print(json.dumps({
+        "metric": "meta-gradients/sec on 1 MI355X",
+        "value": round(1e3 / ref["ms_per_meta_grad"], 4),
+        "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ref["ms_per_meta_grad"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, see workloads/)",
+        "config": {"workload": WORKLOADS["c4_long_context"], "name": "c4_long_context", "T": 2,
+                   "S": W.C4_LONG_S[-1]},
+        "vs_S": rows, "roofline": None, "cpu_baseline": None}))
+
+
 def time_config(cfg: W.Config, args):
     """(ms per meta-gradient, peak device bytes, dV/deta finite) for one workload."""
     import torch
@@ -352,7 +380,8 @@ def time_config(cfg: W.Config, args):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
-    log(f"[bench] {name} (M={cfg.map_steps}): {ms:.3f} ms per meta-gradient")
+    tag = f" (M={cfg.map_steps})" if cfg.loss == W.LOSS_MAPMSE else ""
+    log(f"[bench] {name}{tag}: {ms:.3f} ms per meta-gradient")
     return ms, peak, bool(torch.isfinite(d_eta).all().item())
 
 
@@ -387,6 +416,9 @@ def main():
         sys.exit(2)
     if args.config == W.TOY.name:
         bench_toy(args)
+        return
+    if args.config == "c4_long_context":
+        bench_long_context(args)
         return
     if args.config != W.C5.name:
         bench_config(args.config, args)

@@ -167,6 +167,23 @@ def test_tf_meta_grad_mid_bf16():
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_tf_meta_grad_long_context(prec):
+    """1024-token sequences: causal attention of 1024 x 1024 per head, materialised."""
+    cfg = W.SMALL["c4_long"]
+    if prec == "fp32":
+        cfg = cfg.with_(precision=W.PREC_FP32)
+    inp = W.make_inputs(cfg)
+    print(f"\n[tf meta_grad] c4_long {prec} S={cfg.seq}", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=prec == "bf16")
+    errs = group_errors(cfg, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
 def test_tf_meta_grad_full_size_bf16():
     """The full transformer workload at T=2 with bf16 operands against the
     oracle's float64-accumulated bf16 emulation, each meta-model tensor gated at

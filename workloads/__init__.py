@@ -126,6 +126,10 @@ TOY = Config(name="toy_mstep_map", cfg_id=7, widths=(4096, 4096), act=ACT_NONE,
              map_steps=8)
 TOY_MS = (1, 2, 4, 8, 16, 32, 64)
 
+# Long contexts on the config-4 decoder (the paper sweeps sequence lengths up to
+# 8192): 8192 tokens per batch as S x (8192 / S) sequences, T = 2.
+C4_LONG_S = (2048, 4096, 8192)
+
 TOY_SMALL_BASE = Config(name="toy", cfg_id=0, act=ACT_NONE, loss=LOSS_MAPMSE, optimizer=OPT_SGD,
                         meta=META_MAML, precision=PREC_FP32, has_bias=False, T=2,
                         init="normal0.1")
@@ -174,6 +178,9 @@ SMALL: Dict[str, Config] = {
                         val_rows=264, T=2),
     "c4_small": C4.with_(name="c4_small", cfg_id=104, d_model=64, n_heads=4, d_ff=128, vocab=97,
                          seq=24, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2),
+    # a long context (2 x 1024 tokens): attention of 1024 x 1024 per head
+    "c4_long": C4.with_(name="c4_long", cfg_id=119, d_model=64, n_heads=2, d_ff=128, vocab=97,
+                        seq=1024, rows=2, val_rows=1, n_blocks=1, meta_hidden=16, T=2),
     # enough tokens (8 x 160) for the split-K weight gradients, an odd vocabulary
     "c4_mid": C4.with_(name="c4_mid", cfg_id=113, d_model=128, n_heads=4, d_ff=256, vocab=301,
                        seq=160, rows=8, val_rows=4, n_blocks=2, meta_hidden=32, T=2),
