@@ -82,6 +82,35 @@ def test_create_rejects_bad_descriptions(L, field, value, status):
     assert len(L.mfmg_last_error_message()) > 0
 
 
+@pytest.mark.parametrize("cfg,fields,status", [
+    (W.SMALL["toy_small"], {"map_steps": 0}, 1),        # the map needs M >= 1
+    (W.SMALL["toy_small"], {"map_steps": 1025}, 1),
+    (W.C5, {"ckpt_segment": -1}, 1),
+    (W.C5, {"meta": W.META_MAML, "optimizer": W.OPT_ADAM}, 2),   # MAML is SGD only
+    (W.C4, {"meta": W.META_MAML}, 2),                  # and MLP only
+])
+def test_create_rejects_bad_options(L, cfg, fields, status):
+    d = desc_of(cfg)
+    for k, v in fields.items():
+        setattr(d, k, v)
+    h = ctypes.c_void_p()
+    assert L.mfmg_problem_create(ctypes.byref(d), ctypes.byref(h)) == status
+    assert not h.value
+
+
+def test_segment_checkpoints_shrink_static_memory():
+    """Static bytes with segment checkpoints: (T/k - 1) float32 copies of theta and
+    k + 1 operand checkpoints instead of T + 1 (size query only, no GPU)."""
+    T = 32
+    full = M.Problem(desc_of(W.C5)).mfmg_query_sizes(T)
+    seg = M.Problem(desc_of(W.C5.with_(ckpt_segment=6))).mfmg_query_sizes(T)
+    n = W.n_theta(W.C5)
+    assert full.dynamic_bytes == seg.dynamic_bytes
+    # 32 + 1 operand checkpoints (4 B per weight) against 6 + 1 and 5 float32 thetas
+    saved = full.static_bytes - seg.static_bytes
+    assert abs(saved - (26 * 4 * n - 5 * 4 * n)) < 0.01 * saved
+
+
 FAKE = 0x7f0000000000  # never dereferenced: every call below fails validation first
 
 
