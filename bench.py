@@ -218,7 +218,8 @@ def desc_of(cfg: W.Config):
                            rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
                            d_model=cfg.d_model, n_heads=cfg.n_heads, d_ff=cfg.d_ff,
                            vocab=cfg.vocab, seq=cfg.seq, n_blocks=cfg.n_blocks,
-                           meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps, rope_base=cfg.rope_base)
+                           meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps, rope_base=cfg.rope_base,
+                           fused_attention=cfg.fused_attention)
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
@@ -267,7 +268,7 @@ WORKLOADS = {
                              "theta_0), SGD lr 0.05, bf16 GEMM operands"),
     "c4_long_context": ("decoder 4 blocks d 512, 8 heads, FF 2048, vocab 8192, 8192 tokens per "
                         "batch as S x 8192/S sequences for S = 2048, 4096, 8192, T=2, per-token "
-                        "loss weights, bf16 GEMM operands, attention materialised"),
+                        "loss weights, bf16 GEMM operands"),
     "toy_mstep_map": ("motivating example: y_0 = x w (1024 x 4096, w 4096 x 4096), M map steps "
                       "y_i = i (2 + sin y)^cos y, mean squared error, MAML, T=2, SGD lr 1e-3, "
                       "fp32"),
@@ -280,11 +281,18 @@ def c4_long(S: int) -> W.Config:
     return W.C4.with_(name=f"c4_S{S}", seq=S, rows=8192 // S, val_rows=8192 // S, T=2)
 
 
+def with_attention(cfg: W.Config, form: str) -> W.Config:
+    """A transformer workload with fused or materialised attention."""
+    if cfg.kind != W.KIND_TRANSFORMER:
+        return cfg
+    return cfg.with_(fused_attention=int(form == "fused"))
+
+
 def bench_config(name: str, args):
     """meta-gradients/s of one of the other workloads at its own T, same timing
     protocol as the main line (inputs resident, warm-up calls, HIP-event timing
     on the stream); no roofline, sweep or CPU baseline."""
-    cfg = BENCH_CONFIGS[name]
+    cfg = with_attention(BENCH_CONFIGS[name], args.attention)
     ms, peak, finite = time_config(cfg, args)
     print(json.dumps({
         "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
@@ -292,7 +300,8 @@ def bench_config(name: str, args):
         "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.PREC_BF16 else "f32",
         "data": "synthetic (seeded, see workloads/)",
-        "config": {"workload": WORKLOADS[name], "name": name, "T": cfg.T},
+        "config": {"workload": WORKLOADS[name], "name": name, "T": cfg.T,
+                   **({"attention": args.attention} if cfg.kind == W.KIND_TRANSFORMER else {})},
         "peak_bytes": peak, "roofline": None, "cpu_baseline": None, "d_eta_finite": finite}))
 
 
@@ -322,13 +331,17 @@ def bench_toy(args):
 
 def bench_long_context(args):
     """The config-4 decoder at long contexts: time and peak device bytes per
-    meta-gradient for each S in C4_LONG_S (8192 tokens per batch, T = 2)."""
+    meta-gradient for each S in C4_LONG_S (8192 tokens per batch, T = 2), with
+    fused and with materialised attention; `value` is the --attention form at the
+    longest S."""
     rows = {}
     for S in W.C4_LONG_S:
-        ms, peak, finite = time_config(c4_long(S), args)
-        rows[str(S)] = {"ms_per_meta_grad": round(ms, 4), "peak_bytes": peak,
-                        "d_eta_finite": finite}
-    ref = rows[str(W.C4_LONG_S[-1])]
+        rows[str(S)] = {}
+        for form in ("fused", "materialised"):
+            ms, peak, finite = time_config(with_attention(c4_long(S), form), args)
+            rows[str(S)][form] = {"ms_per_meta_grad": round(ms, 4), "peak_bytes": peak,
+                                  "d_eta_finite": finite}
+    ref = rows[str(W.C4_LONG_S[-1])][args.attention]
     print(json.dumps({
         "metric": "meta-gradients/sec on 1 MI355X",
         "value": round(1e3 / ref["ms_per_meta_grad"], 4),
@@ -336,7 +349,7 @@ def bench_long_context(args):
         "ms_per_step": ref["ms_per_meta_grad"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, see workloads/)",
         "config": {"workload": WORKLOADS["c4_long_context"], "name": "c4_long_context", "T": 2,
-                   "S": W.C4_LONG_S[-1]},
+                   "S": W.C4_LONG_S[-1], "attention": args.attention},
         "vs_S": rows, "roofline": None, "cpu_baseline": None}))
 
 
@@ -405,6 +418,8 @@ def main():
                     help="workload; the default (c5) line carries the roofline, the memory "
                          "sweep and the CPU baseline, the others throughput only")
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
+    ap.add_argument("--attention", default="fused", choices=["fused", "materialised"],
+                    help="attention form of the transformer workloads")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_bytes or (1 << 30),

@@ -135,6 +135,16 @@ typedef struct {
    * the appendix on static device memory proposes (whose logarithmic form
    * needs a recursive schedule).  Ignored for Adam and when k >= T. */
   int ckpt_segment;
+  /* Transformer kind only.  0 materialises each block's attention
+   * probabilities P and their tangent (B*H*S^2 per block, kept from the
+   * forward for the backward).  1 runs fused causal attention: the forward
+   * keeps running row maxima and sums over key blocks and saves two floats per
+   * query row (log-sum-exp and <P, Sd>); the backward recomputes P and its
+   * tangent per tile, so attention adds O(B*H*S) to dynamic memory instead of
+   * O(B*H*S^2).  Same quantities as 0 (Section 2.2, the dual products of
+   * softmax attention); requires MFMG_PREC_BF16, head dimension
+   * d_model / n_heads = 64 and seq a multiple of 64. */
+  int fused_attention;
 } mfmg_problem_desc;
 
 typedef struct mfmg_problem* mfmg_problem_t;

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmfmg.so")
-SOURCES = ["gemm.hip", "elementwise.hip", "transformer.hip", "tf_engine.hip", "api.hip"]
+SOURCES = ["gemm.hip", "elementwise.hip", "transformer.hip", "attention.hip", "tf_engine.hip", "api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

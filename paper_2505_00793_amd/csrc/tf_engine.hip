@@ -20,6 +20,7 @@
 #include <vector>
 
 #include <initializer_list>
+#include <type_traits>
 
 #include "kernels.h"
 #include "tf_engine.h"
@@ -46,7 +47,7 @@ struct Carver {
 constexpr int MAXB = 16;
 
 struct Lay {
-  int d, H, dh, F, V, S, Bt, Bv, L, mh, VE;
+  int d, H, dh, F, V, S, Bt, Bv, L, mh, VE, fused;
   float eps, lr;
   double base;
   long emb, ln1g[MAXB], ln1b[MAXB], wqkv[MAXB], wo[MAXB], ln2g[MAXB], ln2b[MAXB], w1[MAXB],
@@ -72,6 +73,7 @@ Lay make_lay(const mfmg_problem_desc& D) {
   y.L = D.n_blocks;
   y.mh = D.meta_hidden;
   y.VE = D.precision == MFMG_PREC_BF16 ? 8 : 4;
+  y.fused = D.fused_attention;
   y.eps = D.ln_eps;
   y.lr = D.sgd_lr;
   y.base = D.rope_base;
@@ -134,8 +136,9 @@ struct Act {  // one inner step at up to maxB sequences (the dynamic memory)
   T *a2[MAXB], *a2T[MAXB], *a2d[MAXB], *a2dT[MAXB];
   T *Q[MAXB], *QT[MAXB], *K[MAXB], *KT[MAXB], *Vv[MAXB], *VT[MAXB];
   T *Qd[MAXB], *QdT[MAXB], *Kd[MAXB], *KdT[MAXB], *Vd[MAXB], *VdT[MAXB];
-  float *P32[MAXB], *Pd32[MAXB];
+  float *P32[MAXB], *Pd32[MAXB];                 // materialised attention only
   T *Pb[MAXB], *PbT[MAXB], *Pdb[MAXB], *PdbT[MAXB];
+  float *lse[MAXB], *cst[MAXB], *ar, *ard;       // fused attention only: per query row
   T *O[MAXB], *OT[MAXB], *Od[MAXB], *OdT[MAXB];
   float *Z1[MAXB], *Z1d[MAXB];
   T *A1[MAXB], *A1T[MAXB], *A1d[MAXB], *A1dT[MAXB];
@@ -185,9 +188,16 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
     a.Qd[b] = OPT(BH * hrow); a.QdT[b] = OPT(BH * hcol);
     a.Kd[b] = OPT(BH * hrow); a.KdT[b] = OPT(BH * hcol);
     a.Vd[b] = OPT(BH * hrow); a.VdT[b] = OPT(BH * hcol);
-    a.P32[b] = F32(BH * S * S); a.Pd32[b] = F32(BH * S * S);
-    a.Pb[b] = OPT(BH * S * y.ld(S)); a.PbT[b] = OPT(BH * S * y.ld(S));
-    a.Pdb[b] = OPT(BH * S * y.ld(S)); a.PdbT[b] = OPT(BH * S * y.ld(S));
+    if (y.fused) {
+      a.P32[b] = a.Pd32[b] = nullptr;
+      a.Pb[b] = a.PbT[b] = a.Pdb[b] = a.PdbT[b] = nullptr;
+      a.lse[b] = F32(BH * S); a.cst[b] = F32(BH * S);
+    } else {
+      a.P32[b] = F32(BH * S * S); a.Pd32[b] = F32(BH * S * S);
+      a.Pb[b] = OPT(BH * S * y.ld(S)); a.PbT[b] = OPT(BH * S * y.ld(S));
+      a.Pdb[b] = OPT(BH * S * y.ld(S)); a.PdbT[b] = OPT(BH * S * y.ld(S));
+      a.lse[b] = a.cst[b] = nullptr;
+    }
     a.O[b] = OPT(N * y.ld(d)); a.OT[b] = OPT(d * y.ld(N));
     a.Od[b] = OPT(N * y.ld(d)); a.OdT[b] = OPT(d * y.ld(N));
     a.Z1[b] = F32(N * F); a.Z1d[b] = F32(N * F);
@@ -202,10 +212,17 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
   a.qkv32 = F32(N * 3 * d); a.qkvd32 = F32(N * 3 * d);
   a.Qh = F32(N * d); a.Kh = F32(N * d); a.Vh = F32(N * d);
   a.Qdh = F32(N * d); a.Kdh = F32(N * d); a.Vdh = F32(N * d);
-  a.S32 = F32(BH * S * S); a.Sd32 = F32(BH * S * S);
-  a.dS32 = F32(BH * S * S); a.dSd32 = F32(BH * S * S);
-  a.dS = OPT(BH * S * y.ld(S)); a.dST = OPT(BH * S * y.ld(S));
-  a.dSd = OPT(BH * S * y.ld(S)); a.dSdT = OPT(BH * S * y.ld(S));
+  if (y.fused) {
+    a.S32 = a.Sd32 = a.dS32 = a.dSd32 = nullptr;
+    a.dS = a.dST = a.dSd = a.dSdT = nullptr;
+    a.ar = F32(BH * S); a.ard = F32(BH * S);
+  } else {
+    a.S32 = F32(BH * S * S); a.Sd32 = F32(BH * S * S);
+    a.dS32 = F32(BH * S * S); a.dSd32 = F32(BH * S * S);
+    a.dS = OPT(BH * S * y.ld(S)); a.dST = OPT(BH * S * y.ld(S));
+    a.dSd = OPT(BH * S * y.ld(S)); a.dSdT = OPT(BH * S * y.ld(S));
+    a.ar = a.ard = nullptr;
+  }
   a.dz = OPT(N * y.ld(y.V)); a.dzT = OPT((long)y.V * y.ld(N));
   a.dzd = OPT(N * y.ld(y.V)); a.dzdT = OPT((long)y.V * y.ld(N));
   a.dh = F32(N * d); a.dhd = F32(N * d);
@@ -327,6 +344,30 @@ struct TfEng {
     o.ws = a.skws;
     o.ws_floats = a.skws_n;
     return o;
+  }
+  // Operands of block b's fused attention (bf16 only: the option is rejected
+  // for float32 operands before any plan is made).
+  AttnArgs attn_args(int b, int Bn, bool dual, const Act<T>& a) const {
+    AttnArgs t;
+    std::memset(&t, 0, sizeof(t));
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      t.Q = a.Q[b]; t.K = a.K[b]; t.V = a.Vv[b]; t.QT = a.QT[b]; t.KT = a.KT[b]; t.VT = a.VT[b];
+      if (dual) {
+        t.Qd = a.Qd[b]; t.Kd = a.Kd[b]; t.Vd = a.Vd[b];
+        t.QdT = a.QdT[b]; t.KdT = a.KdT[b]; t.VdT = a.VdT[b];
+      }
+      t.O = a.O[b]; t.OT = a.OT[b];
+      t.Od = dual ? a.Od[b] : nullptr; t.OdT = dual ? a.OdT[b] : nullptr;
+      t.dO = a.dOh; t.dOT = a.dOhT;
+      t.dOd = dual ? a.dOdh : nullptr; t.dOdT = dual ? a.dOdhT : nullptr;
+    }
+    t.ldO = (int)y.ld(y.d);
+    t.ldOT = (int)y.ld((long)Bn * y.S);
+    t.lse = a.lse[b]; t.cst = a.cst[b]; t.r = a.ar; t.rd = a.ard;
+    t.dQ = a.Qh; t.dK = a.Kh; t.dV = a.Vh; t.dQd = a.Qdh; t.dKd = a.Kdh; t.dVd = a.Vdh;
+    t.S = y.S; t.H = y.H; t.BH = Bn * y.H; t.dh = y.dh; t.dual = dual;
+    t.scale = 1.0f / std::sqrt((float)y.dh);
+    return t;
   }
   static int fl(bool dual, bool ad = true) {
     return G_C1 | (dual ? (G_BD | (ad ? G_AD : 0)) : 0);
@@ -454,30 +495,34 @@ struct TfEng {
                 {dual ? a.Kdh : nullptr, a.Kd[b], a.KdT[b]},
                 {dual ? a.Vdh : nullptr, a.Vd[b], a.VdT[b]}},
                S, dh, BH, sh, hrow, hcol));
-      // scores S = scale Q K^T (per head), softmax
-      {
-        GemmOperands<T> o = op(a.Q[b], dual ? a.Qd[b] : nullptr, a.K[b], dual ? a.Kd[b] : nullptr,
-                               (int)y.ld(dh), (int)y.ld(dh), S, S, dh);
-        o.batch = BH; o.sA = hrow; o.sB = hrow;
-        HC(store(o, fl(dual), a.S32, a.Sd32, S, (long)S * S, scale, dual));
-      }
-      SoftmaxArgs sm;
-      std::memset(&sm, 0, sizeof(sm));
-      sm.Sc = a.S32; sm.Scd = a.Sd32; sm.P = a.P32[b]; sm.Pd = a.Pd32[b];
-      sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
-      HC(softmax_fwd(sm, s));
-      HC(convs({{a.P32[b], a.Pb[b], a.PbT[b]}, {dual ? a.Pd32[b] : nullptr, a.Pdb[b], a.PdbT[b]}},
-               S, S, BH, (long)S * S, pS, pS));
-      // O = P V (per head) -> token-major operands
-      {
-        GemmOperands<T> o = op(a.Pb[b], dual ? a.Pdb[b] : nullptr, a.VT[b], dual ? a.VdT[b] : nullptr,
-                               (int)y.ld(S), (int)y.ld(S), S, dh, S);
-        o.batch = BH; o.sA = pS; o.sB = hcol;
-        EpiHeadMerge<T> e;
-        e.O = a.O[b]; e.OT = a.OT[b]; e.Od = a.Od[b]; e.OdT = a.OdT[b];
-        e.ldO = (int)y.ld(d); e.ldOT = (int)y.ld(N);
-        e.seq = S; e.heads = H; e.dh = dh; e.M = S; e.N = dh; e.dual = dual;
-        HC(gemm_head_merge<T>(o, fl(dual), e, s));
+      if (y.fused) {
+        HC(attn_fwd(attn_args(b, Bn, dual, a), s));
+      } else {
+        // scores S = scale Q K^T (per head), softmax
+        {
+          GemmOperands<T> o = op(a.Q[b], dual ? a.Qd[b] : nullptr, a.K[b], dual ? a.Kd[b] : nullptr,
+                                 (int)y.ld(dh), (int)y.ld(dh), S, S, dh);
+          o.batch = BH; o.sA = hrow; o.sB = hrow;
+          HC(store(o, fl(dual), a.S32, a.Sd32, S, (long)S * S, scale, dual));
+        }
+        SoftmaxArgs sm;
+        std::memset(&sm, 0, sizeof(sm));
+        sm.Sc = a.S32; sm.Scd = a.Sd32; sm.P = a.P32[b]; sm.Pd = a.Pd32[b];
+        sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
+        HC(softmax_fwd(sm, s));
+        HC(convs({{a.P32[b], a.Pb[b], a.PbT[b]}, {dual ? a.Pd32[b] : nullptr, a.Pdb[b], a.PdbT[b]}},
+                 S, S, BH, (long)S * S, pS, pS));
+        // O = P V (per head) -> token-major operands
+        {
+          GemmOperands<T> o = op(a.Pb[b], dual ? a.Pdb[b] : nullptr, a.VT[b], dual ? a.VdT[b] : nullptr,
+                                 (int)y.ld(S), (int)y.ld(S), S, dh, S);
+          o.batch = BH; o.sA = pS; o.sB = hcol;
+          EpiHeadMerge<T> e;
+          e.O = a.O[b]; e.OT = a.OT[b]; e.Od = a.Od[b]; e.OdT = a.OdT[b];
+          e.ldO = (int)y.ld(d); e.ldOT = (int)y.ld(N);
+          e.seq = S; e.heads = H; e.dh = dh; e.M = S; e.N = dh; e.dual = dual;
+          HC(gemm_head_merge<T>(o, fl(dual), e, s));
+        }
       }
       // h_mid = h + O Wo
       {
@@ -619,37 +664,41 @@ struct TfEng {
                                  (int)y.ld(d), (int)y.ld(d), N, d, d),
                               fl(dual), e, s));
       }
-      {  // dP = dO V^T
-        GemmOperands<T> o = op(a.dOh, dual ? a.dOdh : nullptr, a.Vv[b], dual ? a.Vd[b] : nullptr,
-                               (int)y.ld(dh), (int)y.ld(dh), S, S, dh);
-        o.batch = BH; o.sA = hrow; o.sB = hrow;
-        HC(store(o, fl(dual), a.S32, a.Sd32, S, (long)S * S, 1.0f, dual));
-      }
-      {  // dV = P^T dO
-        GemmOperands<T> o = op(a.PbT[b], dual ? a.PdbT[b] : nullptr, a.dOhT, dual ? a.dOdhT : nullptr,
-                               (int)y.ld(S), (int)y.ld(S), S, dh, S);
-        o.batch = BH; o.sA = pS; o.sB = hcol;
-        HC(store(o, fl(dual), a.Vh, a.Vdh, dh, (long)S * dh, 1.0f, dual));
-      }
-      SoftmaxArgs sm;
-      std::memset(&sm, 0, sizeof(sm));
-      sm.P = a.P32[b]; sm.Pd = a.Pd32[b]; sm.dP = a.S32; sm.dPd = a.Sd32;
-      sm.dS = a.dS32; sm.dSd = a.dSd32; sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
-      sm.scale = scale;
-      HC(softmax_bwd(sm, s));
-      HC(convs({{a.dS32, a.dS, a.dST}, {dual ? a.dSd32 : nullptr, a.dSd, a.dSdT}}, S, S, BH,
-               (long)S * S, pS, pS));
-      {  // dQ = dS K
-        GemmOperands<T> o = op(a.dS, dual ? a.dSd : nullptr, a.KT[b], dual ? a.KdT[b] : nullptr,
-                               (int)y.ld(S), (int)y.ld(S), S, dh, S);
-        o.batch = BH; o.sA = pS; o.sB = hcol;
-        HC(store(o, fl(dual), a.Qh, a.Qdh, dh, (long)S * dh, 1.0f, dual));
-      }
-      {  // dK = dS^T Q
-        GemmOperands<T> o = op(a.dST, dual ? a.dSdT : nullptr, a.QT[b], dual ? a.QdT[b] : nullptr,
-                               (int)y.ld(S), (int)y.ld(S), S, dh, S);
-        o.batch = BH; o.sA = pS; o.sB = hcol;
-        HC(store(o, fl(dual), a.Kh, a.Kdh, dh, (long)S * dh, 1.0f, dual));
+      if (y.fused) {
+        HC(attn_bwd(attn_args(b, Bn, dual, a), s));
+      } else {
+        {  // dP = dO V^T
+          GemmOperands<T> o = op(a.dOh, dual ? a.dOdh : nullptr, a.Vv[b], dual ? a.Vd[b] : nullptr,
+                                 (int)y.ld(dh), (int)y.ld(dh), S, S, dh);
+          o.batch = BH; o.sA = hrow; o.sB = hrow;
+          HC(store(o, fl(dual), a.S32, a.Sd32, S, (long)S * S, 1.0f, dual));
+        }
+        {  // dV = P^T dO
+          GemmOperands<T> o = op(a.PbT[b], dual ? a.PdbT[b] : nullptr, a.dOhT, dual ? a.dOdhT : nullptr,
+                                 (int)y.ld(S), (int)y.ld(S), S, dh, S);
+          o.batch = BH; o.sA = pS; o.sB = hcol;
+          HC(store(o, fl(dual), a.Vh, a.Vdh, dh, (long)S * dh, 1.0f, dual));
+        }
+        SoftmaxArgs sm;
+        std::memset(&sm, 0, sizeof(sm));
+        sm.P = a.P32[b]; sm.Pd = a.Pd32[b]; sm.dP = a.S32; sm.dPd = a.Sd32;
+        sm.dS = a.dS32; sm.dSd = a.dSd32; sm.rows = (long)BH * S; sm.S = S; sm.dual = dual;
+        sm.scale = scale;
+        HC(softmax_bwd(sm, s));
+        HC(convs({{a.dS32, a.dS, a.dST}, {dual ? a.dSd32 : nullptr, a.dSd, a.dSdT}}, S, S, BH,
+                 (long)S * S, pS, pS));
+        {  // dQ = dS K
+          GemmOperands<T> o = op(a.dS, dual ? a.dSd : nullptr, a.KT[b], dual ? a.KdT[b] : nullptr,
+                                 (int)y.ld(S), (int)y.ld(S), S, dh, S);
+          o.batch = BH; o.sA = pS; o.sB = hcol;
+          HC(store(o, fl(dual), a.Qh, a.Qdh, dh, (long)S * dh, 1.0f, dual));
+        }
+        {  // dK = dS^T Q
+          GemmOperands<T> o = op(a.dST, dual ? a.dSdT : nullptr, a.QT[b], dual ? a.QdT[b] : nullptr,
+                                 (int)y.ld(S), (int)y.ld(S), S, dh, S);
+          o.batch = BH; o.sA = pS; o.sB = hcol;
+          HC(store(o, fl(dual), a.Kh, a.Kdh, dh, (long)S * dh, 1.0f, dual));
+        }
       }
       RopeArgs r;
       std::memset(&r, 0, sizeof(r));
@@ -817,6 +866,10 @@ const char* tf_validate(const mfmg_problem_desc& D) {
     return "meta_hidden must be a multiple of 8 in [8, 256]";
   if (!(D.ln_eps > 0.f) || !(D.rope_base > 0.f) || !std::isfinite(D.sgd_lr))
     return "ln_eps and rope_base must be > 0, sgd_lr finite";
+  if (D.fused_attention != 0 && D.fused_attention != 1) return "fused_attention must be 0 or 1";
+  if (D.fused_attention &&
+      (D.precision != MFMG_PREC_BF16 || !attn_fused_supported(D.seq, dh)))
+    return "fused attention needs bf16 operands, head dim 64 and seq a multiple of 64";
   return nullptr;
 }
 

@@ -53,6 +53,22 @@ struct SoftmaxArgs {
   float scale;
 };
 
+// Fused causal attention of head dimension 64 over bf16 operands (forward and
+// backward, primal or dual).  Per-head operands are rows [B*H][S][64] and
+// transposes [B*H][64][S]; S is a multiple of 64.
+struct AttnArgs {
+  const bf16_t *Q, *K, *V, *QT, *KT, *VT;         // per-head operands
+  const bf16_t *Qd, *Kd, *Vd, *QdT, *KdT, *VdT;   // their tangents (dual)
+  bf16_t *O, *OT, *Od, *OdT;                      // token-major [N][ldO], transposed [d][ldOT]
+  int ldO, ldOT;
+  float *lse, *cst;                               // [B*H][S] saved by the forward: m + log l, <P, Sd>
+  const bf16_t *dO, *dOT, *dOd, *dOdT;            // per-head cotangent of O (and its tangent)
+  float *r, *rd;                                  // [B*H][S] <dO, O>, <dOd, O> + <dO, Od>
+  float *dQ, *dK, *dV, *dQd, *dKd, *dVd;          // fp32 per-head rows [B*H][S][64]
+  int S, H, BH, dh, dual;
+  float scale;
+};
+
 // Token positions sorted by id are cut into segments: maximal runs of one id,
 // split further at every multiple of EMB_SEG in the sorted order, so that a
 // segment holds at most EMB_SEG positions of one token.
@@ -87,6 +103,9 @@ hipError_t rope_split(const RopeArgs& a, hipStream_t s);
 hipError_t rope_merge(const RopeArgs& a, hipStream_t s);
 hipError_t softmax_fwd(const SoftmaxArgs& a, hipStream_t s);
 hipError_t softmax_bwd(const SoftmaxArgs& a, hipStream_t s);
+bool attn_fused_supported(int S, int dh);
+hipError_t attn_fwd(const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd(const AttnArgs& a, hipStream_t s);  // dQ pass (writes r, rd), then dK/dV pass
 bool sort_tokens_fits(int N);
 int embed_segments_max(int N);
 hipError_t sort_tokens(const int* ids, int N, int V, const TokenSegs& ts, hipStream_t s);

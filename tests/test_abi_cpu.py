@@ -88,6 +88,11 @@ def test_create_rejects_bad_descriptions(L, field, value, status):
     (W.C5, {"ckpt_segment": -1}, 1),
     (W.C5, {"meta": W.META_MAML, "optimizer": W.OPT_ADAM}, 2),   # MAML is SGD only
     (W.C4, {"meta": W.META_MAML}, 2),                  # and MLP only
+    (W.C5, {"fused_attention": 1}, 1),                  # attention options are transformer only
+    (W.C4, {"fused_attention": 2}, 2),
+    (W.C4.with_(precision=W.PREC_FP32), {"fused_attention": 1}, 2),   # bf16 operands only
+    (W.C4.with_(n_heads=4), {"fused_attention": 1}, 2),               # head dim 128
+    (W.C4.with_(seq=160, rows=8, val_rows=8), {"fused_attention": 1}, 2),  # seq % 64 != 0
 ])
 def test_create_rejects_bad_options(L, cfg, fields, status):
     d = desc_of(cfg)
@@ -109,6 +114,23 @@ def test_segment_checkpoints_shrink_static_memory():
     # 32 + 1 operand checkpoints (4 B per weight) against 6 + 1 and 5 float32 thetas
     saved = full.static_bytes - seg.static_bytes
     assert abs(saved - (26 * 4 * n - 5 * 4 * n)) < 0.01 * saved
+
+
+def test_fused_attention_drops_quadratic_buffers():
+    """Dynamic bytes of the full transformer workload with fused attention: the
+    per-block probabilities (2 fp32 + 4 bf16 copies of B*H*S^2) and the shared
+    score buffers (4 fp32 + 4 bf16) are gone; per-row statistics (2 floats per
+    row and block, 2 shared) are added (size query only, no GPU)."""
+    T = 8
+    cfg = W.C4
+    mat = M.Problem(desc_of(cfg)).mfmg_query_sizes(T)
+    fus = M.Problem(desc_of(cfg.with_(fused_attention=1))).mfmg_query_sizes(T)
+    assert mat.static_bytes == fus.static_bytes
+    BH, S, L = cfg.val_rows * cfg.n_heads, cfg.seq, cfg.n_blocks
+    quad = BH * S * S * (L * (2 * 4 + 4 * 2) + 4 * 4 + 4 * 2)
+    rows = BH * S * 4 * (2 * L + 2)
+    saved = mat.dynamic_bytes - fus.dynamic_bytes
+    assert abs(saved - (quad - rows)) < 4096 * (L * 10 + 12)
 
 
 FAKE = 0x7f0000000000  # never dereferenced: every call below fails validation first

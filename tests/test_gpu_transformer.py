@@ -33,7 +33,9 @@ def c(a):
 SMALL = W.SMALL["c4_small"]
 CASES = {"fp32": SMALL.with_(precision=W.PREC_FP32), "bf16": SMALL}
 # the full transformer workload: d 512, 8 heads, 4 blocks, vocab 8192, 16 x 256 tokens
-FULL = {"fp32": W.C4.with_(precision=W.PREC_FP32), "bf16": W.C4}
+FULL = {"fp32": W.C4.with_(precision=W.PREC_FP32), "bf16": W.C4,
+        "bf16_fused": W.C4.with_(fused_attention=1)}
+FUSED = W.SMALL["c4_fused"]
 
 
 def token_alpha(cfg, theta, eta, tokens):
@@ -50,9 +52,14 @@ def test_tf_inner_step(prec):
     check_inner_step(CASES[prec], prec)
 
 
-@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16", "bf16_fused"])
 def test_tf_inner_step_full_size(prec):
     check_inner_step(FULL[prec], prec)
+
+
+def test_tf_inner_step_fused():
+    """Fused attention, primal forward and backward (three 64-query blocks)."""
+    check_inner_step(FUSED, "bf16_fused")
 
 
 def check_inner_step(cfg, prec):
@@ -63,7 +70,7 @@ def check_inner_step(cfg, prec):
     alpha = token_alpha(cfg, theta, inp["eta"], tok)
     print(f"\n[tf inner_step] {cfg.name} {prec}", flush=True)
     th1_ref, _, g_ref, L_ref = oracle.inner_step(cfg, theta, None, inp["eta"], tok, None, 0,
-                                                 alpha=alpha, bf16=prec == "bf16")
+                                                 alpha=alpha, bf16=prec.startswith("bf16"))
     P = M().Problem(desc_of(cfg))
     th1 = torch.empty(n, device="cuda")
     g = torch.empty(n, device="cuda")
@@ -94,6 +101,11 @@ def test_tf_hvp_full_size_fp32():
     check_hvp(FULL["fp32"], "fp32")
 
 
+def test_tf_hvp_fused():
+    """Fused attention, dual forward and backward: H v and the mixed product."""
+    check_hvp(FUSED, "bf16_fused")
+
+
 def check_hvp(cfg, prec):
     inp = W.make_inputs(cfg, T=1)
     n = W.n_theta(cfg)
@@ -101,7 +113,7 @@ def check_hvp(cfg, prec):
     v = 0.1 * W.random_direction(n, 53)
     tok = inp["train_x"][0]
     alpha = token_alpha(cfg, theta, inp["eta"], tok)
-    bf16 = prec == "bf16"
+    bf16 = prec.startswith("bf16")
     print(f"\n[tf hvp] {cfg.name} {prec}", flush=True)
     hv_ref = oracle.hvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
     mv_ref = oracle.mvp_rev_rev(cfg, theta, tok, None, v, alpha=alpha, bf16=bf16)
@@ -165,6 +177,40 @@ def test_tf_meta_grad_mid_bf16():
     assert np.all(np.isfinite(got))
     assert max(errs) <= tol_of(cfg)
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
+@pytest.mark.parametrize("name", ["c4_fused", "c4_long_fused"])
+def test_tf_meta_grad_fused(name):
+    """Fused attention through the whole meta-gradient (192- and 1024-token
+    sequences, head dim 64) against the oracle's bf16 emulation."""
+    cfg = W.SMALL[name]
+    inp = W.make_inputs(cfg)
+    print(f"\n[tf meta_grad] {name} S={cfg.seq}", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=True)
+    errs = group_errors(cfg, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
+def test_tf_fused_matches_materialised_full_size():
+    """The full transformer workload at T=2 with both attention forms: the two
+    differ only in where bf16 rounding happens (unnormalised probabilities in
+    the fused form), and use less dynamic memory when fused."""
+    base = W.C4.with_(T=2)
+    inp = W.make_inputs(base, T=2)
+    print("\n[tf fused vs materialised] full size T=2", flush=True)
+    ref, Vr, peak_r = run_meta_tf(base, inp)
+    got, V, peak = run_meta_tf(base.with_(fused_attention=1), inp)
+    errs = group_errors(base, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} / {Vr:.6f} "
+          f"peak {peak / 1e9:.2f} / {peak_r / 1e9:.2f} GB", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(base)
+    assert abs(V - Vr) <= 1e-3 * abs(Vr)
+    assert peak < peak_r
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])

@@ -67,6 +67,7 @@ class Config:
     wd_init: float = 1e-4
     map_steps: int = 0                     # M of the toy map (LOSS_MAPMSE)
     ckpt_segment: int = 0                  # GPU static-memory segments (0: keep every step)
+    fused_attention: int = 0               # transformer, bf16: fused causal attention (no S^2 buffers)
     # transformer
     d_model: int = 0
     n_heads: int = 0
@@ -184,6 +185,14 @@ SMALL: Dict[str, Config] = {
     # enough tokens (8 x 160) for the split-K weight gradients, an odd vocabulary
     "c4_mid": C4.with_(name="c4_mid", cfg_id=113, d_model=128, n_heads=4, d_ff=256, vocab=301,
                        seq=160, rows=8, val_rows=4, n_blocks=2, meta_hidden=32, T=2),
+    # fused attention (head dim 64, bf16): three 64-query blocks per sequence,
+    # so diagonal and off-diagonal key blocks; and a 1024-token context
+    "c4_fused": C4.with_(name="c4_fused", cfg_id=120, d_model=128, n_heads=2, d_ff=256, vocab=97,
+                         seq=192, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2,
+                         fused_attention=1),
+    "c4_long_fused": C4.with_(name="c4_long_fused", cfg_id=121, d_model=128, n_heads=2, d_ff=256,
+                              vocab=97, seq=1024, rows=2, val_rows=1, n_blocks=1, meta_hidden=16,
+                              T=2, fused_attention=1),
 }
 
 
