@@ -288,10 +288,14 @@ def test_bruteforce_hessian_vs_fd_of_gradient(key):
     assert np.abs(H - Hfd).max() < 1e-7 * max(1.0, np.abs(H).max())
 
 
-@pytest.mark.parametrize("name", ["c2_small", "c5_small", "c3_small", "c4_small"])
-def test_fwd_over_rev_equals_rev_over_rev(name):
-    """JVP of the gradient map (forward-over-reverse, torch.func) == the oracle's
-    reverse-over-reverse HVP; and the per-row loss tangents == the mixed product."""
+@pytest.mark.parametrize("name", ["c2_small", "c5_small", "c3_small", "c4_small", "c4_fused"])
+def test_three_hvp_modes_agree(name):
+    """The three HVP modes of Section 2.2 on one batch: the JVP of the gradient map
+    (forward-over-reverse), the gradient of the directional derivative <grad L, v>
+    taken in forward mode (reverse-over-forward), both by torch.func, and the
+    oracle's reverse-over-reverse HVP agree to rounding; the per-row loss tangents
+    equal the mixed product, also when taken as the alpha-gradient of the
+    forward-mode directional derivative."""
     cfg = W.SMALL[name]
     th, x, y = _one_batch(cfg)
     v = W.random_direction(th.size, 3).astype(np.float64)
@@ -313,6 +317,17 @@ def test_fwd_over_rev_equals_rev_over_rev(name):
     _, ldot = torch.func.jvp(rows, (tht,), (vt,))
     assert relerr(hv_fr.numpy(), hv_rr) < 1e-12
     assert relerr(ldot.numpy() / ldot.numel(), mv_rr) < 1e-12
+
+    def weighted(p, a):
+        return OM.inner_loss(cfg, p, a, xt, yt, False)
+
+    def dir_deriv(p, a):   # <grad_theta L(p, a), v> in forward mode
+        return torch.func.jvp(lambda q: weighted(q, a), (p,), (vt,))[1]
+
+    a1 = torch.ones(ldot.numel(), dtype=torch.float64)
+    hv_rf, mv_rf = torch.func.grad(dir_deriv, argnums=(0, 1))(tht, a1)
+    assert relerr(hv_rf.numpy(), hv_rr) < 1e-12
+    assert relerr(mv_rf.numpy(), mv_rr) < 1e-12
 
 
 # ---------------------------------------------------------------------------------------
