@@ -20,12 +20,17 @@
 // the sums run in a fixed order.
 //
 // Tiles of 64 queries x 64 keys; four waves per workgroup, each owning 16
-// rows.  Products use v_mfma_f32_16x16x32_bf16 in the NT form (both operands
-// with the contraction index contiguous): a lane holds row lane%16, elements
-// 8 (lane/16) .. +7 of a 32-deep slice, and the accumulator holds rows
-// 4 (lane/16) + 0..3 of column lane%16.  Probabilities and score cotangents
-// go through a per-wave LDS tile to move from the accumulator layout to the
-// operand layout.
+// rows (queries, or keys in the dK/dV pass).  Products use
+// v_mfma_f32_16x16x32_bf16 in the NT form: C[i][j] += sum_k a_i[k] b_j[k],
+// where a lane holds elements k = 8 (lane/16) + 0..7 of row lane%16 of each
+// operand, and the accumulator holds C[4 (lane/16) + 0..3][lane%16].
+// Probabilities and score cotangents never leave registers: the score
+// products are formed so that the lane's accumulator values share the row
+// index the next product needs (lane%16), and the next product contracts over
+// the 64 keys (or queries) in a permuted order in which lane group g, element
+// t of slice c is index 16 (2c + t/4) + 4g + t%4 -- exactly the four
+// accumulator values of the lane in subtiles 2c and 2c+1.  The operand read
+// from LDS takes the same order with two 8-byte reads.
 #include "transformer.h"
 
 namespace mfmg {
@@ -59,25 +64,51 @@ __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row, int lg, int c
   return ld8(lds + row * LP + 8 * lg + 32 * c);
 }
 
-__device__ __forceinline__ float max16(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float sum16(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Operand fragment c of row `row` of an LDS tile in the permuted order.
+__device__ __forceinline__ bf16x8 pfrag(const bf16_t* lds, int row, int lg, int c) {
+  const bf16_t* p = lds + row * LP + 32 * c + 4 * lg;
+  union {
+    bf16x8 v;
+    uint2 h[2];
+  } x;
+  x.h[0] = *reinterpret_cast<const uint2*>(p);
+  x.h[1] = *reinterpret_cast<const uint2*>(p + 16);
+  return x.v;
+}
+
+// Register fragment c in the permuted order from the values of subtiles 2c, 2c+1.
+__device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi) {
+  union {
+    bf16x8 v;
+    uint32_t u[4];
+  } x;
+  x.u[0] = (uint32_t)f2bf(lo[0]) | ((uint32_t)f2bf(lo[1]) << 16);
+  x.u[1] = (uint32_t)f2bf(lo[2]) | ((uint32_t)f2bf(lo[3]) << 16);
+  x.u[2] = (uint32_t)f2bf(hi[0]) | ((uint32_t)f2bf(hi[1]) << 16);
+  x.u[3] = (uint32_t)f2bf(hi[2]) | ((uint32_t)f2bf(hi[3]) << 16);
+  return x.v;
+}
+
+// Sum over the four lane groups (lanes with the same lane%16).
+__device__ __forceinline__ float sum_groups(float v) {
+  v += __shfl_xor(v, 16, 64);
+  return v + __shfl_xor(v, 32, 64);
+}
+__device__ __forceinline__ float max_groups(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  return fmaxf(v, __shfl_xor(v, 32, 64));
+}
+
 // ---------------------------------------------------------------- forward
+// Wave w owns queries q0 .. q0+15; lane holds query q0 + lane%16.  Per key
+// block: S^T (keys x queries) = K Q^T, so the lane's 16 values are keys
+// 16 n + 4 g + r of its own query; O^T (dims x queries) += V^T P^T.
 template <bool DUAL>
 __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sVT[DH * LP],
       sVdT[DH * LP];
-  __shared__ __attribute__((aligned(16))) bf16_t sP[4][16 * LP], sPd[4][16 * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
@@ -85,19 +116,17 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
   const int bh = blockIdx.y;
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int q0 = qb * AB + w * 16;
+  const int ql = w * 16 + lr;  // the lane's query within the block
   bf16x8 qf[2], qdf[2];
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     qf[c] = ld8(a.Q + hb + (long)(q0 + lr) * DH + 8 * lg + 32 * c);
     if (DUAL) qdf[c] = ld8(a.Qd + hb + (long)(q0 + lr) * DH + 8 * lg + 32 * c);
   }
-  float m[4], l[4], cs[4];
+  float m = -INFINITY, l = 0.f, cs = 0.f;
   f32x4 o[4], o2[4], o3[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    m[i] = -INFINITY; l[i] = 0.f; cs[i] = 0.f;
-    o[i] = zero4(); o2[i] = zero4(); o3[i] = zero4();
-  }
+  for (int i = 0; i < 4; ++i) { o[i] = zero4(); o2[i] = zero4(); o3[i] = zero4(); }
   const float sc = a.scale;
   for (int kb = 0; kb <= qb; ++kb) {
     __syncthreads();
@@ -115,109 +144,99 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const bf16x8 kf = frag(sK, n * 16 + lr, lg, c);
-        s[n] = mma(qf[c], kf, s[n]);
+        s[n] = mma(kf, qf[c], s[n]);
         if (DUAL) {
-          sd[n] = mma(qdf[c], kf, sd[n]);
-          sd[n] = mma(qf[c], frag(sKd, n * 16 + lr, lg, c), sd[n]);
+          sd[n] = mma(kf, qdf[c], sd[n]);
+          sd[n] = mma(frag(sKd, n * 16 + lr, lg, c), qf[c], sd[n]);
         }
       }
     }
     const bool diag = kb == qb;
-    float al[4];
+    float mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qrow = w * 16 + 4 * lg + r;  // within the block
-      float mx = -INFINITY;
+    for (int n = 0; n < 4; ++n)
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
+      for (int r = 0; r < 4; ++r) {
         float v = s[n][r] * sc;
-        if (diag && n * 16 + lr > qrow) v = -INFINITY;
+        if (diag && n * 16 + 4 * lg + r > ql) v = -INFINITY;
         s[n][r] = v;
         mx = fmaxf(mx, v);
       }
-      mx = max16(mx);
-      const float mn = fmaxf(m[r], mx);
-      al[r] = __expf(m[r] - mn);
-      m[r] = mn;
-      float ls = 0.f, lc = 0.f;
+    mx = max_groups(mx);
+    const float mn = fmaxf(m, mx);
+    const float al = __expf(m - mn);
+    m = mn;
+    float ls = 0.f, lc = 0.f;
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        const float p = __expf(s[n][r] - mn);
-        ls += p;
-        sP[w][(4 * lg + r) * LP + n * 16 + lr] = f2bf(p);
-        if (DUAL) {
-          const float t = p * sd[n][r] * sc;
-          lc += t;
-          sPd[w][(4 * lg + r) * LP + n * 16 + lr] = f2bf(t);
-        }
-      }
-      l[r] = l[r] * al[r] + ls;
-      if (DUAL) cs[r] = cs[r] * al[r] + lc;
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int n = 0; n < 4; ++n)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        o[e][r] *= al[r];
-        if (DUAL) { o2[e][r] *= al[r]; o3[e][r] *= al[r]; }
-      }
-    __syncthreads();
-    bf16x8 pf[2], pdf[2];
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      pf[c] = frag(sP[w], lr, lg, c);
-      if (DUAL) pdf[c] = frag(sPd[w], lr, lg, c);
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 vf = frag(sVT, e * 16 + lr, lg, c);
-        o[e] = mma(pf[c], vf, o[e]);
+        const float p = __expf(s[n][r] - mn);
+        ls += p;
+        s[n][r] = p;
         if (DUAL) {
-          o2[e] = mma(pdf[c], vf, o2[e]);
-          o3[e] = mma(pf[c], frag(sVdT, e * 16 + lr, lg, c), o3[e]);
+          sd[n][r] = p * sd[n][r] * sc;
+          lc += sd[n][r];
         }
       }
+    l = l * al + ls;
+    if (DUAL) cs = cs * al + lc;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] *= al;
+      if (DUAL) { o2[e] *= al; o3[e] *= al; }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 pf = pack8(s[2 * c], s[2 * c + 1]);
+      bf16x8 pdf;
+      if (DUAL) pdf = pack8(sd[2 * c], sd[2 * c + 1]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x8 vf = pfrag(sVT, e * 16 + lr, lg, c);
+        o[e] = mma(vf, pf, o[e]);
+        if (DUAL) {
+          o2[e] = mma(vf, pdf, o2[e]);
+          o3[e] = mma(pfrag(sVdT, e * 16 + lr, lg, c), pf, o3[e]);
+        }
+      }
+    }
   }
   const int bs = bh / a.H, h = bh % a.H;
-  const long tok0 = (long)bs * S + q0 + 4 * lg;  // token of accumulator row 0
-  float inv[4], cc[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float lt = sum16(l[r]);
-    inv[r] = 1.0f / lt;
-    cc[r] = DUAL ? sum16(cs[r]) * inv[r] : 0.f;
-    if (lr == 0) {
-      a.lse[(long)bh * S + q0 + 4 * lg + r] = m[r] + __logf(lt);
-      if (DUAL) a.cst[(long)bh * S + q0 + 4 * lg + r] = cc[r];
-    }
+  const long tok = (long)bs * S + q0 + lr;
+  const float lt = sum_groups(l);
+  const float inv = 1.0f / lt;
+  const float cc = DUAL ? sum_groups(cs) * inv : 0.f;
+  if (lg == 0) {
+    a.lse[(long)bh * S + q0 + lr] = m + __logf(lt);
+    if (DUAL) a.cst[(long)bh * S + q0 + lr] = cc;
   }
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const int col = h * DH + e * 16 + lr;
+    const int col = h * DH + e * 16 + 4 * lg;  // dims col .. col+3 of the lane's token
     float ov[4], odv[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      ov[r] = o[e][r] * inv[r];
-      a.O[(tok0 + r) * a.ldO + col] = f2bf(ov[r]);
-      if (DUAL) {
-        odv[r] = (o2[e][r] + o3[e][r]) * inv[r] - cc[r] * ov[r];
-        a.Od[(tok0 + r) * a.ldO + col] = f2bf(odv[r]);
-      }
+      ov[r] = o[e][r] * inv;
+      if (DUAL) odv[r] = (o2[e][r] + o3[e][r]) * inv - cc * ov[r];
     }
-    store4(a.OT + (long)col * a.ldOT + tok0, ov[0], ov[1], ov[2], ov[3]);
-    if (DUAL) store4(a.OdT + (long)col * a.ldOT + tok0, odv[0], odv[1], odv[2], odv[3]);
+    store4(a.O + tok * a.ldO + col, ov[0], ov[1], ov[2], ov[3]);
+    if (DUAL) store4(a.Od + tok * a.ldO + col, odv[0], odv[1], odv[2], odv[3]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      a.OT[(long)(col + r) * a.ldOT + tok] = f2bf(ov[r]);
+      if (DUAL) a.OdT[(long)(col + r) * a.ldOT + tok] = f2bf(odv[r]);
+    }
   }
 }
 
 // ---------------------------------------------------------------- backward: dQ
+// Lane holds query q0 + lane%16 as in the forward; S^T, dP^T = V dO^T and
+// their tangents per key block, then dQ^T += K^T dS^T.
 template <bool DUAL>
 __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sV[AB * LP],
       sVd[AB * LP], sKT[DH * LP], sKdT[DH * LP];
-  __shared__ __attribute__((aligned(16))) bf16_t sS[4][16 * LP], sSd[4][16 * LP];
-  __shared__ float sR[4][16], sRd[4][16];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
@@ -226,8 +245,9 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
   const int bs = bh / a.H, h = bh % a.H;
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int q0 = qb * AB + w * 16;
+  const int ql = w * 16 + lr;
   bf16x8 qf[2], qdf[2], gf[2], gdf[2];
-  float r0 = 0.f, r1 = 0.f;
+  float rr = 0.f, rrd = 0.f;
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const long off = hb + (long)(q0 + lr) * DH + 8 * lg + 32 * c;
@@ -241,32 +261,20 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
       const bf16x8 odf = ld8(a.Od + ooff);
 #pragma unroll
       for (int k = 0; k < 8; ++k)
-        r1 += (float)gdf[c][k] * (float)of[k] + (float)gf[c][k] * (float)odf[k];
+        rrd += (float)gdf[c][k] * (float)of[k] + (float)gf[c][k] * (float)odf[k];
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) r0 += (float)gf[c][k] * (float)of[k];
+    for (int k = 0; k < 8; ++k) rr += (float)gf[c][k] * (float)of[k];
   }
-  r0 += __shfl_xor(r0, 16, 64);
-  r0 += __shfl_xor(r0, 32, 64);
-  if (DUAL) {
-    r1 += __shfl_xor(r1, 16, 64);
-    r1 += __shfl_xor(r1, 32, 64);
-  }
+  rr = sum_groups(rr);
+  if (DUAL) rrd = sum_groups(rrd);
+  const long row = (long)bh * S + q0 + lr;
   if (lg == 0) {
-    sR[w][lr] = r0;
-    sRd[w][lr] = r1;
-    a.r[(long)bh * S + q0 + lr] = r0;
-    if (DUAL) a.rd[(long)bh * S + q0 + lr] = r1;
+    a.r[row] = rr;
+    if (DUAL) a.rd[row] = rrd;
   }
-  __syncthreads();
-  float rr[4], rrd[4], lse[4], cst[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    rr[r] = sR[w][4 * lg + r];
-    rrd[r] = sRd[w][4 * lg + r];
-    lse[r] = a.lse[(long)bh * S + q0 + 4 * lg + r];
-    cst[r] = DUAL ? a.cst[(long)bh * S + q0 + 4 * lg + r] : 0.f;
-  }
+  const float lse = a.lse[row];
+  const float cst = DUAL ? a.cst[row] : 0.f;
   f32x4 dq[4], dqd[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) { dq[e] = zero4(); dqd[e] = zero4(); }
@@ -283,70 +291,68 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
     }
     __syncthreads();
     const bool diag = kb == qb;
+    f32x4 ds[4], dsd[4];
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       f32x4 s = zero4(), sd = zero4(), dp = zero4(), dpd = zero4();
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const bf16x8 kf = frag(sK, n * 16 + lr, lg, c), vf = frag(sV, n * 16 + lr, lg, c);
-        s = mma(qf[c], kf, s);
-        dp = mma(gf[c], vf, dp);
+        s = mma(kf, qf[c], s);
+        dp = mma(vf, gf[c], dp);
         if (DUAL) {
-          sd = mma(qdf[c], kf, sd);
-          sd = mma(qf[c], frag(sKd, n * 16 + lr, lg, c), sd);
-          dpd = mma(gdf[c], vf, dpd);
-          dpd = mma(gf[c], frag(sVd, n * 16 + lr, lg, c), dpd);
+          sd = mma(kf, qdf[c], sd);
+          sd = mma(frag(sKd, n * 16 + lr, lg, c), qf[c], sd);
+          dpd = mma(vf, gdf[c], dpd);
+          dpd = mma(frag(sVd, n * 16 + lr, lg, c), gf[c], dpd);
         }
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const bool ok = !diag || n * 16 + lr <= w * 16 + 4 * lg + r;
-        const float p = ok ? __expf(s[r] * sc - lse[r]) : 0.f;
-        const float g = dp[r] - rr[r];
-        sS[w][(4 * lg + r) * LP + n * 16 + lr] = f2bf(sc * p * g);
+        const bool ok = !diag || n * 16 + 4 * lg + r <= ql;
+        const float p = ok ? __expf(s[r] * sc - lse) : 0.f;
+        const float g = dp[r] - rr;
+        ds[n][r] = sc * p * g;
         if (DUAL) {
-          const float pd = p * (sd[r] * sc - cst[r]);
-          sSd[w][(4 * lg + r) * LP + n * 16 + lr] = f2bf(sc * (pd * g + p * (dpd[r] - rrd[r])));
+          const float pd = p * (sd[r] * sc - cst);
+          dsd[n][r] = sc * (pd * g + p * (dpd[r] - rrd));
         }
       }
     }
-    __syncthreads();
-    bf16x8 df[2], ddf[2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      df[c] = frag(sS[w], lr, lg, c);
-      if (DUAL) ddf[c] = frag(sSd[w], lr, lg, c);
-    }
+      const bf16x8 df = pack8(ds[2 * c], ds[2 * c + 1]);
+      bf16x8 ddf;
+      if (DUAL) ddf = pack8(dsd[2 * c], dsd[2 * c + 1]);
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 kt = frag(sKT, e * 16 + lr, lg, c);
-        dq[e] = mma(df[c], kt, dq[e]);
+      for (int e = 0; e < 4; ++e) {
+        const bf16x8 kt = pfrag(sKT, e * 16 + lr, lg, c);
+        dq[e] = mma(kt, df, dq[e]);
         if (DUAL) {
-          dqd[e] = mma(ddf[c], kt, dqd[e]);
-          dqd[e] = mma(df[c], frag(sKdT, e * 16 + lr, lg, c), dqd[e]);
+          dqd[e] = mma(kt, ddf, dqd[e]);
+          dqd[e] = mma(pfrag(sKdT, e * 16 + lr, lg, c), df, dqd[e]);
         }
       }
+    }
   }
 #pragma unroll
-  for (int e = 0; e < 4; ++e)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const long off = hb + (long)(q0 + 4 * lg + r) * DH + e * 16 + lr;
-      a.dQ[off] = dq[e][r];
-      if (DUAL) a.dQd[off] = dqd[e][r];
-    }
+  for (int e = 0; e < 4; ++e) {
+    const long off = hb + (long)(q0 + lr) * DH + e * 16 + 4 * lg;
+    store4(a.dQ + off, dq[e][0], dq[e][1], dq[e][2], dq[e][3]);
+    if (DUAL) store4(a.dQd + off, dqd[e][0], dqd[e][1], dqd[e][2], dqd[e][3]);
+  }
 }
 
 // ---------------------------------------------------------------- backward: dK, dV
+// Wave w owns keys k0 .. k0+15; lane holds key k0 + lane%16.  Per query
+// block: S (queries x keys) = Q K^T and dP = dO V^T with their tangents, so
+// the lane's 16 values are queries 16 n + 4 g + r of its own key; then
+// dV^T += dO^T P and dK^T += Q^T dS.
 template <bool DUAL>
-__global__ void __launch_bounds__(256) attn_bwd_dkv_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) attn_bwd_dkv_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sQ[AB * LP], sQd[AB * LP], sG[AB * LP],
       sGd[AB * LP], sQT[DH * LP], sQdT[DH * LP], sGT[DH * LP], sGdT[DH * LP];
-  __shared__ __attribute__((aligned(16))) bf16_t sP[4][16 * LP], sPd[4][16 * LP],
-      sS[4][16 * LP], sSd[4][16 * LP];
-  __shared__ float sL[AB], sC[AB], sR[AB], sRd[AB];
+  __shared__ __attribute__((aligned(16))) float sL[AB], sC[AB], sR[AB], sRd[AB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
@@ -354,6 +360,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_kernel(AttnArgs a) {
   const int bh = blockIdx.y;
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int k0 = kb * AB + w * 16;
+  const int kl = w * 16 + lr;  // the lane's key within the block
   bf16x8 kf[2], kdf[2], vf[2], vdf[2];
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
@@ -392,77 +399,81 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_kernel(AttnArgs a) {
     }
     __syncthreads();
     const bool diag = kb == qb;
-#pragma unroll
-    for (int n = 0; n < 4; ++n) {  // 16 queries n*16 .. of the block
-      f32x4 s = zero4(), sd = zero4(), dp = zero4(), dpd = zero4();
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 qq = frag(sQ, n * 16 + lr, lg, c), gg = frag(sG, n * 16 + lr, lg, c);
-        s = mma(kf[c], qq, s);
-        dp = mma(vf[c], gg, dp);
-        if (DUAL) {
-          sd = mma(kdf[c], qq, sd);
-          sd = mma(kf[c], frag(sQd, n * 16 + lr, lg, c), sd);
-          dpd = mma(vdf[c], gg, dpd);
-          dpd = mma(vf[c], frag(sGd, n * 16 + lr, lg, c), dpd);
-        }
-      }
-      const int ql = n * 16 + lr;
-      const float L = sL[ql], R = sR[ql];
-      const float C = DUAL ? sC[ql] : 0.f, Rd = DUAL ? sRd[ql] : 0.f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {  // key w*16 + 4*lg + r of the block
-        const bool ok = !diag || w * 16 + 4 * lg + r <= ql;
-        const float p = ok ? __expf(s[r] * sc - L) : 0.f;
-        const float g = dp[r] - R;
-        const int at = (4 * lg + r) * LP + ql;
-        sP[w][at] = f2bf(p);
-        sS[w][at] = f2bf(sc * p * g);
-        if (DUAL) {
-          const float pd = p * (sd[r] * sc - C);
-          sPd[w][at] = f2bf(pd);
-          sSd[w][at] = f2bf(sc * (pd * g + p * (dpd[r] - Rd)));
-        }
-      }
-    }
-    __syncthreads();
-    bf16x8 pf[2], pdf[2], df[2], ddf[2];
+    // Slice c of the query contraction: subtiles 2c, 2c+1 are formed, packed
+    // and consumed before the next pair, which keeps half as many values live.
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      pf[c] = frag(sP[w], lr, lg, c);
-      df[c] = frag(sS[w], lr, lg, c);
-      if (DUAL) {
-        pdf[c] = frag(sPd[w], lr, lg, c);
-        ddf[c] = frag(sSd[w], lr, lg, c);
-      }
-    }
+      f32x4 p[2], pd[2], ds[2], dsd[2];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+      for (int h2 = 0; h2 < 2; ++h2) {  // queries 16 n + 4 g + r of the block
+        const int n = 2 * c + h2;
+        f32x4 s = zero4(), sd = zero4(), dp = zero4(), dpd = zero4();
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 gt = frag(sGT, e * 16 + lr, lg, c), qt = frag(sQT, e * 16 + lr, lg, c);
-        dv[e] = mma(pf[c], gt, dv[e]);
-        dk[e] = mma(df[c], qt, dk[e]);
+        for (int cc = 0; cc < 2; ++cc) {
+          const bf16x8 qq = frag(sQ, n * 16 + lr, lg, cc), gg = frag(sG, n * 16 + lr, lg, cc);
+          s = mma(qq, kf[cc], s);
+          dp = mma(gg, vf[cc], dp);
+          if (DUAL) {
+            sd = mma(qq, kdf[cc], sd);
+            sd = mma(frag(sQd, n * 16 + lr, lg, cc), kf[cc], sd);
+            dpd = mma(gg, vdf[cc], dpd);
+            dpd = mma(frag(sGd, n * 16 + lr, lg, cc), vf[cc], dpd);
+          }
+        }
+        const int qr = n * 16 + 4 * lg;
+        const float4 L = *reinterpret_cast<const float4*>(sL + qr);
+        const float4 R = *reinterpret_cast<const float4*>(sR + qr);
+        float4 C = make_float4(0.f, 0.f, 0.f, 0.f), Rd = C;
         if (DUAL) {
-          dvd[e] = mma(pdf[c], gt, dvd[e]);
-          dvd[e] = mma(pf[c], frag(sGdT, e * 16 + lr, lg, c), dvd[e]);
-          dkd[e] = mma(ddf[c], qt, dkd[e]);
-          dkd[e] = mma(df[c], frag(sQdT, e * 16 + lr, lg, c), dkd[e]);
+          C = *reinterpret_cast<const float4*>(sC + qr);
+          Rd = *reinterpret_cast<const float4*>(sRd + qr);
+        }
+        const float Lr[4] = {L.x, L.y, L.z, L.w}, Rr[4] = {R.x, R.y, R.z, R.w};
+        const float Cr[4] = {C.x, C.y, C.z, C.w}, Rdr[4] = {Rd.x, Rd.y, Rd.z, Rd.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = !diag || kl <= qr + r;
+          const float pv = ok ? __expf(s[r] * sc - Lr[r]) : 0.f;
+          const float g = dp[r] - Rr[r];
+          p[h2][r] = pv;
+          ds[h2][r] = sc * pv * g;
+          if (DUAL) {
+            const float pdv = pv * (sd[r] * sc - Cr[r]);
+            pd[h2][r] = pdv;
+            dsd[h2][r] = sc * (pdv * g + pv * (dpd[r] - Rdr[r]));
+          }
         }
       }
-  }
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const long off = hb + (long)(k0 + 4 * lg + r) * DH + e * 16 + lr;
-      a.dK[off] = dk[e][r];
-      a.dV[off] = dv[e][r];
+      const bf16x8 pf = pack8(p[0], p[1]), df = pack8(ds[0], ds[1]);
+      bf16x8 pdf, ddf;
       if (DUAL) {
-        a.dKd[off] = dkd[e][r];
-        a.dVd[off] = dvd[e][r];
+        pdf = pack8(pd[0], pd[1]);
+        ddf = pack8(dsd[0], dsd[1]);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x8 gt = pfrag(sGT, e * 16 + lr, lg, c), qt = pfrag(sQT, e * 16 + lr, lg, c);
+        dv[e] = mma(gt, pf, dv[e]);
+        dk[e] = mma(qt, df, dk[e]);
+        if (DUAL) {
+          dvd[e] = mma(gt, pdf, dvd[e]);
+          dvd[e] = mma(pfrag(sGdT, e * 16 + lr, lg, c), pf, dvd[e]);
+          dkd[e] = mma(qt, ddf, dkd[e]);
+          dkd[e] = mma(pfrag(sQdT, e * 16 + lr, lg, c), df, dkd[e]);
+        }
       }
     }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const long off = hb + (long)(k0 + lr) * DH + e * 16 + 4 * lg;
+    store4(a.dK + off, dk[e][0], dk[e][1], dk[e][2], dk[e][3]);
+    store4(a.dV + off, dv[e][0], dv[e][1], dv[e][2], dv[e][3]);
+    if (DUAL) {
+      store4(a.dKd + off, dkd[e][0], dkd[e][1], dkd[e][2], dkd[e][3]);
+      store4(a.dVd + off, dvd[e][0], dvd[e][1], dvd[e][2], dvd[e][3]);
+    }
+  }
 }
 
 }  // namespace
