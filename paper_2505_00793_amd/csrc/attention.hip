@@ -39,7 +39,12 @@ namespace {
 
 constexpr int AB = 64;       // queries or keys per block
 constexpr int DH = 64;       // head dimension
-constexpr int LP = DH + 8;   // LDS row pitch in bf16 elements (144 bytes)
+constexpr int LP = DH;       // LDS row pitch in bf16 elements (128 bytes)
+
+// Element offset of 16-byte chunk `chunk` of row `row` in an LDS tile: the
+// chunk index is XOR-swizzled by the row, so the 16 rows one fragment read
+// touches fall on different banks.
+__device__ __forceinline__ int sw(int row, int chunk) { return row * LP + ((chunk ^ (row & 7)) << 3); }
 
 __device__ __forceinline__ f32x4 mma(const bf16x8& a, const bf16x8& b, f32x4 acc) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
@@ -54,27 +59,28 @@ __device__ __forceinline__ void stage(bf16_t* lds, const bf16_t* __restrict__ g,
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int i = tid + 256 * k, r = i >> 3, ch = i & 7;
-    *reinterpret_cast<uint4*>(lds + r * LP + ch * 8) =
+    *reinterpret_cast<uint4*>(lds + sw(r, ch)) =
         *reinterpret_cast<const uint4*>(g + (long)r * ld + ch * 8);
   }
 }
 
 // Operand fragment c (0, 1) of row `row` of an LDS tile.
 __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row, int lg, int c) {
-  return ld8(lds + row * LP + 8 * lg + 32 * c);
+  return ld8(lds + sw(row, lg + 4 * c));
 }
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
 // Operand fragment c of row `row` of an LDS tile in the permuted order.
 __device__ __forceinline__ bf16x8 pfrag(const bf16_t* lds, int row, int lg, int c) {
-  const bf16_t* p = lds + row * LP + 32 * c + 4 * lg;
+  // elements 32c + 4 lg .. +3 and 32c + 16 + 4 lg .. +3 of the row
+  const int half = (lg & 1) * 4;
   union {
     bf16x8 v;
     uint2 h[2];
   } x;
-  x.h[0] = *reinterpret_cast<const uint2*>(p);
-  x.h[1] = *reinterpret_cast<const uint2*>(p + 16);
+  x.h[0] = *reinterpret_cast<const uint2*>(lds + sw(row, 4 * c + (lg >> 1)) + half);
+  x.h[1] = *reinterpret_cast<const uint2*>(lds + sw(row, 4 * c + 2 + (lg >> 1)) + half);
   return x.v;
 }
 
@@ -106,7 +112,7 @@ __device__ __forceinline__ float max_groups(float v) {
 // block: S^T (keys x queries) = K Q^T, so the lane's 16 values are keys
 // 16 n + 4 g + r of its own query; O^T (dims x queries) += V^T P^T.
 template <bool DUAL>
-__global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 3) attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sVT[DH * LP],
       sVdT[DH * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -234,7 +240,7 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
 // Lane holds query q0 + lane%16 as in the forward; S^T, dP^T = V dO^T and
 // their tangents per key block, then dQ^T += K^T dS^T.
 template <bool DUAL>
-__global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 3) attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sV[AB * LP],
       sVd[AB * LP], sKT[DH * LP], sKdT[DH * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -291,39 +297,40 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnArgs a) {
     }
     __syncthreads();
     const bool diag = kb == qb;
-    f32x4 ds[4], dsd[4];
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      f32x4 s = zero4(), sd = zero4(), dp = zero4(), dpd = zero4();
+    for (int c = 0; c < 2; ++c) {  // keys of subtiles 2c, 2c+1, then their products
+      f32x4 ds[2], dsd[2];
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 kf = frag(sK, n * 16 + lr, lg, c), vf = frag(sV, n * 16 + lr, lg, c);
-        s = mma(kf, qf[c], s);
-        dp = mma(vf, gf[c], dp);
-        if (DUAL) {
-          sd = mma(kf, qdf[c], sd);
-          sd = mma(frag(sKd, n * 16 + lr, lg, c), qf[c], sd);
-          dpd = mma(vf, gdf[c], dpd);
-          dpd = mma(frag(sVd, n * 16 + lr, lg, c), gf[c], dpd);
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int n = 2 * c + h2;
+        f32x4 s = zero4(), sd = zero4(), dp = zero4(), dpd = zero4();
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+          const bf16x8 kf = frag(sK, n * 16 + lr, lg, cc), vf = frag(sV, n * 16 + lr, lg, cc);
+          s = mma(kf, qf[cc], s);
+          dp = mma(vf, gf[cc], dp);
+          if (DUAL) {
+            sd = mma(kf, qdf[cc], sd);
+            sd = mma(frag(sKd, n * 16 + lr, lg, cc), qf[cc], sd);
+            dpd = mma(vf, gdf[cc], dpd);
+            dpd = mma(frag(sVd, n * 16 + lr, lg, cc), gf[cc], dpd);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = !diag || n * 16 + 4 * lg + r <= ql;
+          const float p = ok ? __expf(s[r] * sc - lse) : 0.f;
+          const float g = dp[r] - rr;
+          ds[h2][r] = sc * p * g;
+          if (DUAL) {
+            const float pd = p * (sd[r] * sc - cst);
+            dsd[h2][r] = sc * (pd * g + p * (dpd[r] - rrd));
+          }
         }
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool ok = !diag || n * 16 + 4 * lg + r <= ql;
-        const float p = ok ? __expf(s[r] * sc - lse) : 0.f;
-        const float g = dp[r] - rr;
-        ds[n][r] = sc * p * g;
-        if (DUAL) {
-          const float pd = p * (sd[r] * sc - cst);
-          dsd[n][r] = sc * (pd * g + p * (dpd[r] - rrd));
-        }
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const bf16x8 df = pack8(ds[2 * c], ds[2 * c + 1]);
+      const bf16x8 df = pack8(ds[0], ds[1]);
       bf16x8 ddf;
-      if (DUAL) ddf = pack8(dsd[2 * c], dsd[2 * c + 1]);
+      if (DUAL) ddf = pack8(dsd[0], dsd[1]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bf16x8 kt = pfrag(sKT, e * 16 + lr, lg, c);
