@@ -335,13 +335,15 @@ def bench_long_context(args):
     fused and with materialised attention; `value` is the --attention form at the
     longest S."""
     rows = {}
-    for S in W.C4_LONG_S:
+    seqs = (args.seq,) if args.seq else W.C4_LONG_S
+    forms = (args.attention,) if args.seq else ("fused", "materialised")
+    for S in seqs:
         rows[str(S)] = {}
-        for form in ("fused", "materialised"):
+        for form in forms:
             ms, peak, finite = time_config(with_attention(c4_long(S), form), args)
             rows[str(S)][form] = {"ms_per_meta_grad": round(ms, 4), "peak_bytes": peak,
                                   "d_eta_finite": finite}
-    ref = rows[str(W.C4_LONG_S[-1])][args.attention]
+    ref = rows[str(seqs[-1])][args.attention]
     print(json.dumps({
         "metric": "meta-gradients/sec on 1 MI355X",
         "value": round(1e3 / ref["ms_per_meta_grad"], 4),
@@ -349,7 +351,7 @@ def bench_long_context(args):
         "ms_per_step": ref["ms_per_meta_grad"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, see workloads/)",
         "config": {"workload": WORKLOADS["c4_long_context"], "name": "c4_long_context", "T": 2,
-                   "S": W.C4_LONG_S[-1], "attention": args.attention},
+                   "S": seqs[-1], "attention": args.attention},
         "vs_S": rows, "roofline": None, "cpu_baseline": None}))
 
 
@@ -420,6 +422,8 @@ def main():
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
     ap.add_argument("--attention", default="fused", choices=["fused", "materialised"],
                     help="attention form of the transformer workloads")
+    ap.add_argument("--seq", type=int, default=0, choices=[0, *W.C4_LONG_S],
+                    help="c4_long_context: time this sequence length and --attention form only")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_bytes or (1 << 30),

@@ -71,6 +71,18 @@ __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row, int lg, int c
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Block index (0 = most work) and head of this workgroup, for a grid of
+// nblk x nbh.  Workgroups go to the 8 XCDs round-robin by linear id; when the
+// grid divides evenly, each XCD is given a contiguous run of (head, block)
+// pairs, so the tiles of a head are read through one XCD's L2.
+__device__ __forceinline__ void block_of(int nblk, int nbh, int& blk, int& bh) {
+  const int L = blockIdx.x + gridDim.x * blockIdx.y;
+  const int N = nblk * nbh;
+  const int idx = (N & 7) == 0 ? (L & 7) * (N >> 3) + (L >> 3) : L;
+  bh = idx / nblk;
+  blk = idx - bh * nblk;
+}
+
 // Operand fragment c of row `row` of an LDS tile in the permuted order.
 __device__ __forceinline__ bf16x8 pfrag(const bf16_t* lds, int row, int lg, int c) {
   // elements 32c + 4 lg .. +3 and 32c + 16 + 4 lg .. +3 of the row
@@ -118,8 +130,9 @@ __global__ void __launch_bounds__(256, 3) attn_fwd_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // longest rows first
-  const int bh = blockIdx.y;
+  int blk, bh;
+  block_of(nqb, a.BH, blk, bh);
+  const int qb = nqb - 1 - blk;  // longest rows first
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int q0 = qb * AB + w * 16;
   const int ql = w * 16 + lr;  // the lane's query within the block
@@ -246,8 +259,9 @@ __global__ void __launch_bounds__(256, 3) attn_bwd_dq_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
-  const int qb = nqb - 1 - (int)blockIdx.x;
-  const int bh = blockIdx.y;
+  int blk, bh;
+  block_of(nqb, a.BH, blk, bh);
+  const int qb = nqb - 1 - blk;
   const int bs = bh / a.H, h = bh % a.H;
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int q0 = qb * AB + w * 16;
@@ -363,8 +377,8 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkv_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int S = a.S, nqb = S / AB;
-  const int kb = blockIdx.x;  // key block 0 has the most query blocks
-  const int bh = blockIdx.y;
+  int kb, bh;  // key block 0 has the most query blocks
+  block_of(nqb, a.BH, kb, bh);
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
   const int k0 = kb * AB + w * 16;
   const int kl = w * 16 + lr;  // the lane's key within the block
