@@ -957,8 +957,9 @@ hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
 
 // ------------------------------------------------------------------------------------
 // Split-K for backward-weight products with few output tiles and a long k (the
-// token dimension of a transformer's weight gradients): S batched products over
-// k slices write float32 partial sums C1, C2 to the workspace, then a second
+// token dimension of a transformer's weight gradients, and of its meta-model's):
+// S batched products over k slices (128 x 128 tiles for bf16 operands, 64 x 64
+// for float32) write float32 partial sums C1, C2 to the workspace, then a second
 // kernel adds the S slices in order and applies the epilogue (row-major
 // outputs through epi.row, transposed ones through epi.trans).
 // ------------------------------------------------------------------------------------
@@ -1050,7 +1051,11 @@ hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipSt
   EpiStore e;
   e.C = op.ws; e.Cd = op.ws + S * MN; e.ldc = op.N; e.sC = MN; e.scale = 1.0f;
   e.M = op.M; e.N = op.N; e.dual = HC2 ? 1 : 0;
-  hipError_t r = launch<T, FLAGS, 128, 128>(p, StoreOp{e, op.M, op.N}, s);
+  hipError_t r;
+  if constexpr (sizeof(T) == 2)
+    r = launch<T, FLAGS, 128, 128>(p, StoreOp{e, op.M, op.N}, s);
+  else
+    r = launch<T, FLAGS, 64, 64>(p, StoreOp{e, op.M, op.N}, s);
   if (r != hipSuccess) return r;
   const int nb = cdiv(op.M, 16) * cdiv(op.N, 64);
   hipLaunchKernelGGL((splitk_epilogue<Epi>), dim3(nb), dim3(256), 0, s, op.ws,
@@ -1061,7 +1066,7 @@ hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipSt
 template <typename T, int FLAGS, class Epi>
 hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   if (op.M <= 0 || op.N <= 0) return hipSuccess;
-  if constexpr (sizeof(T) == 2 && IsParamOp<Epi>::value) {
+  if constexpr (IsParamOp<Epi>::value) {
     if (op.ws && op.batch == 1) {
       const int S = splitk_count(op.M, op.N, op.K);
       if (S > 1 && op.ws_floats >= 2L * S * op.M * op.N)

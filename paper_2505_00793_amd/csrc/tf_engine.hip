@@ -436,7 +436,7 @@ struct TfEng {
   }
 
   // d eta of the meta-model from ubar (cotangents of u) over all rows.
-  hipError_t meta_vjp_all(Meta& m, float* d_eta) const {
+  hipError_t meta_vjp_all(Meta& m, float* d_eta, const Act<T>& a) const {
     const int d = y.d, h = y.mh;
     const long rows = m.rows;
     const float* w2 = eta + (long)d * h + h;
@@ -451,6 +451,8 @@ struct TfEng {
     o.A = m.ET; o.Ad = nullptr; o.B = m.dhidT; o.Bd = nullptr;
     o.lda = o.ldb = (int)rup(rows, 4);
     o.M = d; o.N = h; o.K = (int)rows;
+    o.ws = a.skws;  // split-K over the T x tokens rows
+    o.ws_floats = a.skws_n;
     ParamArgs<float> P;
     std::memset(&P, 0, sizeof(P));
     P.mode = P_STORE_G;
@@ -789,7 +791,7 @@ hipError_t run_meta_t(const Lay& y, const float* theta0, const float* eta,
     HC(E.backward(p.slot[i], &p.v[vc], y.Bt, P, i > 0 ? &p.v[vc ^ 1] : nullptr, a));
     vc ^= 1;
   }
-  return E.meta_vjp_all(p.meta, d_eta);
+  return E.meta_vjp_all(p.meta, d_eta, p.act);
 }
 
 template <typename T>
