@@ -154,6 +154,120 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(LnBwdArgs a) {
   }
 }
 
+// The same two kernels for d a multiple of 256: lane l holds columns
+// 256 k + 4 l .. +3 and moves 16 bytes per access.
+constexpr int LN_MAXV = LN_MAX_D / 256;
+
+__device__ __forceinline__ f32x4 ldv(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ void stv(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+__device__ __forceinline__ float hsum(f32x4 v) { return (v[0] + v[1]) + (v[2] + v[3]); }
+
+__global__ void __launch_bounds__(256) ln_fwd_vec_kernel(LnArgs a) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.N) return;
+  const int d = a.d, nv = d >> 8;
+  const long base = (long)row * d;
+  f32x4 xv[LN_MAXV], xdv[LN_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      xv[k] = ldv(a.x + base + 256 * k + 4 * lane);
+      s += hsum(xv[k]);
+    }
+  const float mean = wave_sum(s) / d;
+  float v = 0.f;
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      xv[k] -= mean;
+      v += hsum(xv[k] * xv[k]);
+    }
+  const float rstd = rsqrtf(wave_sum(v) / d + a.eps);
+  float c = 0.f, md = 0.f;
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      xv[k] *= rstd;  // xh
+      if (a.dual) {
+        xdv[k] = ldv(a.xd + base + 256 * k + 4 * lane);
+        md += hsum(xdv[k]);
+        c += hsum(xv[k] * xdv[k]);
+      }
+    }
+  if (a.dual) {
+    md = wave_sum(md) / d;
+    c = wave_sum(c) / d;
+  }
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      const int j = 256 * k + 4 * lane;
+      const f32x4 g = ldv(a.g + j);
+      stv(a.xh + base + j, xv[k]);
+      stv(a.y + base + j, g * xv[k] + ldv(a.b + j));
+      if (a.dual) {
+        const f32x4 xhd = rstd * (xdv[k] - md - xv[k] * c);
+        stv(a.xhd + base + j, xhd);
+        stv(a.yd + base + j, g * xhd + ldv(a.gd + j) * xv[k] + ldv(a.bd + j));
+      }
+    }
+  if (lane == 0) {
+    a.rstd[row] = rstd;
+    if (a.dual) a.c[row] = c;
+  }
+}
+
+__global__ void __launch_bounds__(256) ln_bwd_vec_kernel(LnBwdArgs a) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.N) return;
+  const int d = a.d, nv = d >> 8;
+  const long base = (long)row * d;
+  const float rstd = a.rstd[row];
+  f32x4 xh[LN_MAXV], q[LN_MAXV], xhd[LN_MAXV], qd[LN_MAXV];
+  float mq = 0.f, mxq = 0.f, mqd = 0.f, mxdq = 0.f, mxqd = 0.f;
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      const int j = 256 * k + 4 * lane;
+      xh[k] = ldv(a.xh + base + j);
+      const f32x4 dy = ldv(a.dy + base + j), g = ldv(a.g + j);
+      q[k] = g * dy;
+      mq += hsum(q[k]);
+      mxq += hsum(xh[k] * q[k]);
+      if (a.dual) {
+        xhd[k] = ldv(a.xhd + base + j);
+        qd[k] = ldv(a.gd + j) * dy + g * ldv(a.dyd + base + j);
+        mqd += hsum(qd[k]);
+        mxdq += hsum(xhd[k] * q[k]);
+        mxqd += hsum(xh[k] * qd[k]);
+      }
+    }
+  mq = wave_sum(mq) / d;
+  mxq = wave_sum(mxq) / d;
+  if (a.dual) {
+    mqd = wave_sum(mqd) / d;
+    mxdq = wave_sum(mxdq) / d;
+    mxqd = wave_sum(mxqd) / d;
+  }
+  const float rstdd = a.dual ? -rstd * rstd * a.c[row] : 0.f;
+#pragma unroll
+  for (int k = 0; k < LN_MAXV; ++k)
+    if (k < nv) {
+      const int j = 256 * k + 4 * lane;
+      const f32x4 A = q[k] - mq - xh[k] * mxq;
+      const f32x4 hin = a.dh_in ? ldv(a.dh_in + base + j) : f32x4{0.f, 0.f, 0.f, 0.f};
+      stv(a.dh_out + base + j, hin + rstd * A);
+      if (a.dual) {
+        const f32x4 Ad = qd[k] - mqd - xhd[k] * mxq - xh[k] * (mxdq + mxqd);
+        const f32x4 hdin = a.dhd_in ? ldv(a.dhd_in + base + j) : f32x4{0.f, 0.f, 0.f, 0.f};
+        stv(a.dhd_out + base + j, hdin + rstdd * A + rstd * Ad);
+      }
+    }
+}
+
 // Column sums over a chunk of LN_CHUNK rows: partial[chunk][4][d] = sums of
 // dy xh, dy, dyd xh + dy xhd, dyd.  Block: 64 columns x 4 row phases; each
 // phase sums every fourth row of the chunk, then the four are added in order.
@@ -189,20 +303,20 @@ __global__ void __launch_bounds__(256) ln_colsum_kernel(LnBwdArgs a) {
   }
 }
 
-// Column sums of the chunk partials in a fixed order (chunk phase p sums chunks
-// p, p + 4, ...; the four phases are added in order), then the parameter
-// epilogue on g (offset g_off) and b (offset b_off).
+// Column sums of the chunk partials in a fixed order (phase p of 16 sums chunks
+// p, p + 16, ...; the phases are added in order), then the parameter epilogue
+// on g (offset g_off) and b (offset b_off).  16 columns per block.
 template <typename T>
 __global__ void __launch_bounds__(256) ln_param_kernel(const float* __restrict__ partial,
                                                        int nparts, int d, long g_off, long b_off,
                                                        ParamArgs<T> P, float* out_g,
                                                        float* out_b) {
-  __shared__ float red[4][4][64];
-  const int c = threadIdx.x & 63, ph = threadIdx.x >> 6;
-  const int j = blockIdx.x * 64 + c;
+  __shared__ float red[16][4][16];
+  const int c = threadIdx.x & 15, ph = threadIdx.x >> 4;
+  const int j = blockIdx.x * 16 + c;
   float s[4] = {0.f, 0.f, 0.f, 0.f};
   if (j < d) {
-    for (int p = ph; p < nparts; p += 4) {
+    for (int p = ph; p < nparts; p += 16) {
       const float* Pp = partial + (long)p * 4 * d;
 #pragma unroll
       for (int k = 0; k < 4; ++k) s[k] += Pp[k * d + j];
@@ -214,7 +328,10 @@ __global__ void __launch_bounds__(256) ln_param_kernel(const float* __restrict__
   if (ph != 0 || j >= d) return;
   float t[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) t[k] = ((red[0][k][c] + red[1][k][c]) + red[2][k][c]) + red[3][k][c];
+  for (int k = 0; k < 4; ++k) {
+    t[k] = red[0][k][c];
+    for (int q = 1; q < 16; ++q) t[k] += red[q][k][c];
+  }
   const float cg = param_elem(P, g_off + j, t[0], t[2]);
   const float cb = param_elem(P, b_off + j, t[1], t[3]);
   if (out_g) out_g[j] = cg;
@@ -562,7 +679,10 @@ hipError_t gather_rows(const int* ids, int N, int d, const float* E, const float
 }
 
 hipError_t ln_fwd(const LnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(ln_fwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
+  if (a.d % 256 == 0)
+    hipLaunchKernelGGL(ln_fwd_vec_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ln_fwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -572,14 +692,17 @@ template <typename T>
 hipError_t ln_bwd(const LnBwdArgs& a, long g_off, long b_off, const ParamArgs<T>& P,
                   float* out_g, float* out_b, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
+  if (a.d % 256 == 0)
+    hipLaunchKernelGGL(ln_bwd_vec_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(ln_colsum_kernel, dim3(cdivl(a.d, 64), ln_bwd_parts(a.N)), dim3(256), 0, s,
                      a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ln_param_kernel<T>, dim3(cdivl(a.d, 64)), dim3(256), 0, s, a.partial,
+  hipLaunchKernelGGL(ln_param_kernel<T>, dim3(cdivl(a.d, 16)), dim3(256), 0, s, a.partial,
                      ln_bwd_parts(a.N), a.d, g_off, b_off, P, out_g, out_b);
   return hipGetLastError();
 }
