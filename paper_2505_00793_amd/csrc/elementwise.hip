@@ -138,6 +138,46 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ a0
   }
 }
 
+// bf16 version for rows, cols and both leading dimensions multiples of 8: a
+// 64 x 64 tile goes in with one 16-byte load per 8 elements and out with one
+// 16-byte store per 8 transposed elements.
+__global__ void __launch_bounds__(256) transpose_bf16_kernel(const bf16_t* __restrict__ a0,
+                                                             const bf16_t* __restrict__ a1,
+                                                             int rows, int cols, int ld,
+                                                             bf16_t* t0, bf16_t* t1, int ldT) {
+  __shared__ bf16_t tile[64][64 + 2];
+  const bf16_t* src = blockIdx.z ? a1 : a0;
+  bf16_t* dst = blockIdx.z ? t1 : t0;
+  if (!src || !dst) return;
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = threadIdx.x + 256 * k, r = i >> 3, ch = (i & 7) * 8;
+    union {
+      uint4 v;
+      bf16_t e[8];
+    } u;
+    u.v = make_uint4(0, 0, 0, 0);
+    if (r0 + r < rows && c0 + ch < cols)
+      u.v = *reinterpret_cast<const uint4*>(src + (long)(r0 + r) * ld + c0 + ch);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tile[r][ch + e] = u.e[e];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = threadIdx.x + 256 * k, c = i >> 3, rr = (i & 7) * 8;
+    if (c0 + c >= cols || r0 + rr >= rows) continue;
+    union {
+      uint4 v;
+      bf16_t e[8];
+    } u;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u.e[e] = tile[rr + e][c];
+    *reinterpret_cast<uint4*>(dst + (long)(c0 + c) * ldT + r0 + rr) = u.v;
+  }
+}
+
 // ------------------------------------------------------------------------------------
 // Bias entries: column sums of dZ (and its tangent) over the batch rows, read
 // from the transposed copies (one wavefront per column, contiguous reads),
@@ -668,8 +708,16 @@ hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // transposed copies of dL/dz (and its tangent), coalesced through LDS
-  hipLaunchKernelGGL(transpose_kernel<T>, dim3(cdiv(a.C, 64), cdiv(a.rows, 64), 2), dim3(256), 0, s,
-                     a.d, a.dual ? a.dd : nullptr, a.rows, a.C, a.ld, a.dT, a.ddT, a.ldT);
+  const dim3 tg(cdiv(a.C, 64), cdiv(a.rows, 64), 2);
+  if constexpr (sizeof(T) == 2) {
+    if (a.rows % 8 == 0 && a.C % 8 == 0 && a.ld % 8 == 0 && a.ldT % 8 == 0) {
+      hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, s, a.d, a.dual ? a.dd : nullptr,
+                         a.rows, a.C, a.ld, a.dT, a.ddT, a.ldT);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL(transpose_kernel<T>, tg, dim3(256), 0, s, a.d, a.dual ? a.dd : nullptr,
+                     a.rows, a.C, a.ld, a.dT, a.ddT, a.ldT);
   return hipGetLastError();
 }
 
