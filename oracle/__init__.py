@@ -29,7 +29,7 @@ parity against the fp64 mode is by construction only ("parity unpinned" for
 the rounding pattern itself; the unrounded mode is pinned).
 """
 from .metagrad import (meta_grad, meta_grad_checkpointed, unroll, inner_step, grad_and_loss,
-                       hvp_rev_rev, mvp_rev_rev, val_loss_of_eta)
+                       hvp_rev_rev, hvp_rev_fwd, mvp_rev_rev, val_loss_of_eta)
 
 __all__ = ["meta_grad", "meta_grad_checkpointed", "unroll", "inner_step", "grad_and_loss",
-           "hvp_rev_rev", "mvp_rev_rev", "val_loss_of_eta"]
+           "hvp_rev_rev", "hvp_rev_fwd", "mvp_rev_rev", "val_loss_of_eta"]

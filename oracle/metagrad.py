@@ -195,6 +195,25 @@ def hvp_rev_rev(cfg: Config, theta, x, y, v, alpha=None, bf16: bool = False) -> 
     return hv.numpy()
 
 
+def hvp_rev_fwd(cfg: Config, theta, x, y, v, alpha=None) -> Tuple[np.ndarray, np.ndarray]:
+    """(H v, mixed product) by reverse-over-forward, the third mode of Section 2.2:
+    the directional derivative <dL/dtheta, v> is formed in forward mode
+    (torch.func.jvp of L along v) and then differentiated in reverse mode with
+    respect to theta (giving H v) and to the per-row loss weights alpha (giving
+    (d^2 L / d alpha d theta) v, one entry per loss row).  Unrounded operands
+    only (float64)."""
+    th = _t(theta).clone()
+    xt, yt, vt = _t(x), _t(y), _t(v)
+    n_rows = xt.shape[0] if cfg.kind != KIND_TRANSFORMER else xt.shape[0] * (xt.shape[1] - 1)
+    a = torch.ones(n_rows, dtype=F64) if alpha is None else _t(alpha).clone()
+
+    def directional(p, w):
+        return torch.func.jvp(lambda q: inner_loss(cfg, q, w, xt, yt, False), (p,), (vt,))[1]
+
+    hv, mv = torch.func.grad(directional, argnums=(0, 1))(th, a)
+    return hv.numpy(), mv.numpy()
+
+
 def mvp_rev_rev(cfg: Config, theta, x, y, v, alpha=None, bf16: bool = False) -> np.ndarray:
     """Mixed product (d^2 L / d alpha d theta) v, one entry per loss row.
 

@@ -181,6 +181,36 @@ def test_hvp_parity(name):
     assert max(e) <= tol_of(cfg)
 
 
+REV_FWD_CASES = ["toy_small", "c1_small", "c2_small", "c5_tanh_fp32", "c5_gelu_fp32", "c3_fp32"]
+
+
+@pytest.mark.parametrize("name", REV_FWD_CASES)
+def test_hvp_matches_reverse_over_forward(name):
+    """The GPU's forward-over-reverse H v and mixed product against the oracle's
+    reverse-over-forward ones (Section 2.2: the modes compose the same products);
+    float32 operands against float64."""
+    cfg = cfg_of(name)
+    assert cfg.precision == W.PREC_FP32
+    inp = W.make_inputs(cfg)
+    n = W.n_theta(cfg)
+    step = 0
+    theta = start_of(cfg, inp)
+    v = W.random_direction(n, 22)
+    x, y = inp["train_x"][step], inp["train_y"][step]
+    alpha = step_alpha(cfg, inp["eta"], step)
+    print(f"\n[hvp vs rev-over-fwd] {name}", flush=True)
+    hv_ref, mv_ref = oracle.hvp_rev_fwd(cfg, theta, x, y, v, alpha=alpha)
+    P = M().Problem(desc_of(cfg))
+    c = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    hv = torch.empty(n, device="cuda")
+    mv = torch.empty(cfg.rows, device="cuda")
+    P.mfmg_hvp_fwd_over_rev(c(theta), c(inp["eta"]), c(x), c(y), step, c(v), None, hv, mv)
+    torch.cuda.synchronize()
+    e = (relerr(hv.cpu().numpy(), hv_ref), relerr(mv.cpu().numpy(), mv_ref))
+    print(f"  hvp {e[0]:.2e} mvp {e[1]:.2e}", flush=True)
+    assert max(e) <= tol_of(cfg)
+
+
 def test_hvp_symmetry_full_size_c5():
     """u.(H v) == v.(H u) on the full 8 x 4096 ReLU network (a property that holds at
     any size), both products from the GPU's forward-over-reverse pass."""

@@ -101,6 +101,29 @@ def test_tf_hvp_full_size_fp32():
     check_hvp(FULL["fp32"], "fp32")
 
 
+def test_tf_hvp_matches_reverse_over_forward():
+    """Transformer H v and per-token mixed product (float32 operands) against the
+    oracle's reverse-over-forward mode (Section 2.2)."""
+    cfg = CASES["fp32"]
+    inp = W.make_inputs(cfg, T=1)
+    n = W.n_theta(cfg)
+    theta = inp["theta0"] + 0.02 * W.random_direction(n, 54)
+    v = 0.1 * W.random_direction(n, 55)
+    tok = inp["train_x"][0]
+    alpha = token_alpha(cfg, theta, inp["eta"], tok)
+    print("\n[tf hvp vs rev-over-fwd] c4_small fp32", flush=True)
+    hv_ref, mv_ref = oracle.hvp_rev_fwd(cfg, theta, tok, None, v, alpha=alpha)
+    P = M().Problem(desc_of(cfg))
+    hv = torch.empty(n, device="cuda")
+    mv = torch.empty(cfg.rows * cfg.seq, device="cuda")
+    dummy_y = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.mfmg_hvp_fwd_over_rev(c(theta), c(inp["eta"]), c(tok), dummy_y, 0, c(v), None, hv, mv)
+    torch.cuda.synchronize()
+    e = (relerr(hv.cpu().numpy(), hv_ref), relerr(mv.cpu().numpy(), mv_ref))
+    print(f"  hvp {e[0]:.2e} mvp {e[1]:.2e}", flush=True)
+    assert max(e) <= tol_of(cfg)
+
+
 def test_tf_hvp_fused():
     """Fused attention, dual forward and backward: H v and the mixed product."""
     check_hvp(FUSED, "bf16_fused")

@@ -318,16 +318,9 @@ def test_three_hvp_modes_agree(name):
     assert relerr(hv_fr.numpy(), hv_rr) < 1e-12
     assert relerr(ldot.numpy() / ldot.numel(), mv_rr) < 1e-12
 
-    def weighted(p, a):
-        return OM.inner_loss(cfg, p, a, xt, yt, False)
-
-    def dir_deriv(p, a):   # <grad_theta L(p, a), v> in forward mode
-        return torch.func.jvp(lambda q: weighted(q, a), (p,), (vt,))[1]
-
-    a1 = torch.ones(ldot.numel(), dtype=torch.float64)
-    hv_rf, mv_rf = torch.func.grad(dir_deriv, argnums=(0, 1))(tht, a1)
-    assert relerr(hv_rf.numpy(), hv_rr) < 1e-12
-    assert relerr(mv_rf.numpy(), mv_rr) < 1e-12
+    hv_rf, mv_rf = oracle.hvp_rev_fwd(cfg, th, x, y, v)
+    assert relerr(hv_rf, hv_rr) < 1e-12
+    assert relerr(mv_rf, mv_rr) < 1e-12
 
 
 # ---------------------------------------------------------------------------------------
