@@ -124,7 +124,7 @@ __device__ __forceinline__ float max_groups(float v) {
 // block: S^T (keys x queries) = K Q^T, so the lane's 16 values are keys
 // 16 n + 4 g + r of its own query; O^T (dims x queries) += V^T P^T.
 template <bool DUAL>
-__global__ void __launch_bounds__(256, 3) attn_fwd_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sVT[DH * LP],
       sVdT[DH * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -253,7 +253,7 @@ __global__ void __launch_bounds__(256, 3) attn_fwd_kernel(AttnArgs a) {
 // Lane holds query q0 + lane%16 as in the forward; S^T, dP^T = V dO^T and
 // their tangents per key block, then dQ^T += K^T dS^T.
 template <bool DUAL>
-__global__ void __launch_bounds__(256, 3) attn_bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sV[AB * LP],
       sVd[AB * LP], sKT[DH * LP], sKdT[DH * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
