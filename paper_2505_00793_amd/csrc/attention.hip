@@ -96,17 +96,16 @@ __device__ __forceinline__ bf16x8 pfrag(const bf16_t* lds, int row, int lg, int 
   return x.v;
 }
 
-// Register fragment c in the permuted order from the values of subtiles 2c, 2c+1.
+// Register fragment c in the permuted order from the values of subtiles 2c, 2c+1
+// (round to nearest even; gfx950 converts two values per instruction).
 __device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi) {
-  union {
-    bf16x8 v;
-    uint32_t u[4];
-  } x;
-  x.u[0] = (uint32_t)f2bf(lo[0]) | ((uint32_t)f2bf(lo[1]) << 16);
-  x.u[1] = (uint32_t)f2bf(lo[2]) | ((uint32_t)f2bf(lo[3]) << 16);
-  x.u[2] = (uint32_t)f2bf(hi[0]) | ((uint32_t)f2bf(hi[1]) << 16);
-  x.u[3] = (uint32_t)f2bf(hi[2]) | ((uint32_t)f2bf(hi[3]) << 16);
-  return x.v;
+  bf16x8 v;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[k] = (__bf16)lo[k];
+    v[4 + k] = (__bf16)hi[k];
+  }
+  return v;
 }
 
 // Sum over the four lane groups (lanes with the same lane%16).
