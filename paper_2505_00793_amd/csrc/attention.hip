@@ -55,10 +55,11 @@ __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
 }
 
 // 64 x 64 tile of a row-major bf16 matrix (leading dimension ld) into LDS.
+template <int NT>
 __device__ __forceinline__ void stage(bf16_t* lds, const bf16_t* __restrict__ g, long ld, int tid) {
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int i = tid + 256 * k, r = i >> 3, ch = i & 7;
+  for (int k = 0; k < 512 / NT; ++k) {
+    const int i = tid + NT * k, r = i >> 3, ch = i & 7;
     *reinterpret_cast<uint4*>(lds + sw(r, ch)) =
         *reinterpret_cast<const uint4*>(g + (long)r * ld + ch * 8);
   }
@@ -122,19 +123,21 @@ __device__ __forceinline__ float max_groups(float v) {
 // Wave w owns queries q0 .. q0+15; lane holds query q0 + lane%16.  Per key
 // block: S^T (keys x queries) = K Q^T, so the lane's 16 values are keys
 // 16 n + 4 g + r of its own query; O^T (dims x queries) += V^T P^T.
-template <bool DUAL>
-__global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_fwd_kernel(AttnArgs a) {
+template <bool DUAL, int RB>
+__global__ void __launch_bounds__(RB * 4, RB == 64 ? (DUAL ? 2 : 3) : (DUAL ? 1 : 2))
+    attn_fwd_kernel(AttnArgs a) {
+  constexpr int NT = RB * 4;
   __shared__ __attribute__((aligned(16))) bf16_t sK[AB * LP], sKd[AB * LP], sVT[DH * LP],
       sVdT[DH * LP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int S = a.S, nqb = S / AB;
+  const int S = a.S, nqb = S / RB;
   int blk, bh;
   block_of(nqb, a.BH, blk, bh);
   const int qb = nqb - 1 - blk;  // longest rows first
   const long hb = (long)bh * S * DH, tb = (long)bh * DH * S;
-  const int q0 = qb * AB + w * 16;
-  const int ql = w * 16 + lr;  // the lane's query within the block
+  const int q0 = qb * RB + w * 16;
+  const int qg = q0 + lr;  // the lane's query
   bf16x8 qf[2], qdf[2];
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
@@ -146,13 +149,14 @@ __global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_fwd_kernel(AttnArgs a)
 #pragma unroll
   for (int i = 0; i < 4; ++i) { o[i] = zero4(); o2[i] = zero4(); o3[i] = zero4(); }
   const float sc = a.scale;
-  for (int kb = 0; kb <= qb; ++kb) {
+  const int nkb = (qb + 1) * RB / AB;
+  for (int kb = 0; kb < nkb; ++kb) {
     __syncthreads();
-    stage(sK, a.K + hb + (long)kb * AB * DH, DH, tid);
-    stage(sVT, a.VT + tb + kb * AB, S, tid);
+    stage<NT>(sK, a.K + hb + (long)kb * AB * DH, DH, tid);
+    stage<NT>(sVT, a.VT + tb + kb * AB, S, tid);
     if (DUAL) {
-      stage(sKd, a.Kd + hb + (long)kb * AB * DH, DH, tid);
-      stage(sVdT, a.VdT + tb + kb * AB, S, tid);
+      stage<NT>(sKd, a.Kd + hb + (long)kb * AB * DH, DH, tid);
+      stage<NT>(sVdT, a.VdT + tb + kb * AB, S, tid);
     }
     __syncthreads();
     f32x4 s[4], sd[4];
@@ -169,14 +173,14 @@ __global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_fwd_kernel(AttnArgs a)
         }
       }
     }
-    const bool diag = kb == qb;
+    const bool diag = kb * AB + AB - 1 > qb * RB;  // some key may follow some query
     float mx = -INFINITY;
 #pragma unroll
     for (int n = 0; n < 4; ++n)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float v = s[n][r] * sc;
-        if (diag && n * 16 + 4 * lg + r > ql) v = -INFINITY;
+        if (diag && kb * AB + n * 16 + 4 * lg + r > qg) v = -INFINITY;
         s[n][r] = v;
         mx = fmaxf(mx, v);
       }
@@ -300,13 +304,13 @@ __global__ void __launch_bounds__(256, DUAL ? 2 : 3) attn_bwd_dq_kernel(AttnArgs
   const float sc = a.scale;
   for (int kb = 0; kb <= qb; ++kb) {
     __syncthreads();
-    stage(sK, a.K + hb + (long)kb * AB * DH, DH, tid);
-    stage(sV, a.V + hb + (long)kb * AB * DH, DH, tid);
-    stage(sKT, a.KT + tb + kb * AB, S, tid);
+    stage<256>(sK, a.K + hb + (long)kb * AB * DH, DH, tid);
+    stage<256>(sV, a.V + hb + (long)kb * AB * DH, DH, tid);
+    stage<256>(sKT, a.KT + tb + kb * AB, S, tid);
     if (DUAL) {
-      stage(sKd, a.Kd + hb + (long)kb * AB * DH, DH, tid);
-      stage(sVd, a.Vd + hb + (long)kb * AB * DH, DH, tid);
-      stage(sKdT, a.KdT + tb + kb * AB, S, tid);
+      stage<256>(sKd, a.Kd + hb + (long)kb * AB * DH, DH, tid);
+      stage<256>(sVd, a.Vd + hb + (long)kb * AB * DH, DH, tid);
+      stage<256>(sKdT, a.KdT + tb + kb * AB, S, tid);
     }
     __syncthreads();
     const bool diag = kb == qb;
@@ -398,15 +402,15 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkv_kernel(AttnArgs a) {
   const float sc = a.scale;
   for (int qb = kb; qb < nqb; ++qb) {
     __syncthreads();
-    stage(sQ, a.Q + hb + (long)qb * AB * DH, DH, tid);
-    stage(sG, a.dO + hb + (long)qb * AB * DH, DH, tid);
-    stage(sQT, a.QT + tb + qb * AB, S, tid);
-    stage(sGT, a.dOT + tb + qb * AB, S, tid);
+    stage<256>(sQ, a.Q + hb + (long)qb * AB * DH, DH, tid);
+    stage<256>(sG, a.dO + hb + (long)qb * AB * DH, DH, tid);
+    stage<256>(sQT, a.QT + tb + qb * AB, S, tid);
+    stage<256>(sGT, a.dOT + tb + qb * AB, S, tid);
     if (DUAL) {
-      stage(sQd, a.Qd + hb + (long)qb * AB * DH, DH, tid);
-      stage(sGd, a.dOd + hb + (long)qb * AB * DH, DH, tid);
-      stage(sQdT, a.QdT + tb + qb * AB, S, tid);
-      stage(sGdT, a.dOdT + tb + qb * AB, S, tid);
+      stage<256>(sQd, a.Qd + hb + (long)qb * AB * DH, DH, tid);
+      stage<256>(sGd, a.dOd + hb + (long)qb * AB * DH, DH, tid);
+      stage<256>(sQdT, a.QdT + tb + qb * AB, S, tid);
+      stage<256>(sGdT, a.dOdT + tb + qb * AB, S, tid);
     }
     if (tid < AB) {
       const long i = (long)bh * S + qb * AB + tid;
@@ -502,11 +506,18 @@ bool attn_fused_supported(int S, int dh) { return dh == DH && S >= AB && S % AB 
 
 hipError_t attn_fwd(const AttnArgs& a, hipStream_t s) {
   if (!attn_fused_supported(a.S, a.dh) || a.BH < 1 || a.H < 1 || a.BH % a.H) return hipErrorInvalidValue;
-  const dim3 g(a.S / AB, a.BH);
-  if (a.dual)
-    hipLaunchKernelGGL(attn_fwd_kernel<true>, g, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(attn_fwd_kernel<false>, g, dim3(256), 0, s, a);
+  // The dual forward runs 128-row blocks when it can (each staged tile then
+  // serves eight waves: 512 -> 448 us at S = 8192); every other pass was
+  // measured faster with 64-row blocks.
+  if (a.dual && a.S % 128 == 0) {
+    hipLaunchKernelGGL((attn_fwd_kernel<true, 128>), dim3(a.S / 128, a.BH), dim3(512), 0, s, a);
+  } else {
+    const dim3 g(a.S / AB, a.BH);
+    if (a.dual)
+      hipLaunchKernelGGL((attn_fwd_kernel<true, 64>), g, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<false, 64>), g, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
