@@ -236,6 +236,24 @@ def test_tf_fused_matches_materialised_full_size():
     assert peak < peak_r
 
 
+def test_tf_fused_matches_materialised_S4096():
+    """The long-context workload's model at S = 4096 (2 sequences per batch, T = 2):
+    fused attention against materialised attention, both bf16 (the fused kernels at
+    the lengths the long-context measurement runs; 64 query blocks per head)."""
+    base = W.C4.with_(name="c4_S4096", seq=4096, rows=2, val_rows=2, T=2)
+    inp = W.make_inputs(base, T=2)
+    print("\n[tf fused vs materialised] S=4096 T=2", flush=True)
+    ref, Vr, peak_r = run_meta_tf(base, inp)
+    got, V, peak = run_meta_tf(base.with_(fused_attention=1), inp)
+    errs = group_errors(base, got, ref)
+    print(f"  group errors {['%.2e' % e for e in errs]} V {V:.6f} / {Vr:.6f} "
+          f"peak {peak / 1e9:.2f} / {peak_r / 1e9:.2f} GB", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(base)
+    assert abs(V - Vr) <= 1e-3 * abs(Vr)
+    assert peak < peak_r
+
+
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_tf_meta_grad_long_context(prec):
     """1024-token sequences: causal attention of 1024 x 1024 per head, materialised."""
