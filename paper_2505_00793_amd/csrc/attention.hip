@@ -19,8 +19,9 @@
 // one per key block (dK, dKd, dV, dVd), so every output has one writer and
 // the sums run in a fixed order.
 //
-// Tiles of 64 queries x 64 keys; four waves per workgroup, each owning 16
-// rows (queries, or keys in the dK/dV pass).  Products use
+// Tiles of 64 keys (or queries) staged in LDS; four waves per workgroup, each
+// owning 16 rows (queries, or keys in the dK/dV pass) -- eight waves and 128
+// query rows in the dual forward when S is a multiple of 128.  Products use
 // v_mfma_f32_16x16x32_bf16 in the NT form: C[i][j] += sum_k a_i[k] b_j[k],
 // where a lane holds elements k = 8 (lane/16) + 0..7 of row lane%16 of each
 // operand, and the accumulator holds C[4 (lane/16) + 0..3][lane%16].
@@ -120,9 +121,13 @@ __device__ __forceinline__ float max_groups(float v) {
 }
 
 // ---------------------------------------------------------------- forward
-// Wave w owns queries q0 .. q0+15; lane holds query q0 + lane%16.  Per key
-// block: S^T (keys x queries) = K Q^T, so the lane's 16 values are keys
-// 16 n + 4 g + r of its own query; O^T (dims x queries) += V^T P^T.
+// A workgroup owns RB queries (RB / 16 waves); wave w owns queries q0 .. q0+15
+// and lane holds query q0 + lane%16.  Per key block: S^T (keys x queries) =
+// K Q^T, so the lane's 16 values are keys 16 n + 4 g + r of its own query;
+// O^T (dims x queries) += V^T P^T.  Key blocks run up to the last one that
+// holds a key not after the workgroup's last query; keys after the lane's
+// query are masked (a wave whose queries all precede a block gets p = 0
+// there, its running maximum already finite from block 0).
 template <bool DUAL, int RB>
 __global__ void __launch_bounds__(RB * 4, RB == 64 ? (DUAL ? 2 : 3) : (DUAL ? 1 : 2))
     attn_fwd_kernel(AttnArgs a) {
