@@ -190,6 +190,9 @@ SMALL: Dict[str, Config] = {
     "c4_fused": C4.with_(name="c4_fused", cfg_id=120, d_model=128, n_heads=2, d_ff=256, vocab=97,
                          seq=192, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2,
                          fused_attention=1),
+    "c4_fused128": C4.with_(name="c4_fused128", cfg_id=122, d_model=128, n_heads=2, d_ff=256,
+                            vocab=97, seq=128, rows=3, val_rows=2, n_blocks=2, meta_hidden=16,
+                            T=2, fused_attention=1),
     "c4_long_fused": C4.with_(name="c4_long_fused", cfg_id=121, d_model=128, n_heads=2, d_ff=256,
                               vocab=97, seq=1024, rows=2, val_rows=1, n_blocks=1, meta_hidden=16,
                               T=2, fused_attention=1),
