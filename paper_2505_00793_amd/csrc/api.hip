@@ -798,17 +798,20 @@ void timing_begin(int cls, hipStream_t s) {
   std::lock_guard<std::mutex> g(g_tm);
   if (!g_timing) return;
   g_open = get_event();
-  if (g_open) hipEventRecord(g_open, s);
+  if (g_open && hipEventRecord(g_open, s) != hipSuccess) {  // no record: time nothing
+    g_pool.push_back(g_open);
+    g_open = nullptr;
+  }
 }
 
 void timing_end(int cls, hipStream_t s) {
   std::lock_guard<std::mutex> g(g_tm);
   if (!g_timing || !g_open) return;
   hipEvent_t e = get_event();
-  if (e) {
-    hipEventRecord(e, s);
+  if (e && hipEventRecord(e, s) == hipSuccess) {
     g_recs.push_back(Rec{cls, g_open, e});
   } else {
+    if (e) g_pool.push_back(e);
     g_pool.push_back(g_open);
   }
   g_open = nullptr;
