@@ -125,6 +125,18 @@ void carve_ops(const Lay& y, Carver& c, Ops<T>& o) {
   o.emb = c.take<float>((size_t)y.V * y.d);
 }
 
+// Sorted token positions and their segments for N tokens over a vocabulary of V.
+TokenSegs carve_segs(Carver& c, long N, int V) {
+  const long nsm = embed_segments_max((int)N);
+  TokenSegs t;
+  t.perm = c.take<int>(N);
+  t.seg_start = c.take<int>(nsm + 1);
+  t.seg_tok = c.take<int>(nsm);
+  t.nseg = c.take<int>(1);
+  t.tok2seg = c.take<int>(V);
+  return t;
+}
+
 template <typename T>
 struct Act {  // one inner step at up to maxB sequences (the dynamic memory)
   int *ids, *labels;
@@ -235,11 +247,7 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
   a.dOdh = OPT(BH * hrow); a.dOdhT = OPT(BH * hcol);
   a.lnpart = F32((long)ln_bwd_parts((int)N) * 4 * d);
   const long nsm = embed_segments_max((int)N);
-  a.ts.perm = c.take<int>(N);
-  a.ts.seg_start = c.take<int>(nsm + 1);
-  a.ts.seg_tok = c.take<int>(nsm);
-  a.ts.nseg = c.take<int>(1);
-  a.ts.tok2seg = c.take<int>(y.V);
+  a.ts = carve_segs(c, N, y.V);
   a.epart = F32(nsm * 2 * d);
   a.skws_n = std::max({gemm_splitk_floats(F, d, (int)N), gemm_splitk_floats(d, F, (int)N),
                        gemm_splitk_floats(d, d, (int)N), gemm_splitk_floats(d, 3 * d, (int)N),
@@ -276,6 +284,7 @@ void carve_meta(const Lay& y, Carver& c, Meta& m, long rows, bool vjp) {
 template <typename T>
 struct MetaPlanT {
   std::vector<Ops<T>> slot;
+  std::vector<TokenSegs> segs;  // the training batches' sorted tokens, one per step
   Ops<T> v[2];
   float *run[2], *thetabar;
   Meta meta;
@@ -293,6 +302,8 @@ void plan_meta_t(const Lay& y, int T_, char* base, MetaPlanT<T>& p) {
   p.run[0] = c.take<float>(y.n);
   p.run[1] = c.take<float>(y.n);
   p.thetabar = c.take<float>(y.n);
+  p.segs.resize(T_);
+  for (int t = 0; t < T_; ++t) p.segs[t] = carve_segs(c, (long)y.Bt * y.S, y.V);
   carve_meta(y, c, p.meta, (long)T_ * y.Bt * y.S, true);
   p.st = c.off;
   carve_act(y, c, p.act);
@@ -594,8 +605,11 @@ struct TfEng {
 
   // ------------------------------------------------------------ backward
   // out: operand copies to write from the parameter epilogue (or null).
+  // segs: where the batch's sorted tokens go (null: the step workspace's);
+  // sorted: they are already there (the same batch was sorted by an earlier pass).
   hipError_t backward(const Ops<T>& th, const Ops<T>* v, int Bn, ParamArgs<T> P,
-                      const Ops<T>* out, const Act<T>& a) const {
+                      const Ops<T>* out, const Act<T>& a, const TokenSegs* segs = nullptr,
+                      bool sorted = false) const {
     const bool dual = v != nullptr;
     const int d = y.d, S = y.S, H = y.H, dh = y.dh, F = y.F;
     const int N = Bn * S, BH = Bn * H;
@@ -722,9 +736,10 @@ struct TfEng {
                      out ? out->ln[b][0] : nullptr, out ? out->ln[b][1] : nullptr));
     }
     // embedding rows
-    HC(sort_tokens(a.ids, N, y.V, a.ts, s));
+    const TokenSegs& ts = segs ? *segs : a.ts;
+    if (!(segs && sorted)) HC(sort_tokens(a.ids, N, y.V, ts, s));
     EmbedGradArgs eg;
-    eg.dh = a.dh; eg.dhd = dual ? a.dhd : nullptr; eg.ts = a.ts; eg.part = a.epart;
+    eg.dh = a.dh; eg.dhd = dual ? a.dhd : nullptr; eg.ts = ts; eg.part = a.epart;
     eg.emb_off = y.emb; eg.outE = out ? out->emb : nullptr;
     eg.V = y.V; eg.d = d; eg.N = N;
     return embed_grad<T>(eg, P, s);
@@ -767,7 +782,7 @@ hipError_t run_meta_t(const Lay& y, const float* theta0, const float* eta,
     ParamArgs<T> P = pbase<T>(y, P_UPD_SGD_FIXED, eta);
     P.theta = t == 0 ? theta0 : p.run[(t - 1) & 1];
     P.theta_next = p.run[t & 1];
-    HC(E.backward(p.slot[t], nullptr, y.Bt, P, &p.slot[t + 1], a));
+    HC(E.backward(p.slot[t], nullptr, y.Bt, P, &p.slot[t + 1], a, &p.segs[t], false));
   }
   // outer loss and seed
   {
@@ -788,7 +803,8 @@ hipError_t run_meta_t(const Lay& y, const float* theta0, const float* eta,
     HC(E.head(y.Bt, true, p.meta.u + (long)i * Nt, nullptr, p.meta.ubar + (long)i * Nt, a));
     ParamArgs<T> P = pbase<T>(y, P_REV_SGD_FIXED, eta);
     P.thetabar = p.thetabar;
-    HC(E.backward(p.slot[i], &p.v[vc], y.Bt, P, i > 0 ? &p.v[vc ^ 1] : nullptr, a));
+    HC(E.backward(p.slot[i], &p.v[vc], y.Bt, P, i > 0 ? &p.v[vc ^ 1] : nullptr, a, &p.segs[i],
+                  true));
     vc ^= 1;
   }
   return E.meta_vjp_all(p.meta, d_eta, p.act);
