@@ -675,6 +675,15 @@ hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, i
   return hipGetLastError();
 }
 
+hipError_t transpose_bf16(const bf16_t* a0, const bf16_t* a1, int rows, int cols, int ld,
+                          bf16_t* t0, bf16_t* t1, int ldT, hipStream_t s) {
+  if (rows % 8 || cols % 8 || ld % 8 || ldT % 8) return hipErrorInvalidValue;
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(cdiv(cols, 64), cdiv(rows, 64), a1 ? 2 : 1),
+                     dim3(256), 0, s, a0, a1, rows, cols, ld, t0, t1, ldT);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t convert_matrix(const float* src, int rows, int cols, int lds, T* dst, int ldd,
                           T* dstT, int lddT, hipStream_t s, int batch, long s_src, long s_dst,

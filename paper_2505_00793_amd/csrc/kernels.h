@@ -208,6 +208,10 @@ struct ConvJobs {
   T* dst[CONV_MAX_JOBS] = {};
   T* dstT[CONV_MAX_JOBS] = {};
 };
+// Transposed copies of one or two bf16 matrices (rows, cols and both leading
+// dimensions multiples of 8; a1/t1 may be null).
+hipError_t transpose_bf16(const bf16_t* a0, const bf16_t* a1, int rows, int cols, int ld,
+                          bf16_t* t0, bf16_t* t1, int ldT, hipStream_t s);
 template <typename T>
 hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, int ldd, int lddT,
                             hipStream_t s, int batch = 1, long s_src = 0, long s_dst = 0,

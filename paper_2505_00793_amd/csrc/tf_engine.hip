@@ -401,6 +401,36 @@ struct TfEng {
     return convert_matrices<T>(J, rows, cols, cols, (int)y.ld(cols), (int)y.ld(rows), s, batch, ss,
                                sd, sdT);
   }
+  // With bf16 operands and d a multiple of 256 the LayerNorm kernels write the
+  // bf16 operand rows themselves and a bf16 transpose makes the transposed
+  // copies; otherwise float32 rows are converted to both layouts.
+  bool ln_direct() const { return std::is_same<T, bf16_t>::value && y.d % 256 == 0; }
+  // A LayerNorm's output (and tangent) as operand rows [N][ld(d)] and transposes [d][ld(N)].
+  hipError_t ln_operands(LnArgs ln, T* row, T* rowd, T* tr, T* trd) const {
+    const bool dual = ln.dual;
+    ln.yb = ln.ydb = nullptr;
+    ln.ldb = 0;
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      if (ln_direct()) {
+        ln.yb = row; ln.ydb = dual ? rowd : nullptr; ln.ldb = (int)y.ld(y.d);
+        HC(ln_fwd(ln, s));
+        return transpose_bf16(row, dual ? rowd : nullptr, ln.N, y.d, (int)y.ld(y.d), tr,
+                              dual ? trd : nullptr, (int)y.ld(ln.N), s);
+      }
+    }
+    HC(ln_fwd(ln, s));
+    return convs({{ln.y, row, tr}, {dual ? ln.yd : nullptr, rowd, trd}}, ln.N, y.d);
+  }
+  // The residual-stream gradient dh (and tangent) as operands dhb, dhbT, right
+  // after the LayerNorm backward that produced it.
+  hipError_t dh_operands(int N, bool dual, const Act<T>& a) const {
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      if (ln_direct())
+        return transpose_bf16(a.dhb, dual ? a.dhdb : nullptr, N, y.d, (int)y.ld(y.d), a.dhbT,
+                              dual ? a.dhdbT : nullptr, (int)y.ld(N), s);
+    }
+    return convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, y.d);
+  }
   hipError_t store(const GemmOperands<T>& o, int flags, float* C, float* Cd, int ldc, long sC,
                    float scale, bool dual) const {
     EpiStore e;
@@ -489,9 +519,7 @@ struct TfEng {
       ln.gd = dual ? v->ln[b][0] : nullptr; ln.bd = dual ? v->ln[b][1] : nullptr;
       ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xh1[b]; ln.xhd = a.xhd1[b];
       ln.rstd = a.rs1[b]; ln.c = a.c1[b]; ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
-      HC(ln_fwd(ln, s));
-      HC(convs({{a.y32, a.a1[b], a.a1T[b]}, {dual ? a.yd32 : nullptr, a.a1d[b], a.a1dT[b]}}, N,
-               d));
+      HC(ln_operands(ln, a.a1[b], a.a1d[b], a.a1T[b], a.a1dT[b]));
       // qkv = a1 Wqkv
       HC(store(op(a.a1[b], dual ? a.a1d[b] : nullptr, th.WT[b][0], dual ? v->WT[b][0] : nullptr,
                   (int)y.ld(d), (int)y.ld(d), N, 3 * d, d),
@@ -551,9 +579,7 @@ struct TfEng {
       ln.g = th.ln[b][2]; ln.b = th.ln[b][3];
       ln.gd = dual ? v->ln[b][2] : nullptr; ln.bd = dual ? v->ln[b][3] : nullptr;
       ln.xh = a.xh2[b]; ln.xhd = a.xhd2[b]; ln.rstd = a.rs2[b]; ln.c = a.c2[b];
-      HC(ln_fwd(ln, s));
-      HC(convs({{a.y32, a.a2[b], a.a2T[b]}, {dual ? a.yd32 : nullptr, a.a2d[b], a.a2dT[b]}}, N,
-               d));
+      HC(ln_operands(ln, a.a2[b], a.a2d[b], a.a2T[b], a.a2dT[b]));
       // A1 = GELU(a2 W1)
       {
         EpiActFwd<T> e;
@@ -582,8 +608,7 @@ struct TfEng {
     ln.gd = dual ? v->lnf[0] : nullptr; ln.bd = dual ? v->lnf[1] : nullptr;
     ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xhf; ln.xhd = a.xhdf; ln.rstd = a.rsf; ln.c = a.cf;
     ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
-    HC(ln_fwd(ln, s));
-    HC(convs({{a.y32, a.af, a.afT}, {dual ? a.yd32 : nullptr, a.afd, a.afdT}}, N, d));
+    HC(ln_operands(ln, a.af, a.afd, a.afT, a.afdT));
     HC(store(op(a.af, dual ? a.afd : nullptr, th.UT, dual ? v->UT : nullptr, (int)y.ld(d),
                 (int)y.ld(d), N, y.V, d),
              fl(dual), a.logits, a.logitsd, y.V, 0, 1.0f, dual));
@@ -630,6 +655,13 @@ struct TfEng {
       l.dy = dy; l.dyd = dyd; l.xh = xh; l.xhd = xhd; l.rstd = rs; l.c = c; l.g = g; l.gd = gd;
       l.dh_in = dh_in; l.dhd_in = dhd_in; l.dh_out = a.dh; l.dhd_out = a.dhd;
       l.partial = a.lnpart; l.N = N; l.d = d; l.dual = dual;
+      l.hb = l.hdb = nullptr;
+      l.ldb = 0;
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        if (ln_direct()) {
+          l.hb = a.dhb; l.hdb = dual ? a.dhdb : nullptr; l.ldb = (int)y.ld(d);
+        }
+      }
       return ln_bwd<T>(l, goff, boff, P, og, ob, s);
     };
     // unembedding
@@ -644,7 +676,7 @@ struct TfEng {
                    out ? out->lnf[1] : nullptr));
     for (int b = y.L - 1; b >= 0; --b) {
       // ---- MLP: h_out = h_mid + GELU(a2 W1) W2
-      HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
+      HC(dh_operands(N, dual, a));
       HC(gemm_param<T>(wsk(op(a.A1T[b], dual ? a.A1dT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), F, d, N), a),
                        fl(dual), matP(y.w2[b], F, d, out ? out->W[b][3] : nullptr, out ? out->WT[b][3] : nullptr), s));
@@ -667,7 +699,7 @@ struct TfEng {
                      dual ? v->ln[b][2] : nullptr, a.dh, dual ? a.dhd : nullptr, y.ln2g[b], y.ln2b[b],
                      out ? out->ln[b][2] : nullptr, out ? out->ln[b][3] : nullptr));
       // ---- attention: h_mid = h + Attn(LN1(h)) Wo
-      HC(convs({{a.dh, a.dhb, a.dhbT}, {dual ? a.dhd : nullptr, a.dhdb, a.dhdbT}}, N, d));
+      HC(dh_operands(N, dual, a));
       HC(gemm_param<T>(wsk(op(a.OT[b], dual ? a.OdT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), d, d, N), a),
                        fl(dual), matP(y.wo[b], d, d, out ? out->W[b][1] : nullptr, out ? out->WT[b][1] : nullptr), s));

@@ -19,6 +19,8 @@ struct LnArgs {
   float* y;  float* yd;                      // [N][d] output (and tangent)
   float* xh; float* xhd;                     // normalised input (and tangent), saved
   float* rstd; float* c;                     // [N] 1/sigma and mean(xh xd), saved
+  bf16_t* yb; bf16_t* ydb;                   // if set (d a multiple of 256): y, yd as bf16
+  int ldb;                                   //   rows [N][ldb] instead of the float32 ones
   int N, d, dual;
   float eps;
 };
@@ -31,6 +33,8 @@ struct LnBwdArgs {
   const float* dh_in; const float* dhd_in;   // residual-stream gradient entering
   float* dh_out; float* dhd_out;             // dh_in + dx (may alias dh_in)
   float* partial;                            // [ln_bwd_parts(N)][4][d] column-sum partials
+  bf16_t* hb; bf16_t* hdb;                   // if set (d a multiple of 256): also bf16 rows
+  int ldb;                                   //   [N][ldb] of dh_out, dhd_out
   int N, d, dual;
 };
 

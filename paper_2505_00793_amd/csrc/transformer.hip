@@ -206,11 +206,19 @@ __global__ void __launch_bounds__(256) ln_fwd_vec_kernel(LnArgs a) {
       const int j = 256 * k + 4 * lane;
       const f32x4 g = ldv(a.g + j);
       stv(a.xh + base + j, xv[k]);
-      stv(a.y + base + j, g * xv[k] + ldv(a.b + j));
+      const f32x4 yv = g * xv[k] + ldv(a.b + j);
+      if (a.yb)
+        store4(a.yb + (long)row * a.ldb + j, yv[0], yv[1], yv[2], yv[3]);
+      else
+        stv(a.y + base + j, yv);
       if (a.dual) {
         const f32x4 xhd = rstd * (xdv[k] - md - xv[k] * c);
         stv(a.xhd + base + j, xhd);
-        stv(a.yd + base + j, g * xhd + ldv(a.gd + j) * xv[k] + ldv(a.bd + j));
+        const f32x4 ydv = g * xhd + ldv(a.gd + j) * xv[k] + ldv(a.bd + j);
+        if (a.ydb)
+          store4(a.ydb + (long)row * a.ldb + j, ydv[0], ydv[1], ydv[2], ydv[3]);
+        else
+          stv(a.yd + base + j, ydv);
       }
     }
   if (lane == 0) {
@@ -259,11 +267,15 @@ __global__ void __launch_bounds__(256) ln_bwd_vec_kernel(LnBwdArgs a) {
       const int j = 256 * k + 4 * lane;
       const f32x4 A = q[k] - mq - xh[k] * mxq;
       const f32x4 hin = a.dh_in ? ldv(a.dh_in + base + j) : f32x4{0.f, 0.f, 0.f, 0.f};
-      stv(a.dh_out + base + j, hin + rstd * A);
+      const f32x4 ho = hin + rstd * A;
+      stv(a.dh_out + base + j, ho);
+      if (a.hb) store4(a.hb + (long)row * a.ldb + j, ho[0], ho[1], ho[2], ho[3]);
       if (a.dual) {
         const f32x4 Ad = qd[k] - mqd - xhd[k] * mxq - xh[k] * (mxdq + mxqd);
         const f32x4 hdin = a.dhd_in ? ldv(a.dhd_in + base + j) : f32x4{0.f, 0.f, 0.f, 0.f};
-        stv(a.dhd_out + base + j, hdin + rstdd * A + rstd * Ad);
+        const f32x4 hdo = hdin + rstdd * A + rstd * Ad;
+        stv(a.dhd_out + base + j, hdo);
+        if (a.hdb) store4(a.hdb + (long)row * a.ldb + j, hdo[0], hdo[1], hdo[2], hdo[3]);
       }
     }
 }
@@ -679,6 +691,7 @@ hipError_t gather_rows(const int* ids, int N, int d, const float* E, const float
 }
 
 hipError_t ln_fwd(const LnArgs& a, hipStream_t s) {
+  if ((a.yb || a.ydb) && (a.d % 256 || a.ldb % 4)) return hipErrorInvalidValue;
   if (a.d % 256 == 0)
     hipLaunchKernelGGL(ln_fwd_vec_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
   else
@@ -692,6 +705,7 @@ template <typename T>
 hipError_t ln_bwd(const LnBwdArgs& a, long g_off, long b_off, const ParamArgs<T>& P,
                   float* out_g, float* out_b, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
+  if ((a.hb || a.hdb) && (a.d % 256 || a.ldb % 4)) return hipErrorInvalidValue;
   if (a.d % 256 == 0)
     hipLaunchKernelGGL(ln_bwd_vec_kernel, dim3(cdivl(a.N, 4)), dim3(256), 0, s, a);
   else
