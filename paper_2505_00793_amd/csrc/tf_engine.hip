@@ -401,17 +401,20 @@ struct TfEng {
     return convert_matrices<T>(J, rows, cols, cols, (int)y.ld(cols), (int)y.ld(rows), s, batch, ss,
                                sd, sdT);
   }
-  // With bf16 operands and d a multiple of 256 the LayerNorm kernels write the
-  // bf16 operand rows themselves and a bf16 transpose makes the transposed
-  // copies; otherwise float32 rows are converted to both layouts.
-  bool ln_direct() const { return std::is_same<T, bf16_t>::value && y.d % 256 == 0; }
+  // With bf16 operands, d a multiple of 256 and N (tokens) a multiple of 8 the
+  // LayerNorm kernels write the bf16 operand rows themselves and a bf16
+  // transpose makes the transposed copies; otherwise float32 rows are converted
+  // to both layouts.
+  bool ln_direct(int N) const {
+    return std::is_same<T, bf16_t>::value && y.d % 256 == 0 && N % 8 == 0;
+  }
   // A LayerNorm's output (and tangent) as operand rows [N][ld(d)] and transposes [d][ld(N)].
   hipError_t ln_operands(LnArgs ln, T* row, T* rowd, T* tr, T* trd) const {
     const bool dual = ln.dual;
     ln.yb = ln.ydb = nullptr;
     ln.ldb = 0;
     if constexpr (std::is_same<T, bf16_t>::value) {
-      if (ln_direct()) {
+      if (ln_direct(ln.N)) {
         ln.yb = row; ln.ydb = dual ? rowd : nullptr; ln.ldb = (int)y.ld(y.d);
         HC(ln_fwd(ln, s));
         return transpose_bf16(row, dual ? rowd : nullptr, ln.N, y.d, (int)y.ld(y.d), tr,
@@ -425,7 +428,7 @@ struct TfEng {
   // after the LayerNorm backward that produced it.
   hipError_t dh_operands(int N, bool dual, const Act<T>& a) const {
     if constexpr (std::is_same<T, bf16_t>::value) {
-      if (ln_direct())
+      if (ln_direct(N))
         return transpose_bf16(a.dhb, dual ? a.dhdb : nullptr, N, y.d, (int)y.ld(y.d), a.dhbT,
                               dual ? a.dhdbT : nullptr, (int)y.ld(N), s);
     }
@@ -658,7 +661,7 @@ struct TfEng {
       l.hb = l.hdb = nullptr;
       l.ldb = 0;
       if constexpr (std::is_same<T, bf16_t>::value) {
-        if (ln_direct()) {
+        if (ln_direct(N)) {
           l.hb = a.dhb; l.hdb = dual ? a.dhdb : nullptr; l.ldb = (int)y.ld(d);
         }
       }
@@ -753,10 +756,24 @@ struct TfEng {
       r.Q = a.Qh; r.K = a.Kh; r.V = a.Vh; r.Qd = a.Qdh; r.Kd = a.Kdh; r.Vd = a.Vdh;
       r.qkv_out = a.qkv32; r.qkvd_out = a.qkvd32;
       r.cs = a.cs; r.sn = a.sn; r.N = N; r.S = S; r.H = H; r.dh = dh; r.dual = dual;
+      // dqkv operands in the dZ1 buffers (sized for max(F, 3d)): bf16 rows
+      // straight from the merge and a bf16 transpose, or float32 rows converted
+      bool direct = false;
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        if (N % 8 == 0) {
+          direct = true;
+          r.ob = a.dZ1; r.odb = dual ? a.dZ1d : nullptr; r.ldb = (int)y.ld(3 * d);
+        }
+      }
       HC(rope_merge(r, s));
-      // dqkv operands in the dZ1 buffers (sized for max(F, 3d))
-      HC(convs({{a.qkv32, a.dZ1, a.dZ1T}, {dual ? a.qkvd32 : nullptr, a.dZ1d, a.dZ1dT}}, N,
-               3 * d));
+      if (direct) {
+        if constexpr (std::is_same<T, bf16_t>::value)
+          HC(transpose_bf16(a.dZ1, dual ? a.dZ1d : nullptr, N, 3 * d, (int)y.ld(3 * d), a.dZ1T,
+                            dual ? a.dZ1dT : nullptr, (int)y.ld(N), s));
+      } else {
+        HC(convs({{a.qkv32, a.dZ1, a.dZ1T}, {dual ? a.qkvd32 : nullptr, a.dZ1d, a.dZ1dT}}, N,
+                 3 * d));
+      }
       HC(gemm_param<T>(wsk(op(a.a1T[b], dual ? a.a1dT[b] : nullptr, a.dZ1T, dual ? a.dZ1dT : nullptr,
                           (int)y.ld(N), (int)y.ld(N), d, 3 * d, N), a),
                        fl(dual), matP(y.wqkv[b], d, 3 * d, out ? out->W[b][0] : nullptr, out ? out->WT[b][0] : nullptr), s));

@@ -43,6 +43,7 @@ struct RopeArgs {
   float* Q; float* K; float* V;              // per-head [B*H][S][dh]
   float* Qd; float* Kd; float* Vd;
   float* qkv_out; float* qkvd_out;           // merge: [N][3d] out
+  bf16_t* ob; bf16_t* odb; int ldb;          // merge: if set, bf16 rows [N][ldb] instead
   const float* cs; const float* sn;          // [S][dh/2]
   int N, S, H, dh, dual;
 };

@@ -407,10 +407,21 @@ __global__ void rope_merge_kernel(RopeArgs a) {
     const float* Q = t == 0 ? a.Q : a.Qd;
     const float* K = t == 0 ? a.K : a.Kd;
     const float* Vv = t == 0 ? a.V : a.Vd;
-    float* q = t == 0 ? a.qkv_out : a.qkvd_out;
-    q[dst + h * a.dh + j] = Q[src + j] * cs + sg * Q[src + jp];
-    q[dst + d + h * a.dh + j] = K[src + j] * cs + sg * K[src + jp];
-    q[dst + 2 * d + h * a.dh + j] = Vv[src + j];
+    const float vq = Q[src + j] * cs + sg * Q[src + jp];
+    const float vk = K[src + j] * cs + sg * K[src + jp];
+    const float vv = Vv[src + j];
+    bf16_t* ob = t == 0 ? a.ob : a.odb;
+    if (ob) {
+      const long o = (long)n * a.ldb + h * a.dh + j;
+      ob[o] = f2bf(vq);
+      ob[o + d] = f2bf(vk);
+      ob[o + 2 * d] = f2bf(vv);
+    } else {
+      float* q = t == 0 ? a.qkv_out : a.qkvd_out;
+      q[dst + h * a.dh + j] = vq;
+      q[dst + d + h * a.dh + j] = vk;
+      q[dst + 2 * d + h * a.dh + j] = vv;
+    }
   }
 }
 

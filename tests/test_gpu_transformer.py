@@ -57,6 +57,31 @@ def test_tf_inner_step_full_size(prec):
     check_inner_step(FULL[prec], prec)
 
 
+@pytest.mark.parametrize("name", ["c4_d256", "c4_d256_n12"])
+def test_tf_d256_paths(name):
+    """d = 256, bf16: LayerNorm and RoPE outputs written as bf16 operand rows with bf16
+    transposes (32 tokens), or through float32 and conversions (36 tokens); inner step,
+    H v and the meta-gradient against the oracle's bf16 emulation, and the float32
+    meta-gradient of the same shapes against the float64 oracle."""
+    cfg = W.SMALL[name]
+    c32 = cfg.with_(precision=W.PREC_FP32)
+    inp32 = W.make_inputs(c32)
+    got32, _, _ = run_meta_tf(c32, inp32)
+    ref32, _ = oracle.meta_grad_checkpointed(c32, inp32)
+    e32 = group_errors(c32, got32, ref32)
+    print(f"\n[tf d256] {name} fp32 meta group errors {['%.2e' % e for e in e32]}", flush=True)
+    assert max(e32) <= tol_of(c32)
+    check_inner_step(cfg, "bf16")
+    check_hvp(cfg, "bf16")
+    inp = W.make_inputs(cfg)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=True)
+    errs = group_errors(cfg, got, ref)
+    print(f"  meta group errors {['%.2e' % e for e in errs]} V {V:.6f} ref {Vref:.6f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+
+
 def test_tf_inner_step_fused():
     """Fused attention, primal forward and backward (three 64-query blocks)."""
     check_inner_step(FUSED, "bf16_fused")

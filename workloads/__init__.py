@@ -193,6 +193,13 @@ SMALL: Dict[str, Config] = {
     "c4_fused128": C4.with_(name="c4_fused128", cfg_id=122, d_model=128, n_heads=2, d_ff=256,
                             vocab=97, seq=128, rows=3, val_rows=2, n_blocks=2, meta_hidden=16,
                             T=2, fused_attention=1),
+    # d = 256: the 16-byte LayerNorm kernels writing bf16 operand rows directly
+    # (2 x 16 tokens), and with 3 x 12 tokens (not a multiple of 8) their float32 path
+    "c4_d256": C4.with_(name="c4_d256", cfg_id=123, d_model=256, n_heads=4, d_ff=512, vocab=97,
+                        seq=16, rows=2, val_rows=2, n_blocks=1, meta_hidden=16, T=2),
+    "c4_d256_n12": C4.with_(name="c4_d256_n12", cfg_id=124, d_model=256, n_heads=4, d_ff=512,
+                            vocab=97, seq=12, rows=3, val_rows=2, n_blocks=1, meta_hidden=16,
+                            T=2),
     "c4_long_fused": C4.with_(name="c4_long_fused", cfg_id=121, d_model=128, n_heads=2, d_ff=256,
                               vocab=97, seq=1024, rows=2, val_rows=1, n_blocks=1, meta_hidden=16,
                               T=2, fused_attention=1),
