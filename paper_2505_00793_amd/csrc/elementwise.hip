@@ -141,14 +141,14 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ a0
 // bf16 version for rows, cols and both leading dimensions multiples of 8: a
 // 64 x 64 tile goes in with one 16-byte load per 8 elements and out with one
 // 16-byte store per 8 transposed elements.
-__global__ void __launch_bounds__(256) transpose_bf16_kernel(const bf16_t* __restrict__ a0,
-                                                             const bf16_t* __restrict__ a1,
-                                                             int rows, int cols, int ld,
-                                                             bf16_t* t0, bf16_t* t1, int ldT) {
+// blockIdx.z = job * batch + matrix; matrix k of job j is src[j] + k s_src.
+__global__ void __launch_bounds__(256) transpose_bf16_kernel(TrJobs J, int batch, int rows,
+                                                             int cols, int ld, int ldT,
+                                                             long s_src, long s_dst) {
   __shared__ bf16_t tile[64][64 + 2];
-  const bf16_t* src = blockIdx.z ? a1 : a0;
-  bf16_t* dst = blockIdx.z ? t1 : t0;
-  if (!src || !dst) return;
+  const int job = blockIdx.z / batch, k = blockIdx.z - job * batch;
+  const bf16_t* src = J.src[job] + k * s_src;
+  bf16_t* dst = J.dst[job] + k * s_dst;
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
@@ -675,13 +675,26 @@ hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, i
   return hipGetLastError();
 }
 
+hipError_t transpose_bf16_jobs(const TrJobs& J, int batch, int rows, int cols, int ld, int ldT,
+                               long s_src, long s_dst, hipStream_t s) {
+  if (rows % 8 || cols % 8 || ld % 8 || ldT % 8 || s_src % 8 || s_dst % 8 || batch < 1 ||
+      J.n < 0 || J.n > TR_MAX_JOBS)
+    return hipErrorInvalidValue;
+  for (int j = 0; j < J.n; ++j)
+    if (!J.src[j] || !J.dst[j]) return hipErrorInvalidValue;
+  if (rows <= 0 || cols <= 0 || J.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(cdiv(cols, 64), cdiv(rows, 64), J.n * batch),
+                     dim3(256), 0, s, J, batch, rows, cols, ld, ldT, s_src, s_dst);
+  return hipGetLastError();
+}
+
 hipError_t transpose_bf16(const bf16_t* a0, const bf16_t* a1, int rows, int cols, int ld,
                           bf16_t* t0, bf16_t* t1, int ldT, hipStream_t s) {
-  if (rows % 8 || cols % 8 || ld % 8 || ldT % 8) return hipErrorInvalidValue;
-  if (rows <= 0 || cols <= 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(cdiv(cols, 64), cdiv(rows, 64), a1 ? 2 : 1),
-                     dim3(256), 0, s, a0, a1, rows, cols, ld, t0, t1, ldT);
-  return hipGetLastError();
+  TrJobs J;
+  J.n = a1 ? 2 : 1;
+  J.src[0] = a0; J.dst[0] = t0;
+  J.src[1] = a1; J.dst[1] = t1;
+  return transpose_bf16_jobs(J, 1, rows, cols, ld, ldT, 0, 0, s);
 }
 
 template <typename T>
@@ -720,9 +733,8 @@ hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
   const dim3 tg(cdiv(a.C, 64), cdiv(a.rows, 64), 2);
   if constexpr (sizeof(T) == 2) {
     if (a.rows % 8 == 0 && a.C % 8 == 0 && a.ld % 8 == 0 && a.ldT % 8 == 0) {
-      hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, s, a.d, a.dual ? a.dd : nullptr,
-                         a.rows, a.C, a.ld, a.dT, a.ddT, a.ldT);
-      return hipGetLastError();
+      return transpose_bf16(a.d, a.dual ? a.dd : nullptr, a.rows, a.C, a.ld, a.dT,
+                            a.dual ? a.ddT : nullptr, a.ldT, s);
     }
   }
   hipLaunchKernelGGL(transpose_kernel<T>, tg, dim3(256), 0, s, a.d, a.dual ? a.dd : nullptr,

@@ -208,8 +208,18 @@ struct ConvJobs {
   T* dst[CONV_MAX_JOBS] = {};
   T* dstT[CONV_MAX_JOBS] = {};
 };
-// Transposed copies of one or two bf16 matrices (rows, cols and both leading
-// dimensions multiples of 8; a1/t1 may be null).
+// Transposed copies of bf16 matrices: up to TR_MAX_JOBS of one shape, each a
+// batch of matrices at strides s_src / s_dst (rows, cols, leading dimensions and
+// strides multiples of 8).
+constexpr int TR_MAX_JOBS = 6;
+struct TrJobs {
+  int n = 0;
+  const bf16_t* src[TR_MAX_JOBS];
+  bf16_t* dst[TR_MAX_JOBS];
+};
+hipError_t transpose_bf16_jobs(const TrJobs& J, int batch, int rows, int cols, int ld, int ldT,
+                               long s_src, long s_dst, hipStream_t s);
+// One or two matrices (a1/t1 may be null).
 hipError_t transpose_bf16(const bf16_t* a0, const bf16_t* a1, int rows, int cols, int ld,
                           bf16_t* t0, bf16_t* t1, int ldT, hipStream_t s);
 template <typename T>

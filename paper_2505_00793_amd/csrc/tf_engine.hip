@@ -532,13 +532,35 @@ struct TfEng {
       r.qkv = a.qkv32; r.qkvd = a.qkvd32;
       r.Q = a.Qh; r.K = a.Kh; r.V = a.Vh; r.Qd = a.Qdh; r.Kd = a.Kdh; r.Vd = a.Vdh;
       r.cs = a.cs; r.sn = a.sn; r.N = N; r.S = S; r.H = H; r.dh = dh; r.dual = dual;
+      // per-head operands: bf16 rows straight from the split and batched bf16
+      // transposes (S a multiple of 8), or float32 per-head rows converted
+      bool qdirect = false;
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        if (S % 8 == 0) {
+          qdirect = true;
+          r.Qb = a.Q[b]; r.Kb = a.K[b]; r.Vb = a.Vv[b];
+          if (dual) { r.Qdb = a.Qd[b]; r.Kdb = a.Kd[b]; r.Vdb = a.Vd[b]; }
+        }
+      }
       HC(rope_split(r, s));
       const long sh = (long)S * dh;
-      HC(convs({{a.Qh, a.Q[b], a.QT[b]}, {a.Kh, a.K[b], a.KT[b]}, {a.Vh, a.Vv[b], a.VT[b]},
-                {dual ? a.Qdh : nullptr, a.Qd[b], a.QdT[b]},
-                {dual ? a.Kdh : nullptr, a.Kd[b], a.KdT[b]},
-                {dual ? a.Vdh : nullptr, a.Vd[b], a.VdT[b]}},
-               S, dh, BH, sh, hrow, hcol));
+      if (qdirect) {
+        if constexpr (std::is_same<T, bf16_t>::value) {
+          TrJobs J;
+          auto add = [&](const bf16_t* src, bf16_t* dst) {
+            J.src[J.n] = src; J.dst[J.n] = dst; ++J.n;
+          };
+          add(a.Q[b], a.QT[b]); add(a.K[b], a.KT[b]); add(a.Vv[b], a.VT[b]);
+          if (dual) { add(a.Qd[b], a.QdT[b]); add(a.Kd[b], a.KdT[b]); add(a.Vd[b], a.VdT[b]); }
+          HC(transpose_bf16_jobs(J, BH, S, dh, (int)y.ld(dh), (int)y.ld(S), hrow, hcol, s));
+        }
+      } else {
+        HC(convs({{a.Qh, a.Q[b], a.QT[b]}, {a.Kh, a.K[b], a.KT[b]}, {a.Vh, a.Vv[b], a.VT[b]},
+                  {dual ? a.Qdh : nullptr, a.Qd[b], a.QdT[b]},
+                  {dual ? a.Kdh : nullptr, a.Kd[b], a.KdT[b]},
+                  {dual ? a.Vdh : nullptr, a.Vd[b], a.VdT[b]}},
+                 S, dh, BH, sh, hrow, hcol));
+      }
       if (y.fused) {
         HC(attn_fwd(attn_args(b, Bn, dual, a), s));
       } else {

@@ -42,6 +42,8 @@ struct RopeArgs {
   const float* qkv; const float* qkvd;       // split: [N][3d] in
   float* Q; float* K; float* V;              // per-head [B*H][S][dh]
   float* Qd; float* Kd; float* Vd;
+  bf16_t* Qb; bf16_t* Kb; bf16_t* Vb;        // split: if set, bf16 per-head rows instead
+  bf16_t* Qdb; bf16_t* Kdb; bf16_t* Vdb;
   float* qkv_out; float* qkvd_out;           // merge: [N][3d] out
   bf16_t* ob; bf16_t* odb; int ldb;          // merge: if set, bf16 rows [N][ldb] instead
   const float* cs; const float* sn;          // [S][dh/2]

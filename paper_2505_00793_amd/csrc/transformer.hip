@@ -381,12 +381,19 @@ __global__ void rope_split_kernel(RopeArgs a) {
   const float sg = j < half ? -sn : sn;
   for (int t = 0; t < (a.dual ? 2 : 1); ++t) {
     const float* q = t == 0 ? a.qkv : a.qkvd;
-    float* Q = t == 0 ? a.Q : a.Qd;
-    float* K = t == 0 ? a.K : a.Kd;
-    float* Vv = t == 0 ? a.V : a.Vd;
-    Q[dst] = q[src + h * a.dh + j] * cs + sg * q[src + h * a.dh + jp];
-    K[dst] = q[src + d + h * a.dh + j] * cs + sg * q[src + d + h * a.dh + jp];
-    Vv[dst] = q[src + 2 * d + h * a.dh + j];
+    const float vq = q[src + h * a.dh + j] * cs + sg * q[src + h * a.dh + jp];
+    const float vk = q[src + d + h * a.dh + j] * cs + sg * q[src + d + h * a.dh + jp];
+    const float vv = q[src + 2 * d + h * a.dh + j];
+    bf16_t* Qb = t == 0 ? a.Qb : a.Qdb;
+    if (Qb) {
+      Qb[dst] = f2bf(vq);
+      (t == 0 ? a.Kb : a.Kdb)[dst] = f2bf(vk);
+      (t == 0 ? a.Vb : a.Vdb)[dst] = f2bf(vv);
+    } else {
+      (t == 0 ? a.Q : a.Qd)[dst] = vq;
+      (t == 0 ? a.K : a.Kd)[dst] = vk;
+      (t == 0 ? a.V : a.Vd)[dst] = vv;
+    }
   }
 }
 
