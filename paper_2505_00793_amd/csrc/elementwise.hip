@@ -483,34 +483,41 @@ struct Offsets {
   int off[MFMG_MAX_LAYERS + 1];
 };
 
-__global__ void adam_reduce_kernel(const float* __restrict__ partial, Offsets o, int n_layers,
-                                   int first, float* d_eta) {
-  __shared__ float red[256];
-  float tot_om = 0.0f;
+// Per-layer sums of the adam_vjp_kernel partials, in a fixed order: thread t sums
+// partials t, t + 1024, ... of each layer, waves combine by butterfly, and the 16
+// wave sums of a layer are added in wave order; the weight-decay sums of the
+// layers are then added in layer order.
+__global__ void __launch_bounds__(1024) adam_reduce_kernel(const float* __restrict__ partial,
+                                                           Offsets o, int n_layers, int first,
+                                                           float* d_eta) {
+  __shared__ float red[2][MFMG_MAX_LAYERS][16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int l = 0; l < n_layers; ++l) {
     float s = 0.0f, so = 0.0f;
-    for (int b = o.off[l] + threadIdx.x; b < o.off[l + 1]; b += 256) {
+    for (int b = o.off[l] + threadIdx.x; b < o.off[l + 1]; b += 1024) {
       s += partial[2 * b];
       so += partial[2 * b + 1];
     }
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int k = 128; k > 0; k >>= 1) {
-      if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
-      __syncthreads();
+    s = wave_sum(s);
+    so = wave_sum(so);
+    if (lane == 0) {
+      red[0][l][w] = s;
+      red[1][l][w] = so;
     }
-    if (threadIdx.x == 0) d_eta[l] = (first ? 0.0f : d_eta[l]) + red[0];
-    __syncthreads();
-    red[threadIdx.x] = so;
-    __syncthreads();
-    for (int k = 128; k > 0; k >>= 1) {
-      if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
-      __syncthreads();
-    }
-    tot_om += red[0];
-    __syncthreads();
   }
-  if (threadIdx.x == 0) d_eta[n_layers] = (first ? 0.0f : d_eta[n_layers]) + tot_om;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  float tot_om = 0.0f;
+  for (int l = 0; l < n_layers; ++l) {
+    float s = red[0][l][0], so = red[1][l][0];
+    for (int k = 1; k < 16; ++k) {
+      s += red[0][l][k];
+      so += red[1][l][k];
+    }
+    d_eta[l] = (first ? 0.0f : d_eta[l]) + s;
+    tot_om += so;
+  }
+  d_eta[n_layers] = (first ? 0.0f : d_eta[n_layers]) + tot_om;
 }
 
 // ------------------------------------------------------------------------------------
@@ -762,7 +769,8 @@ hipError_t adam_reduce(const float* partial, const int* block_offsets, int n_lay
                        float* d_eta, hipStream_t s) {
   Offsets o;
   for (int l = 0; l <= n_layers; ++l) o.off[l] = block_offsets[l];
-  hipLaunchKernelGGL(adam_reduce_kernel, dim3(1), dim3(256), 0, s, partial, o, n_layers, first,
+  if (n_layers < 1 || n_layers > MFMG_MAX_LAYERS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adam_reduce_kernel, dim3(1), dim3(1024), 0, s, partial, o, n_layers, first,
                      d_eta);
   return hipGetLastError();
 }
