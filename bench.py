@@ -302,7 +302,10 @@ def bench_config(name: str, args):
         "data": "synthetic (seeded, see workloads/)",
         "config": {"workload": WORKLOADS[name], "name": name, "T": cfg.T,
                    **({"attention": args.attention} if cfg.kind == W.KIND_TRANSFORMER else {})},
-        "peak_bytes": peak, "roofline": None, "cpu_baseline": None, "d_eta_finite": finite}))
+        "peak_bytes": peak, "roofline": None, "cpu_baseline": None, "d_eta_finite": finite,
+        **({"graph_replay": {"ms_per_step": round(args.graph_ms, 4),
+                             "meta_grads_per_s": round(1e3 / args.graph_ms, 4)}}
+           if args.graph_ms else {})}))
 
 
 def bench_toy(args):
@@ -397,6 +400,29 @@ def time_config(cfg: W.Config, args):
     ms = e0.elapsed_time(e1) / args.steps
     tag = f" (M={cfg.map_steps})" if cfg.loss == W.LOSS_MAPMSE else ""
     log(f"[bench] {name}{tag}: {ms:.3f} ms per meta-gradient")
+    args.graph_ms = None
+    if getattr(args, "graph", False):
+        # the same call recorded once in a HIP graph and replayed (no host launch
+        # cost per kernel); replays are bit-identical to eager calls
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            call()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            call()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        args.graph_ms = e0.elapsed_time(e1) / args.steps
+        log(f"[bench] {name}{tag}: {args.graph_ms:.3f} ms per meta-gradient as a graph replay")
     return ms, peak, bool(torch.isfinite(d_eta).all().item())
 
 
@@ -422,6 +448,8 @@ def main():
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
     ap.add_argument("--attention", default="fused", choices=["fused", "materialised"],
                     help="attention form of the transformer workloads")
+    ap.add_argument("--graph", action="store_true",
+                    help="other workloads: also time graph replays of the same call")
     ap.add_argument("--seq", type=int, default=0, choices=[0, *W.C4_LONG_S],
                     help="c4_long_context: time this sequence length and --attention form only")
     args = ap.parse_args()
