@@ -149,10 +149,11 @@ def test_tf_hvp_matches_reverse_over_forward():
     assert max(e) <= tol_of(cfg)
 
 
-@pytest.mark.parametrize("name", ["c4_fused", "c4_fused128"])
+@pytest.mark.parametrize("name", ["c4_fused", "c4_fused128", "c4_fused64"])
 def test_tf_hvp_fused(name):
     """Fused attention, dual forward and backward: H v and the mixed product
-    (S = 192: 64-row blocks throughout; S = 128: the 128-row dual forward)."""
+    (S = 192: 64-row blocks throughout; S = 128: the 128-row dual forward; S = 64: one
+    diagonal tile per head)."""
     check_hvp(W.SMALL[name], "bf16_fused")
 
 
@@ -229,7 +230,7 @@ def test_tf_meta_grad_mid_bf16():
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
 
 
-@pytest.mark.parametrize("name", ["c4_fused", "c4_fused128", "c4_long_fused"])
+@pytest.mark.parametrize("name", ["c4_fused", "c4_fused128", "c4_fused64", "c4_long_fused"])
 def test_tf_meta_grad_fused(name):
     """Fused attention through the whole meta-gradient (192- and 1024-token
     sequences, head dim 64) against the oracle's bf16 emulation."""

@@ -190,6 +190,9 @@ SMALL: Dict[str, Config] = {
     "c4_fused": C4.with_(name="c4_fused", cfg_id=120, d_model=128, n_heads=2, d_ff=256, vocab=97,
                          seq=192, rows=3, val_rows=2, n_blocks=2, meta_hidden=16, T=2,
                          fused_attention=1),
+    "c4_fused64": C4.with_(name="c4_fused64", cfg_id=125, d_model=128, n_heads=2, d_ff=256,
+                           vocab=97, seq=64, rows=4, val_rows=2, n_blocks=2, meta_hidden=16,
+                           T=2, fused_attention=1),
     "c4_fused128": C4.with_(name="c4_fused128", cfg_id=122, d_model=128, n_heads=2, d_ff=256,
                             vocab=97, seq=128, rows=3, val_rows=2, n_blocks=2, meta_hidden=16,
                             T=2, fused_attention=1),
