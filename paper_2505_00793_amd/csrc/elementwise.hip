@@ -141,14 +141,14 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ a0
 // bf16 version for rows, cols and both leading dimensions multiples of 8: a
 // 64 x 64 tile goes in with one 16-byte load per 8 elements and out with one
 // 16-byte store per 8 transposed elements.
-// blockIdx.z = job * batch + matrix; matrix k of job j is src[j] + k s_src.
+// blockIdx.z = job * batch + matrix; matrix m of job j is src[j] + m s_src.
 __global__ void __launch_bounds__(256) transpose_bf16_kernel(TrJobs J, int batch, int rows,
                                                              int cols, int ld, int ldT,
                                                              long s_src, long s_dst) {
   __shared__ bf16_t tile[64][64 + 2];
-  const int job = blockIdx.z / batch, k = blockIdx.z - job * batch;
-  const bf16_t* src = J.src[job] + k * s_src;
-  bf16_t* dst = J.dst[job] + k * s_dst;
+  const int job = blockIdx.z / batch, m = blockIdx.z - job * batch;
+  const bf16_t* src = J.src[job] + m * s_src;
+  bf16_t* dst = J.dst[job] + m * s_dst;
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
