@@ -175,9 +175,11 @@ struct MetaPlan {
   size_t static_bytes, dynamic_bytes, total;
 };
 
+// Blocks of the Adam reverse kernel for layer l: 16 x 64 tiles of W, then 256
+// bias entries per block (the kernel's launcher checks the count against this).
 int adam_blocks(const mfmg_problem* p, int l) {
-  const long n = (long)p->w[l] * p->w[l + 1] + (p->d.has_bias ? p->w[l + 1] : 0);
-  return (int)((n + 255) / 256);
+  const long tiles = (long)((p->w[l] + 15) / 16) * ((p->w[l + 1] + 63) / 64);
+  return (int)(tiles + (p->d.has_bias ? (p->w[l + 1] + 255) / 256 : 0));
 }
 
 // Segment length of the recomputed checkpoints for T inner steps (0: every
@@ -633,7 +635,7 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
         A.ldW = (int)p->ld(A.nout);
         A.ldWT = (int)p->ld(A.nin);
         A.partial = mp.partial + 2 * (size_t)mp.part_off[l];
-        int used = 0;
+        int used = mp.part_off[l + 1] - mp.part_off[l];  // capacity in, blocks used out
         TimingScope ts(7, s);
         HIPCHK(adam_vjp<T>(A, &used, s));
       }

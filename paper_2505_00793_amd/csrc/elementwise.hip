@@ -425,55 +425,83 @@ __global__ void __launch_bounds__(256) loss_reduce_kernel(const float* __restric
 //   d eta_l  += sum_layer -lr tb (u + omega theta)    (d lr / d eta_l = lr)
 //   d omega  += sum_all   -lr tb theta
 // ------------------------------------------------------------------------------------
+// Blocks 0 .. tiles-1 take 16 x 64 tiles of W (coalesced reads of every stream,
+// coalesced row-major tangent, the transposed tangent through an LDS tile in
+// 32-byte runs); the remaining blocks take 256 bias entries each.  Each block
+// writes the sums of its entries' eta and omega terms (fixed order) to
+// partial[2 block ..].
+template <typename T>
+__device__ __forceinline__ void adam_vjp_elem(const AdamVjpArgs<T>& a, long idx, float& vg,
+                                              float& pe, float& po) {
+  const float g = a.g[idx], m = a.m[idx], v = a.v[idx], th = a.theta[idx];
+  const float m1 = a.b1 * m + (1.0f - a.b1) * g;
+  const float v1 = a.b2 * v + (1.0f - a.b2) * g * g;
+  const float s = sqrtf(v1 / a.k2);
+  const float D = s + a.eps;
+  const float mh = m1 / a.k1;
+  const float u = mh / D;
+  const float lam = expf(a.eta[a.layer]);
+  const float om = a.eta[a.n_layers];
+  const float tb = a.thetabar[idx];
+  const float ub = -lam * tb;
+  const float mb = (a.first ? 0.0f : a.mbar[idx]) + ub / (a.k1 * D);
+  const float vbt = (a.first ? 0.0f : a.vbar[idx]) +
+                    (v1 > 0.0f ? -ub * mh / (D * D) / (2.0f * s * a.k2) : 0.0f);
+  vg = (1.0f - a.b1) * mb + 2.0f * (1.0f - a.b2) * g * vbt;
+  a.mbar[idx] = a.b1 * mb;
+  a.vbar[idx] = a.b2 * vbt;
+  a.thetabar[idx] = tb * (1.0f - lam * om);
+  pe += -lam * tb * (u + om * th);
+  po += -lam * tb * th;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpArgs<T> a, float* partial) {
+  __shared__ float tile[16][65];
   __shared__ float red0[256], red1[256];
-  const long nW = (long)a.nin * a.nout;
-  const long ntot = nW + (a.b_off >= 0 ? a.nout : 0);
-  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  const int tiles_n = (a.nout + 63) / 64;
+  const int tiles = ((a.nin + 15) / 16) * tiles_n;
+  const int tid = threadIdx.x;
   float pe = 0.0f, po = 0.0f;
-  if (e < ntot) {
-    const bool isb = e >= nW;
-    const long idx = isb ? a.b_off + (e - nW) : a.w_off + e;
-    const float g = a.g[idx], m = a.m[idx], v = a.v[idx], th = a.theta[idx];
-    const float m1 = a.b1 * m + (1.0f - a.b1) * g;
-    const float v1 = a.b2 * v + (1.0f - a.b2) * g * g;
-    const float s = sqrtf(v1 / a.k2);
-    const float D = s + a.eps;
-    const float mh = m1 / a.k1;
-    const float u = mh / D;
-    const float lam = expf(a.eta[a.layer]);
-    const float om = a.eta[a.n_layers];
-    const float tb = a.thetabar[idx];
-    const float ub = -lam * tb;
-    const float mb = (a.first ? 0.0f : a.mbar[idx]) + ub / (a.k1 * D);
-    const float vbt = (a.first ? 0.0f : a.vbar[idx]) +
-                      (v1 > 0.0f ? -ub * mh / (D * D) / (2.0f * s * a.k2) : 0.0f);
-    const float vg = (1.0f - a.b1) * mb + 2.0f * (1.0f - a.b2) * g * vbt;
-    a.mbar[idx] = a.b1 * mb;
-    a.vbar[idx] = a.b2 * vbt;
-    a.thetabar[idx] = tb * (1.0f - lam * om);
-    pe = -lam * tb * (u + om * th);
-    po = -lam * tb * th;
-    if (isb) {
-      a.vb[e - nW] = vg;
-    } else {
-      const long mm = e / a.nout, nn = e % a.nout;
-      a.vW[mm * a.ldW + nn] = Elem<T>::from_float(vg);
-      a.vWT[nn * a.ldWT + mm] = Elem<T>::from_float(vg);
+  if ((int)blockIdx.x < tiles) {
+    const int r0 = (blockIdx.x / tiles_n) * 16, c0 = (blockIdx.x % tiles_n) * 64;
+    const int tx = tid & 63, ty = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = ty + 4 * i, mm = r0 + r, nn = c0 + tx;
+      float vg = 0.0f;
+      if (mm < a.nin && nn < a.nout) {
+        adam_vjp_elem(a, a.w_off + (long)mm * a.nout + nn, vg, pe, po);
+        a.vW[(long)mm * a.ldW + nn] = Elem<T>::from_float(vg);
+      }
+      tile[r][tx] = vg;
+    }
+    __syncthreads();
+    const int rr = tid & 15;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = (tid >> 4) + 16 * j, nn = c0 + c, mm = r0 + rr;
+      if (nn < a.nout && mm < a.nin) a.vWT[(long)nn * a.ldWT + mm] = Elem<T>::from_float(tile[rr][c]);
+    }
+  } else {
+    const long e = (long)(blockIdx.x - tiles) * 256 + tid;
+    if (a.b_off >= 0 && e < a.nout) {
+      float vg = 0.0f;
+      adam_vjp_elem(a, a.b_off + e, vg, pe, po);
+      a.vb[e] = vg;
     }
   }
-  red0[threadIdx.x] = pe;
-  red1[threadIdx.x] = po;
+  red0[tid] = pe;
+  red1[tid] = po;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {
-    if ((int)threadIdx.x < o) {
-      red0[threadIdx.x] += red0[threadIdx.x + o];
-      red1[threadIdx.x] += red1[threadIdx.x + o];
+    if (tid < o) {
+      red0[tid] += red0[tid + o];
+      red1[tid] += red1[tid + o];
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     partial[2 * blockIdx.x] = red0[0];
     partial[2 * blockIdx.x + 1] = red1[0];
   }
@@ -757,11 +785,13 @@ hipError_t loss_reduce(const float* loss_rows, const float* alpha_logits, int ro
 }
 
 template <typename T>
-hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks_used, hipStream_t s) {
-  const long ntot = (long)a.nin * a.nout + (a.b_off >= 0 ? a.nout : 0);
-  const int blocks = cdiv(ntot, 256);
-  *blocks_used = blocks;
-  hipLaunchKernelGGL(adam_vjp_kernel<T>, dim3(blocks), dim3(256), 0, s, a, a.partial);
+// *blocks: in, how many blocks the partial buffer holds; out, how many were used
+// (16 x 64 tiles of W, then 256 bias entries per block).
+hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks, hipStream_t s) {
+  const long nb = (long)cdiv(a.nin, 16) * cdiv(a.nout, 64) + (a.b_off >= 0 ? cdiv(a.nout, 256) : 0);
+  if (nb > *blocks) return hipErrorInvalidValue;
+  *blocks = (int)nb;
+  hipLaunchKernelGGL(adam_vjp_kernel<T>, dim3(nb), dim3(256), 0, s, a, a.partial);
   return hipGetLastError();
 }
 
