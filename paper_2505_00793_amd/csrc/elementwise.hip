@@ -712,8 +712,10 @@ hipError_t convert_matrices(const ConvJobs<T>& J, int rows, int cols, int lds, i
 
 hipError_t transpose_bf16_jobs(const TrJobs& J, int batch, int rows, int cols, int ld, int ldT,
                                long s_src, long s_dst, hipStream_t s) {
-  if (rows % 8 || cols % 8 || ld % 8 || ldT % 8 || s_src % 8 || s_dst % 8 || batch < 1 ||
-      J.n < 0 || J.n > TR_MAX_JOBS)
+  // Source rows are read in 16-byte chunks up to the next multiple of 8 columns
+  // (padding, present when ld >= that); transposed rows past cols are not written.
+  if (rows % 8 || ld % 8 || ldT % 8 || s_src % 8 || s_dst % 8 || ld < (cols + 7) / 8 * 8 ||
+      batch < 1 || J.n < 0 || J.n > TR_MAX_JOBS)
     return hipErrorInvalidValue;
   for (int j = 0; j < J.n; ++j)
     if (!J.src[j] || !J.dst[j]) return hipErrorInvalidValue;
@@ -767,7 +769,7 @@ hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
   // transposed copies of dL/dz (and its tangent), coalesced through LDS
   const dim3 tg(cdiv(a.C, 64), cdiv(a.rows, 64), 2);
   if constexpr (sizeof(T) == 2) {
-    if (a.rows % 8 == 0 && a.C % 8 == 0 && a.ld % 8 == 0 && a.ldT % 8 == 0) {
+    if (a.rows % 8 == 0 && a.ld % 8 == 0 && a.ld >= (a.C + 7) / 8 * 8 && a.ldT % 8 == 0) {
       return transpose_bf16(a.d, a.dual ? a.dd : nullptr, a.rows, a.C, a.ld, a.dT,
                             a.dual ? a.ddT : nullptr, a.ldT, s);
     }
