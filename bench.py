@@ -309,7 +309,7 @@ def bench_config(name: str, args):
 
 
 def bench_toy(args):
-    """The motivating example of Section 3.3 (B = 1024, D = 4096, T = 2, MAML) over
+    """The motivating example of Section 3.2 (B = 1024, D = 4096, T = 2, MAML) over
     the number of map steps M: time and peak device bytes per meta-gradient.
     The map's derivatives are carried in registers, so memory does not grow with
     M.  The map's derivative grows roughly like M!, so in float32 the meta-gradient

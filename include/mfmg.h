@@ -56,19 +56,43 @@
  *                                  unweighted loss.  dV/deta = bar theta_0;
  *                                  mfmg_meta_grad ignores its theta0 argument
  *                                  (which may be null).  MLP kind only.
+ *  Transformer (MFMG_KIND_TRANSFORMER; d = d_model, F = d_ff, V = vocab; every
+ *  matrix row-major [in][out], applied as x W): the token embedding E [V][d];
+ *  then for each block b = 0..n_blocks-1: ln1 gain [d], ln1 bias [d],
+ *  W_qkv [d][3d] (output columns q | k | v, head h owning columns h*d/H ..
+ *  (h+1)*d/H - 1 of each), W_o [d][d], ln2 gain [d], ln2 bias [d], W_1 [d][F],
+ *  W_2 [F][d]; then the final LayerNorm gain [d] and bias [d] and the
+ *  unembedding U [d][V].  No linear biases.  Each block is pre-LayerNorm:
+ *  h += Attn(LN1(h)) W_o, h += GELU(LN2(h) W_1) W_2, with causal softmax
+ *  attention scaled by 1/sqrt(d/H) and rotary position embeddings on q and k
+ *  (rotate-half pairing of head dims j and j + d/(2H), angle pos *
+ *  rope_base^(-2j/(d/H))); GELU is the exact erf form; logits = LNf(h) U.
+ *   MFMG_META_TOKEN_WEIGHT_MLP (transformer only): eta = [W1 [d][meta_hidden] |
+ *                                  b1 [meta_hidden] | w2 [meta_hidden] | b2],
+ *                                  d*meta_hidden + 2*meta_hidden + 1 floats.
+ *                                  Token (b, s) of inner step t has loss weight
+ *                                  sigmoid(tanh(e W1 + b1) . w2 + b2), where e is
+ *                                  row tokens[b][s] of the embedding E of the
+ *                                  theta_0 passed in, held constant (for the
+ *                                  single-step calls: of the theta passed in).
  *  The inner loss is L = (1/N) sum_n alpha_n l_n over the N rows of a batch,
  *  alpha_n = 1 unless the loss is weighted; the outer loss V is the unweighted
  *  mean over the validation rows.  l_n is softmax cross-entropy (CE) or the
  *  squared error sum_j (z_nj - y_nj)^2 (MSE), or for MAPMSE the mean over the
  *  outputs j of (y_M,nj - y_nj)^2, where y_0 = z and y_i = i (2 + sin y_{i-1})^
- *  cos(y_{i-1}) elementwise for i = 1..M (the map of Section 3.3, eq.
+ *  cos(y_{i-1}) elementwise for i = 1..M (the map of Section 3.2, eq.
  *  motivational_example; with one D x D layer and MAML this is the paper's
  *  motivating example).  MAPMSE targets are float32 like MSE ones.
  *
  * Batches (mfmg_batch)
  * --------------------
- *  x (dev) float32 [rows][widths[0]] row-major; y (dev) int32 class labels
- *  [rows] for CE or float32 targets [rows][widths[n_layers]] for MSE.
+ *  MLP: x (dev) float32 [rows][widths[0]] row-major; y (dev) int32 class
+ *  labels [rows] for CE or float32 targets [rows][widths[n_layers]] for MSE
+ *  and MAPMSE.
+ *  Transformer: x (dev) int32 tokens [rows][seq + 1] row-major, ids in
+ *  [0, vocab); sequence b predicts tokens[b][1..seq] from tokens[b][0..seq-1],
+ *  so a batch has N = rows * seq loss rows (the mvp_out rows of
+ *  mfmg_hvp_fwd_over_rev are ordered b * seq + s).  y is unused (may be NULL).
  */
 #ifndef MFMG_H_
 #define MFMG_H_
@@ -85,7 +109,8 @@ typedef enum {
   MFMG_ERR_INVALID_ARGUMENT = 1, /* a null/misaligned pointer, a bad size or shape */
   MFMG_ERR_UNSUPPORTED = 2,      /* a valid combination this build does not implement */
   MFMG_ERR_WORKSPACE = 3,        /* ws_bytes smaller than mfmg_query_sizes reports */
-  MFMG_ERR_HIP = 4               /* a HIP runtime call failed while enqueueing */
+  MFMG_ERR_HIP = 4,              /* a HIP runtime call failed while enqueueing */
+  MFMG_ERR_NUMERIC = 5           /* mfmg_check_finite found a NaN or an infinity */
 } mfmg_status;
 
 enum { MFMG_KIND_MLP = 0, MFMG_KIND_TRANSFORMER = 1 };
@@ -121,7 +146,13 @@ typedef struct {
   int val_rows;                        /* rows of the validation batch */
   float sgd_lr;                        /* fixed inner learning rate (weighted-loss metas) */
   float adam_b1, adam_b2, adam_eps;    /* Adam constants */
-  /* transformer fields (reserved) */
+  /* Transformer kind only (see "Parameter layout"): model width, heads,
+   * feed-forward width, vocabulary, tokens per sequence, blocks, width of the
+   * token-weight meta-model's hidden layer, LayerNorm epsilon, RoPE base.
+   * Supported: d_model, d_ff and d_model / n_heads multiples of 8, d_model <=
+   * 1024; seq a multiple of 4; rows * seq and val_rows * seq <= 8192 tokens;
+   * meta_hidden a multiple of 8 in [8, 256]; SGD with the fixed rate sgd_lr,
+   * cross-entropy, MFMG_META_TOKEN_WEIGHT_MLP. */
   int d_model, n_heads, d_ff, vocab, seq, n_blocks, meta_hidden;
   float ln_eps, rope_base;
   int map_steps;                       /* MFMG_LOSS_MAPMSE: M, 1..1024 */
@@ -226,6 +257,17 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t problem, const float* theta0, const fl
                            const float* eta, const mfmg_batch* train_batches, int T,
                            const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
                            size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Non-finite check of a result, e.g. d_eta_out of mfmg_meta_grad (whose
+ * calls never inspect their outputs: that would need a host synchronisation
+ * inside the call).  Counts the NaN and infinite entries of x (dev, n floats)
+ * into the caller's workspace ws (dev, >= 256 bytes, 256-byte aligned), copies
+ * the count to the host and waits for `stream`: unlike every other entry point
+ * this one synchronises.  count_out (host, nullable) receives the count.
+ * Returns MFMG_ERR_NUMERIC when the count is not zero, MFMG_ERR_HIP when the
+ * stream reports an error (including one left by earlier work on it). */
+mfmg_status mfmg_check_finite(const float* x, size_t n, size_t* count_out, void* ws,
+                              size_t ws_bytes, void* stream);
 
 /* Static string naming a status. */
 const char* mfmg_status_string(mfmg_status status);

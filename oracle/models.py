@@ -59,7 +59,7 @@ def per_example_loss(cfg: Config, out: torch.Tensor, y: torch.Tensor) -> torch.T
 
 
 def toy_map(y: torch.Tensor, M: int) -> torch.Tensor:
-    """The M-step recursive map of Section 3.3 (eq. motivational_example),
+    """The M-step recursive map of Section 3.2 (eq. motivational_example),
     elementwise: y_i = i * (2 + sin y_{i-1}) ** cos y_{i-1}, i = 1..M."""
     for i in range(1, M + 1):
         y = i * (2.0 + torch.sin(y)) ** torch.cos(y)

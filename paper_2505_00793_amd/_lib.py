@@ -15,12 +15,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmfmg.so")
 
 MAX_LAYERS = 16
-OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_NUMERIC = 0, 1, 2, 3, 4, 5
 
 EXPORTED = [
     "mfmg_problem_create", "mfmg_problem_destroy", "mfmg_query_sizes", "mfmg_inner_step",
     "mfmg_hvp_fwd_over_rev", "mfmg_meta_grad", "mfmg_status_string", "mfmg_last_error_message",
-    "mfmg_timing_enable", "mfmg_timing_read",
+    "mfmg_timing_enable", "mfmg_timing_read", "mfmg_check_finite",
 ]
 
 
@@ -78,6 +78,8 @@ def lib() -> ctypes.CDLL:
     L.mfmg_meta_grad.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, P(mfmg_batch), c_int,
                                  P(mfmg_batch), c_void_p, c_void_p, P(c_size_t), c_void_p,
                                  c_size_t, c_void_p]
+    L.mfmg_check_finite.argtypes = [c_void_p, c_size_t, P(c_size_t), c_void_p, c_size_t,
+                                    c_void_p]
     L.mfmg_status_string.argtypes = [c_int]
     L.mfmg_status_string.restype = c_char_p
     L.mfmg_last_error_message.argtypes = []
@@ -86,7 +88,7 @@ def lib() -> ctypes.CDLL:
     L.mfmg_timing_read.argtypes = [c_int, P(c_int), P(c_double)]
     for name in ("mfmg_problem_create", "mfmg_query_sizes", "mfmg_inner_step",
                  "mfmg_hvp_fwd_over_rev", "mfmg_meta_grad", "mfmg_timing_enable",
-                 "mfmg_timing_read"):
+                 "mfmg_timing_read", "mfmg_check_finite"):
         getattr(L, name).restype = c_int
     _lib = L
     return L
@@ -100,6 +102,11 @@ def check(status: int) -> None:
 
 def _ptr(t):
     return None if t is None else c_void_p(t.data_ptr())
+
+
+def _batch(x, y):
+    """mfmg_batch of a CUDA tensor x (rows = its first dimension) and y (None: NULL)."""
+    return mfmg_batch(x.data_ptr(), None if y is None else y.data_ptr(), x.shape[0])
 
 
 def _stream():
@@ -154,7 +161,7 @@ class Problem:
 
     def mfmg_inner_step(self, theta, opt_state, eta, x, y, step_index, theta_next,
                         opt_state_next=None, grad_out=None, loss_out=None, ws=None):
-        b = mfmg_batch(x.data_ptr(), y.data_ptr(), x.shape[0])
+        b = _batch(x, y)
         if ws is None:
             ws = self.workspace(self.mfmg_query_sizes(1).step_workspace_bytes, theta.device)
         check(lib().mfmg_inner_step(self._h, _ptr(theta), _ptr(opt_state), _ptr(eta),
@@ -164,7 +171,7 @@ class Problem:
 
     def mfmg_hvp_fwd_over_rev(self, theta, eta, x, y, step_index, v, grad_out, hvp_out,
                               mvp_out=None, ws=None):
-        b = mfmg_batch(x.data_ptr(), y.data_ptr(), x.shape[0])
+        b = _batch(x, y)
         if ws is None:
             ws = self.workspace(self.mfmg_query_sizes(1).step_workspace_bytes, theta.device)
         check(lib().mfmg_hvp_fwd_over_rev(self._h, _ptr(theta), _ptr(eta), ctypes.byref(b),
@@ -175,9 +182,8 @@ class Problem:
                        val_loss_out=None, ws=None) -> int:
         """Returns peak bytes."""
         T = len(xs)
-        arr = (mfmg_batch * T)(*[mfmg_batch(x.data_ptr(), y.data_ptr(), x.shape[0])
-                                 for x, y in zip(xs, ys)])
-        vb = mfmg_batch(vx.data_ptr(), vy.data_ptr(), vx.shape[0])
+        arr = (mfmg_batch * T)(*[_batch(x, y) for x, y in zip(xs, ys)])
+        vb = _batch(vx, vy)
         if ws is None:
             ws = self.workspace(self.mfmg_query_sizes(T).workspace_bytes, theta0.device)
         peak = c_size_t(0)
@@ -185,6 +191,18 @@ class Problem:
                                    ctypes.byref(vb), _ptr(d_eta_out), _ptr(val_loss_out),
                                    ctypes.byref(peak), _ptr(ws), ws.numel(), _stream()))
         return peak.value
+
+
+def mfmg_check_finite(x, ws=None) -> int:
+    """Number of NaN / infinite entries of the float32 CUDA tensor x (synchronises the
+    current stream); raises MfmgError (status ERR_NUMERIC) when it is not zero."""
+    import torch
+    if ws is None:
+        ws = torch.empty(256, dtype=torch.uint8, device=x.device)
+    n = c_size_t(0)
+    check(lib().mfmg_check_finite(_ptr(x), x.numel(), ctypes.byref(n), _ptr(ws), ws.numel(),
+                                  _stream()))
+    return n.value
 
 
 def mfmg_timing_enable(enable: bool) -> None:

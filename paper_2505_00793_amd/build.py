@@ -1,6 +1,7 @@
 """Build libmfmg.so (HIP, gfx950) in-tree with hipcc.
 
-    python -m paper_2505_00793_amd.build          # rebuild everything
+    python -m paper_2505_00793_amd.build                 # rebuild everything
+    python -m paper_2505_00793_amd.build api.hip ...     # recompile these, relink
 """
 from __future__ import annotations
 
@@ -34,11 +35,16 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
-    """Compile every source and link the shared library; returns its path."""
+def build(verbose: bool = True, only=None) -> str:
+    """Compile every source (or only the named ones, reusing the other objects)
+    and link the shared library; returns its path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
+    todo = SOURCES if not only else [s for s in SOURCES if s in only]
+    if only and len(todo) != len(set(only)):
+        raise ValueError(f"unknown sources in {only}; sources are {SOURCES}")
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        list(ex.map(_compile, todo))
+    objs = [os.path.join(BUILD_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -51,4 +57,4 @@ def build(verbose: bool = True) -> str:
 
 
 if __name__ == "__main__":
-    build()
+    build(only=sys.argv[1:] or None)

@@ -832,6 +832,7 @@ const char* mfmg_status_string(mfmg_status s) {
     case MFMG_ERR_UNSUPPORTED: return "MFMG_ERR_UNSUPPORTED";
     case MFMG_ERR_WORKSPACE: return "MFMG_ERR_WORKSPACE";
     case MFMG_ERR_HIP: return "MFMG_ERR_HIP";
+    case MFMG_ERR_NUMERIC: return "MFMG_ERR_NUMERIC";
   }
   return "MFMG_UNKNOWN_STATUS";
 }
@@ -1020,10 +1021,15 @@ mfmg_status mfmg_hvp_fwd_over_rev(mfmg_problem_t p, const float* theta, const fl
                         (char*)ws, s);
 }
 
-mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* opt_state0,
-                           const float* eta, const mfmg_batch* train_batches, int T,
-                           const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
-                           size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks of mfmg_meta_grad's arguments (all but the workspace);
+// *need = the workspace bytes the call uses.
+mfmg_status check_meta_args(mfmg_problem_t p, const float* theta0, const float* opt_state0,
+                            const float* eta, const mfmg_batch* train_batches, int T,
+                            const mfmg_batch* val_batch, const float* d_eta_out, size_t* need) {
   if (!p) return fail(MFMG_ERR_INVALID_ARGUMENT, "null problem");
   if (T < 1) return fail(MFMG_ERR_INVALID_ARGUMENT, "T = %d, must be >= 1", T);
   if ((!theta0 && p->d.meta != MFMG_META_MAML) || !eta || !d_eta_out)
@@ -1033,8 +1039,15 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
   TRY(check_batch(p, val_batch, p->d.val_rows, "val_batch", 0));
   TRY(check_align16({theta0, opt_state0, eta, d_eta_out}));
   size_t st = 0, dy = 0;
-  const size_t need = p->tf ? tf_meta_ws(p->d, T, &st, &dy) : meta_ws_bytes(p, T, &st, &dy);
-  TRY(check_ws(ws, ws_bytes, need));
+  *need = p->tf ? tf_meta_ws(p->d, T, &st, &dy) : meta_ws_bytes(p, T, &st, &dy);
+  return MFMG_OK;
+}
+
+// The meta-gradient on validated arguments and a workspace of at least `need` bytes.
+mfmg_status meta_grad_run(mfmg_problem_t p, const float* theta0, const float* opt_state0,
+                          const float* eta, const mfmg_batch* train_batches, int T,
+                          const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
+                          size_t* peak_bytes_out, size_t need, void* ws, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (p->tf) {
     if (peak_bytes_out) {
@@ -1077,6 +1090,38 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
                             val_loss_out, (char*)ws, s);
   return run_meta<float>(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out,
                          val_loss_out, (char*)ws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* opt_state0,
+                           const float* eta, const mfmg_batch* train_batches, int T,
+                           const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
+                           size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream) {
+  size_t need = 0;
+  TRY(check_meta_args(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out, &need));
+  TRY(check_ws(ws, ws_bytes, need));
+  return meta_grad_run(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out,
+                       val_loss_out, peak_bytes_out, need, ws, stream);
+}
+
+mfmg_status mfmg_check_finite(const float* x, size_t n, size_t* count_out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (!x && n) return fail(MFMG_ERR_INVALID_ARGUMENT, "null x");
+  if (x && !aligned(x, 4)) return fail(MFMG_ERR_INVALID_ARGUMENT, "x not 4-byte aligned");
+  TRY(check_ws(ws, ws_bytes, 256));
+  if (!ws) return fail(MFMG_ERR_INVALID_ARGUMENT, "null workspace");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned long long* cnt = static_cast<unsigned long long*>(ws);
+  HIPCHK(count_nonfinite(x, (long)n, cnt, s));
+  unsigned long long h = 0;
+  HIPCHK(hipMemcpyAsync(&h, cnt, sizeof(h), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  if (count_out) *count_out = (size_t)h;
+  if (h) return fail(MFMG_ERR_NUMERIC, "%llu of %zu values are NaN or infinite", h, n);
+  return MFMG_OK;
 }
 
 mfmg_status mfmg_timing_enable(int enable) {

@@ -672,7 +672,29 @@ __global__ void copy_kernel(const float* __restrict__ src, float* __restrict__ d
     dst[i] = src[i];
 }
 
+// Number of NaN / infinite entries of x, added to *count by one atomic per wave.
+__global__ void count_nonfinite_kernel(const float* __restrict__ x, long n,
+                                       unsigned long long* count) {
+  unsigned c = 0;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    c += (__float_as_uint(x[i]) & 0x7f800000u) == 0x7f800000u;
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+  if ((threadIdx.x & 63) == 0 && c) atomicAdd(count, (unsigned long long)c);
+}
+
+__global__ void zero_count_kernel(unsigned long long* count) {
+  if (threadIdx.x == 0) count[threadIdx.x] = 0ull;
+}
+
 }  // namespace
+
+hipError_t count_nonfinite(const float* x, long n, unsigned long long* count, hipStream_t s) {
+  hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(64), 0, s, count);
+  if (n > 0)
+    hipLaunchKernelGGL(count_nonfinite_kernel, dim3(min(cdiv(n, 256), 4096)), dim3(256), 0, s, x,
+                       n, count);
+  return hipGetLastError();
+}
 
 hipError_t fill(float* p, long n, float v, hipStream_t s) {
   if (n <= 0) return hipSuccess;

@@ -274,6 +274,9 @@ bool linreg_fits(int T, int rows, int vrows, int d);
 hipError_t fill(float* p, long n, float v, hipStream_t s);
 hipError_t copy(const float* src, float* dst, long n, hipStream_t s);
 
+// *count (device) = number of NaN or infinite entries of x[0..n).
+hipError_t count_nonfinite(const float* x, long n, unsigned long long* count, hipStream_t s);
+
 // Kernel timing (api.hip).
 void timing_begin(int cls, hipStream_t s);
 void timing_end(int cls, hipStream_t s);

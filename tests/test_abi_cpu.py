@@ -36,8 +36,9 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for s in range(5):
+    for s in range(6):
         assert L.mfmg_status_string(s).decode().startswith("MFMG_")
+    assert L.mfmg_status_string(M.ERR_NUMERIC) == b"MFMG_ERR_NUMERIC"
 
 
 @pytest.mark.parametrize("cfg", [W.C1, W.C2, W.C3, W.C5], ids=lambda c: c.name)
@@ -179,3 +180,14 @@ def test_step_argument_errors(L):
 def test_timing_read_validates(L):
     n, ms = ctypes.c_int(), ctypes.c_double()
     assert L.mfmg_timing_read(99, ctypes.byref(n), ctypes.byref(ms)) == M.ERR_INVALID_ARGUMENT
+
+
+def test_check_finite_validates(L):
+    n = ctypes.c_size_t(7)
+    assert L.mfmg_check_finite(None, 10, ctypes.byref(n), FAKE, 256, None) == M.ERR_INVALID_ARGUMENT
+    assert L.mfmg_check_finite(FAKE, 10, ctypes.byref(n), FAKE, 255, None) == M.ERR_WORKSPACE
+    assert L.mfmg_check_finite(FAKE, 10, ctypes.byref(n), FAKE + 8, 256, None) == \
+        M.ERR_INVALID_ARGUMENT
+    assert L.mfmg_check_finite(FAKE + 2, 10, ctypes.byref(n), FAKE, 256, None) == \
+        M.ERR_INVALID_ARGUMENT
+    assert n.value == 7   # untouched on a validation error

@@ -316,3 +316,22 @@ def test_tf_meta_grad_full_size_bf16():
     for e, sp in zip(errs, spread):
         assert e <= max(tol_of(cfg), 1.5 * sp)
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
+def test_tf_meta_grad_full_size_bf16_T8():
+    """The transformer workload as specified (T = 8 inner steps, 16 x 256 tokens,
+    d 512, 4 blocks, vocab 8192, bf16 operands, fused attention as bench.py runs
+    it) against the oracle's float64-accumulated bf16 emulation at the plain 2e-2
+    per meta-model tensor (two valid emulations differ by ~1e-3 here)."""
+    cfg = W.C4.with_(fused_attention=1)
+    inp = W.make_inputs(cfg)
+    print(f"\n[tf meta_grad full bf16] T={cfg.T} fused attention", flush=True)
+    got, V, peak = run_meta_tf(cfg, inp)
+    ref, Vref = oracle.meta_grad_checkpointed(cfg, inp, bf16=True)
+    errs = group_errors(cfg, got, ref)
+    print(f"  errors {['%.2e' % e for e in errs]} spread "
+          f"{['%.2e' % e for e in spread_of(f'{W.C4.name}/T8')]} V {V:.6f} ref {Vref:.6f}",
+          flush=True)
+    assert np.all(np.isfinite(got))
+    assert max(errs) <= tol_of(cfg)
+    assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)

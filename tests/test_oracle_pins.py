@@ -440,3 +440,93 @@ def test_bf16_emulation_is_a_small_perturbation(name):
     a, _ = oracle.meta_grad(cfg, inp)
     b, _ = oracle.meta_grad(cfg, inp, bf16=True)
     assert 0 < relerr(b, a) < 2e-2
+
+
+# ---------------------------------------------------------------------------------------
+# Where the bf16 emulation rounds: a hand-written numpy forward/backward with every
+# GEMM operand rounded (round-to-nearest-even written from the float32 bit layout,
+# not through torch's conversion)
+# ---------------------------------------------------------------------------------------
+def rne_bf16(x):
+    """float64 -> float32 -> bfloat16 (round to nearest, ties to even) as float64:
+    add 0x7FFF plus the lowest kept bit to the float32 pattern, clear the low 16 bits."""
+    u = np.ascontiguousarray(np.asarray(x, dtype=np.float32)).view(np.uint32).astype(np.uint64)
+    u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def test_rne_bf16_matches_the_emulation_rounding():
+    x = np.random.default_rng(5).standard_normal(10000) * np.exp(
+        np.random.default_rng(6).uniform(-20, 20, 10000))
+    assert np.array_equal(rne_bf16(x), bf16_round(torch.from_numpy(x)).numpy())
+    # exact ties go to the even mantissa
+    assert rne_bf16(np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8])).tolist() == [1.0, 1 + 2 ** -6]
+
+
+def _softmax_rows(z):
+    e = np.exp(z - z.max(1, keepdims=True))
+    return e / e.sum(1, keepdims=True)
+
+
+@pytest.mark.parametrize("act", [W.ACT_TANH, W.ACT_RELU])
+def test_bf16_emulation_rounding_placement_two_layers(act):
+    """Gradient of a two-layer CE network under the bf16 emulation equals the
+    plain backward with these operands rounded: X, W1 | r(A1), W2 in the forward;
+    dZ2 and W2 in the data product; r(A1), dZ2 and X, dZ1 in the weight products;
+    bias gradients summing the rounded dZ (the reduction reads the same bf16
+    operand copy the weight product does)."""
+    r = rne_bf16
+    cfg = W.C5.with_(name="t_emu2", cfg_id=230, widths=(9, 11, 5), act=act, rows=13,
+                     val_rows=4, T=1, precision=W.PREC_BF16)
+    inp = W.make_inputs(cfg)
+    theta = inp["theta0"].astype(np.float64) + 0.1 * W.random_direction(W.n_theta(cfg), 60)
+    theta = theta.astype(np.float32).astype(np.float64)
+    x, y = inp["train_x"][0].astype(np.float64), inp["train_y"][0]
+    lay = {n: (o, s) for n, o, s in W.theta_layout(cfg)}
+    P = {n: theta[o:o + int(np.prod(s))].reshape(s) for n, (o, s) in lay.items()}
+    N = x.shape[0]
+    z1 = r(x) @ r(P["W0"]) + P["b0"]
+    a1 = np.tanh(z1) if act == W.ACT_TANH else np.maximum(z1, 0)
+    dphi = 1 - a1 ** 2 if act == W.ACT_TANH else (z1 > 0).astype(np.float64)
+    z2 = r(a1) @ r(P["W1"]) + P["b1"]
+    p = _softmax_rows(z2)
+    dz2 = p.copy()
+    dz2[np.arange(N), y] -= 1.0
+    dz2 /= N
+    g = {"W1": r(a1).T @ r(dz2), "b1": r(dz2).sum(0)}
+    dz1 = (r(dz2) @ r(P["W1"]).T) * dphi
+    g["W0"] = r(x).T @ r(dz1)
+    g["b0"] = r(dz1).sum(0)
+    want = np.concatenate([g[n].ravel() for n, _, _ in W.theta_layout(cfg)])
+    got, _ = oracle.grad_and_loss(cfg, theta, x, y, bf16=True)
+    assert relerr(got, want) <= 1e-12
+    # and the rounding is visible: the unrounded gradient is measurably elsewhere
+    plain, _ = oracle.grad_and_loss(cfg, theta, x, y)
+    assert relerr(plain, want) > 1e-4
+
+
+def test_bf16_emulation_hvp_one_layer():
+    """H v of a one-layer CE model (z = x W + b) under the bf16 emulation: the
+    tangent logits are r(x) r(V) + v_b, the tangent of the output gradient is
+    p (zdot - <p, zdot>) / N, and H v = r(x)^T r(that), its bias part the sum of
+    the rounded rows."""
+    r = rne_bf16
+    cfg = W.C5.with_(name="t_emu1", cfg_id=231, widths=(10, 6), rows=12, val_rows=4, T=1,
+                     precision=W.PREC_BF16)
+    inp = W.make_inputs(cfg)
+    n = W.n_theta(cfg)
+    theta = (0.5 * W.random_direction(n, 61)).astype(np.float64)
+    v = W.random_direction(n, 62).astype(np.float64)
+    x, y = inp["train_x"][0].astype(np.float64), inp["train_y"][0]
+    lay = {nm: (o, s) for nm, o, s in W.theta_layout(cfg)}
+    Wt = theta[lay["W0"][0]:lay["W0"][0] + 60].reshape(10, 6)
+    bt = theta[lay["b0"][0]:lay["b0"][0] + 6]
+    Vw = v[lay["W0"][0]:lay["W0"][0] + 60].reshape(10, 6)
+    Vb = v[lay["b0"][0]:lay["b0"][0] + 6]
+    N = x.shape[0]
+    p = _softmax_rows(r(x) @ r(Wt) + bt)
+    zd = r(x) @ r(Vw) + Vb
+    dd = p * (zd - (p * zd).sum(1, keepdims=True)) / N
+    want = np.concatenate([(r(x).T @ r(dd)).ravel(), r(dd).sum(0)])
+    got = oracle.hvp_rev_rev(cfg, theta, x, y, v, bf16=True)
+    assert relerr(got, want) <= 1e-12

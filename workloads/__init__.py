@@ -29,7 +29,7 @@ ROOT_SEED = 250500793
 # enum values shared with include/mfmg.h (plain integers, no arithmetic)
 ACT_TANH, ACT_GELU, ACT_RELU, ACT_NONE = 0, 1, 2, 3
 LOSS_MSE, LOSS_CE = 0, 1
-# squared error after the M-step map y_i = i (2 + sin y_{i-1})^cos y_{i-1} of Section 3.3
+# squared error after the M-step map y_i = i (2 + sin y_{i-1})^cos y_{i-1} of Section 3.2
 # (eq. motivational_example), averaged over the outputs
 LOSS_MAPMSE = 2
 OPT_SGD, OPT_ADAM = 0, 1
@@ -118,7 +118,7 @@ CONFIGS: Dict[str, Config] = {c.name: c for c in (C1, C2, C3, C4, C5)}
 # MAML on the config-5 network: eta = theta_0, SGD at a fixed rate
 MAML5 = C5.with_(name="maml_mlp_relu_8x4096", cfg_id=6, meta=META_MAML, sgd_lr=0.05)
 
-# The paper's motivating example (Section 3.3): y_0 = x w with x of B x D and
+# The paper's motivating example (Section 3.2): y_0 = x w with x of B x D and
 # w of D x D, M map steps, mean squared error against standard normal targets,
 # MAML (w_0 = eta), T = 2 inner SGD steps at rate 1e-3, B = 1024, D = 4096.
 TOY = Config(name="toy_mstep_map", cfg_id=7, widths=(4096, 4096), act=ACT_NONE,
@@ -207,6 +207,26 @@ SMALL: Dict[str, Config] = {
                               vocab=97, seq=1024, rows=2, val_rows=1, n_blocks=1, meta_hidden=16,
                               T=2, fused_attention=1),
 }
+
+
+# Full-width slices of the 8 x 4096 network: its 4096-wide layers and 1024-row
+# batches with bf16 operands, but two or three weight matrices instead of eight.
+# Rounding alone moves their meta-gradients by well under 2e-2 (the deep network
+# amplifies one bf16 ulp of an activation into percent-level changes), so every
+# full-size product shape is gated at the plain bf16 tolerance on these.
+SLICES: Dict[str, Config] = {
+    "c5_slice2": C5.with_(name="c5_slice2", cfg_id=130, widths=(4096, 4096, 1000)),
+    "c5_slice3": C5.with_(name="c5_slice3", cfg_id=131, widths=(4096, 4096, 4096, 1000)),
+}
+
+
+def get(name: str) -> Config:
+    """A workload by name: the five configurations, their reduced variants, the
+    full-width slices, MAML on config 5 and the motivating example."""
+    for table in (CONFIGS, SMALL, SLICES, {MAML5.name: MAML5, TOY.name: TOY}):
+        if name in table:
+            return table[name]
+    raise KeyError(name)
 
 
 # --------------------------------------------------------------------------------------
