@@ -10,7 +10,7 @@ One "step" is one mfmg_meta_grad call: T forward inner steps with
 checkpoints, the validation pass, and T forward-over-reverse reverse steps.
 The line also carries the peak device bytes at every T of the memory sweep,
 the roofline of the dominant kernel (timed with HIP events on the stream it
-runs on) and the float64 CPU oracle timed on a bounded sample.
+runs on) and one whole float64 CPU oracle meta-gradient, timed on the host.
 """
 from __future__ import annotations
 
@@ -101,6 +101,24 @@ def algorithmic_bytes(cfg: W.Config, T: int):
             par = (8 + 4 + (0 if first else 4) + 4 + (0 if last_rev else 4)) * P
             ops = 2 * R * o * 2 + (2 if l == 0 else 4) * R * i
             b[5 if l == 0 else 8] += par + ops
+    # loss head, per pass of `rows` rows over C classes: logits read (float32),
+    # labels read, the output gradient written as bf16 operands in both layouts,
+    # per-row losses written; dual passes also read the logit tangents and write
+    # the gradient's tangent in both layouts
+    C = cfg.widths[-1]
+    for rows, dual in [(R, False)] * T + [(Rv, False)] + [(R, True)] * T:
+        b[6] += rows * C * (16 if dual else 8) + rows * 8
+    # other elementwise kernels: theta_0 to its operand copies once (float32 read,
+    # bf16 W and W^T written); every pass converts its input rows (float32 read,
+    # bf16 rows in both layouts); every pass's bias reductions read dZ^T (and its
+    # tangent) in bf16 and touch the bias streams (~24 bytes per bias)
+    n_w = sum(cfg.widths[l] * cfg.widths[l + 1] for l in range(L))
+    n_b = sum(cfg.widths[1:]) if cfg.has_bias else 0
+    b[7] += 8 * (n_w + n_b)
+    for rows, dual in [(R, False)] * T + [(Rv, False)] + [(R, True)] * T:
+        b[7] += rows * cfg.widths[0] * 8
+        if cfg.has_bias:
+            b[7] += sum(rows * o * (4 if dual else 2) for o in cfg.widths[1:]) + 24 * n_b
     return b
 
 
@@ -210,6 +228,51 @@ def pmc_summary(fetch_csv: str, write_csv: str, copy_bytes: int, cls: str, comma
     print(path)
 
 
+def pmc_mfma_summary(csv_path: str, out_name: str, command: str):
+    """Per-kernel MFMA counters from one rocprofv3 --pmc run of MfmaUtil (matrix-core
+    busy cycles over the dispatch's active cycles, all SIMDs) and MfmaFlopsBF16 /
+    MfmaFlopsF32 (512 x the MFMA ops the hardware counted): a markdown table per
+    kernel instantiation, written under profiles/."""
+    import csv
+    import re
+    per = {}
+    for r in csv.DictReader(open(csv_path)):
+        key = (r["Dispatch_Id"], r["Kernel_Name"])
+        d = per.setdefault(key, {})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+            d["_ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    kern = {}
+    for (_, name), d in per.items():
+        k = kern.setdefault(name, {"n": 0, "util": 0.0, "flops": 0.0, "ns": 0.0})
+        k["n"] += 1
+        k["util"] += d.get("MfmaUtil", 0.0)
+        k["flops"] += d.get("MfmaFlopsBF16", 0.0) + d.get("MfmaFlopsF32", 0.0)
+        k["ns"] += d.get("_ns", 0.0)
+    rows = sorted(((n, k) for n, k in kern.items() if k["flops"] > 0),
+                  key=lambda nk: -nk[1]["ns"])
+    body = [f"# MFMA counters per GEMM kernel: {out_name}", "",
+            "Command (repository root, one MI355X):", "", "```", command, "```", "",
+            "`MfmaUtil` = matrix-core busy cycles summed over all SIMDs / (active cycles of the "
+            "dispatch x SIMDs), in %; `MFMA GFLOP` = 512 x the MFMA ops counted "
+            "(`SQ_INSTS_VALU_MFMA_MOPS_*`), per dispatch; the duration is the dispatch's own "
+            "timestamps under counter collection (kernels serialised).", "",
+            "| kernel | dispatches | MfmaUtil % | MFMA GFLOP / dispatch | us / dispatch | TFLOP/s |",
+            "|---|---:|---:|---:|---:|---:|"]
+    for name, k in rows:
+        short = re.sub(r"^void |\(mfmg::GemmOperands.*$|mfmg::\(anonymous namespace\)::", "", name)
+        short = re.sub(r"<unsigned short>|unsigned short", "bf16", short)[:110]
+        us = k["ns"] / k["n"] / 1e3 if k["ns"] else float("nan")
+        gf = k["flops"] / k["n"] / 1e9
+        tf = gf / us * 1e-3 if k["ns"] else float("nan")
+        body.append(f"| `{short}` | {k['n']} | {k['util'] / k['n']:.1f} | {gf:.2f} | {us:.1f} | "
+                    f"{tf:.0f} |")
+    path = os.path.join(ROOT, "profiles", f"gemm_mfma_counters_{out_name}.md")
+    with open(path, "w") as f:
+        f.write("\n".join(body) + "\n")
+    print(path)
+
+
 def desc_of(cfg: W.Config):
     from paper_2505_00793_amd import _lib as M
     if cfg.kind == W.KIND_TRANSFORMER:
@@ -219,7 +282,7 @@ def desc_of(cfg: W.Config):
                            d_model=cfg.d_model, n_heads=cfg.n_heads, d_ff=cfg.d_ff,
                            vocab=cfg.vocab, seq=cfg.seq, n_blocks=cfg.n_blocks,
                            meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps, rope_base=cfg.rope_base,
-                           fused_attention=cfg.fused_attention)
+                           fused_attention=cfg.fused_attention, block_remat=cfg.block_remat)
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,
@@ -227,32 +290,71 @@ def desc_of(cfg: W.Config):
                        map_steps=cfg.map_steps, ckpt_segment=cfg.ckpt_segment)
 
 
-def cpu_baseline(cfg: W.Config, inp: dict, T: int):
-    """The float64 oracle on the host cores, on a bounded sample of the workload:
-    one forward inner step, the validation seed and one reverse step of the
-    step-checkpointed oracle at full size, extrapolated to T steps."""
+def cpu_model() -> str:
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg: W.Config, inp: dict, runs: int = 1):
+    """The float64 reverse-over-reverse oracle (step-checkpointed) on the host
+    cores: `runs` whole meta-gradients of the workload, timed; 1 / median."""
     import torch
     import oracle
-    from oracle.metagrad import _Inputs, reverse_step, seed
+    times = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        oracle.meta_grad_checkpointed(cfg, inp)
+        times.append(time.perf_counter() - t0)
+    med = sorted(times)[len(times) // 2]
+    return {"value": 1.0 / med, "unit": "meta-gradients/s", "cores": torch.get_num_threads(),
+            "kind": "oracle", "measured": True, "cpu": cpu_model(),
+            "sample": (f"{runs} whole float64 oracle meta-gradient(s) at T={len(inp['train_x'])} "
+                       f"(reverse-over-reverse, one inner step's graph at a time): "
+                       f"{', '.join(f'{t:.2f}' for t in times)} s")}
+
+
+def cpu_baseline_sampled(cfg: W.Config, inp: dict):
+    """The float64 oracle on a bounded sample of a workload too slow to run whole
+    on the host: one forward inner step (with the validation loss), the
+    validation seed and one reverse step at full size, extrapolated to T."""
+    import torch
+    from oracle.metagrad import _Inputs, reverse_step, seed, unroll
+    T = len(inp["train_x"])
     one = dict(inp)
     one["train_x"], one["train_y"] = inp["train_x"][:1], inp["train_y"][:1]
-    I = _Inputs(cfg, one)
+    if cfg.meta == W.META_EXAMPLE_WEIGHT_LOGITS:
+        one["eta"] = inp["eta"][:cfg.rows]
+    c1 = cfg.with_(T=1)
+    I = _Inputs(c1, one)
     t0 = time.perf_counter()
-    th1, _, _, _ = oracle.inner_step(cfg, inp["theta0"], None, inp["eta"], inp["train_x"][0],
-                                     inp["train_y"][0], 0)
+    thetas, opts, _, _ = unroll(c1, one)
     t1 = time.perf_counter()
-    th1 = torch.from_numpy(th1)
-    V, thbar = seed(cfg, I, th1, False)
+    V, thbar = seed(c1, I, thetas[-1], False)
     t2 = time.perf_counter()
-    reverse_step(cfg, I, 0, I.theta0, None, thbar, None, False)
+    reverse_step(c1, I, 0, thetas[0], opts[0], thbar,
+                 None if opts[-1] is None else torch.zeros_like(opts[-1]), False)
     t3 = time.perf_counter()
     per = T * ((t1 - t0) + (t3 - t2)) + (t2 - t1)
     return {"value": 1.0 / per, "unit": "meta-gradients/s", "cores": torch.get_num_threads(),
-            "kind": "oracle",
-            "sample": (f"float64 reverse-over-reverse oracle at full size: one inner step "
+            "kind": "oracle", "measured": False, "cpu": cpu_model(),
+            "sample": (f"float64 oracle at full size: one inner step with the validation loss "
                        f"({t1 - t0:.2f} s), the validation seed ({t2 - t1:.2f} s) and one "
-                       f"reverse step ({t3 - t2:.2f} s), extrapolated to T={T}: "
-                       f"{per:.1f} s per meta-gradient")}
+                       f"reverse step ({t3 - t2:.2f} s), extrapolated to T={T}: {per:.1f} s "
+                       f"per meta-gradient")}
 
 
 WORKLOADS = {
@@ -292,8 +394,33 @@ def bench_config(name: str, args):
     """meta-gradients/s of one of the other workloads at its own T, same timing
     protocol as the main line (inputs resident, warm-up calls, HIP-event timing
     on the stream); no roofline, sweep or CPU baseline."""
+    import torch
+    from paper_2505_00793_amd import _lib as M
     cfg = with_attention(BENCH_CONFIGS[name], args.attention)
+    if cfg.kind == W.KIND_TRANSFORMER:
+        cfg = cfg.with_(block_remat=args.block_remat)
     ms, peak, finite = time_config(cfg, args)
+    sizes = M.Problem(desc_of(cfg)).mfmg_query_sizes(cfg.T)
+    extra = {"static_bytes": sizes.static_bytes, "dynamic_bytes": sizes.dynamic_bytes}
+    if cfg.kind == W.KIND_TRANSFORMER:
+        # the other block-rematerialisation setting, for its time and memory
+        other = cfg.with_(block_remat=1 - cfg.block_remat)
+        ms2, peak2, _ = time_config(other, args)
+        s2 = M.Problem(desc_of(other)).mfmg_query_sizes(cfg.T)
+        extra["block_remat"] = cfg.block_remat
+        extra["vs_block_remat"] = {
+            str(c.block_remat): {"ms_per_meta_grad": round(m, 4), "peak_bytes": pk,
+                                 "static_bytes": z.static_bytes, "dynamic_bytes": z.dynamic_bytes}
+            for c, m, pk, z in ((cfg, ms, peak, sizes), (other, ms2, peak2, s2))}
+    cpu = None
+    if not args.no_cpu_baseline and torch.cuda.is_available():
+        inp = W.make_inputs(cfg)
+        if name in ("c1_linreg", "c2_mlp_tanh_lossweights", "c3_mlp_gelu_adam"):
+            log(f"[bench] {name}: cpu baseline, 3 whole float64 oracle meta-gradients")
+            cpu = cpu_baseline(cfg, inp, runs=3)
+        else:
+            log(f"[bench] {name}: cpu baseline, float64 oracle sample")
+            cpu = cpu_baseline_sampled(cfg, inp)
     print(json.dumps({
         "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
         "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -302,7 +429,8 @@ def bench_config(name: str, args):
         "data": "synthetic (seeded, see workloads/)",
         "config": {"workload": WORKLOADS[name], "name": name, "T": cfg.T,
                    **({"attention": args.attention} if cfg.kind == W.KIND_TRANSFORMER else {})},
-        "peak_bytes": peak, "roofline": None, "cpu_baseline": None, "d_eta_finite": finite,
+        "peak_bytes": peak, **extra, "roofline": None, "cpu_baseline": cpu,
+        "d_eta_finite": finite,
         **({"graph_replay": {"ms_per_step": round(args.graph_ms, 4),
                              "meta_grads_per_s": round(1e3 / args.graph_ms, 4)}}
            if args.graph_ms else {})}))
@@ -442,17 +570,26 @@ def main():
                     help="write the HBM counter summary of --pmc-class from two rocprofv3 "
                          "--pmc runs (made with --copy-bytes) and exit; no GPU needed")
     ap.add_argument("--pmc-class", default="dual_bwd_weight_gemm_reverse")
+    ap.add_argument("--pmc-mfma-summary", nargs=2, metavar=("CSV", "NAME"),
+                    help="write profiles/gemm_mfma_counters_NAME.md from a rocprofv3 --pmc run "
+                         "of MfmaUtil and MfmaFlopsBF16 and exit; no GPU needed")
     ap.add_argument("--config", default="c5_mlp_relu_8x4096", choices=list(BENCH_CONFIGS),
                     help="workload; the default (c5) line carries the roofline, the memory "
                          "sweep and the CPU baseline, the others throughput only")
     ap.add_argument("--pmc-command", default="", help="the commands that made the CSVs")
     ap.add_argument("--attention", default="fused", choices=["fused", "materialised"],
                     help="attention form of the transformer workloads")
+    ap.add_argument("--block-remat", type=int, default=1, choices=[0, 1],
+                    help="transformer workloads: block rematerialisation (the line also "
+                         "times the other setting)")
     ap.add_argument("--graph", action="store_true",
                     help="other workloads: also time graph replays of the same call")
     ap.add_argument("--seq", type=int, default=0, choices=[0, *W.C4_LONG_S],
                     help="c4_long_context: time this sequence length and --attention form only")
     args = ap.parse_args()
+    if args.pmc_mfma_summary:
+        pmc_mfma_summary(args.pmc_mfma_summary[0], args.pmc_mfma_summary[1], args.pmc_command)
+        return
     if args.pmc_summary:
         pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_bytes or (1 << 30),
                     args.pmc_class, args.pmc_command)
@@ -608,8 +745,11 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (float64 oracle sample)")
-        cpu = cpu_baseline(cfg, inp, T)
+        log(f"[bench] cpu baseline: one whole float64 oracle meta-gradient at T={T}")
+        one = dict(inp)
+        one["train_x"], one["train_y"] = inp["train_x"][:T], inp["train_y"][:T]
+        cpu = cpu_baseline(cfg, one, runs=1)
+        log(f"[bench] cpu baseline: {1.0 / cpu['value']:.1f} s per meta-gradient")
 
     out = {
         "metric": "meta-gradients/sec + peak HBM bytes vs T on 1 MI355X; MFMA util of HVP GEMMs",

@@ -176,6 +176,18 @@ typedef struct {
    * softmax attention); requires MFMG_PREC_BF16, head dimension
    * d_model / n_heads = 64 and seq a multiple of 64. */
   int fused_attention;
+  /* Transformer kind only: block rematerialisation (Section 4, "Block
+   * rematerialisation").  0 keeps every block's activations (and tangents) of
+   * one inner step from its forward for its backward, so dynamic memory grows
+   * with n_blocks.  1 keeps only the residual stream entering each block (and
+   * its tangent) and recomputes the block's forward, with the tangent in dual
+   * passes, at the start of that block's backward: one buffer set serves all
+   * blocks, dynamic memory is flat in n_blocks up to the block inputs
+   * (2 * 4 * rows * seq * d_model bytes per block), and each backward does one
+   * more block forward per block (its last residual product excepted).  The
+   * recomputation repeats the same kernels on the same inputs, so results are
+   * bit-identical to 0. */
+  int block_remat;
 } mfmg_problem_desc;
 
 typedef struct mfmg_problem* mfmg_problem_t;

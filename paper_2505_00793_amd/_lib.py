@@ -33,6 +33,7 @@ class mfmg_problem_desc(ctypes.Structure):
         ("d_model", c_int), ("n_heads", c_int), ("d_ff", c_int), ("vocab", c_int), ("seq", c_int),
         ("n_blocks", c_int), ("meta_hidden", c_int), ("ln_eps", c_float), ("rope_base", c_float),
         ("map_steps", c_int), ("ckpt_segment", c_int), ("fused_attention", c_int),
+        ("block_remat", c_int),
     ]
 
 

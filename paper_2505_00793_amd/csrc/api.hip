@@ -871,8 +871,9 @@ mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* o
   if (d.ckpt_segment < 0 || d.ckpt_segment > (1 << 20))
     return fail(MFMG_ERR_INVALID_ARGUMENT, "ckpt_segment = %d outside [0, 2^20]",
                 d.ckpt_segment);
-  if (d.fused_attention != 0)
-    return fail(MFMG_ERR_INVALID_ARGUMENT, "fused_attention applies to transformer problems");
+  if (d.fused_attention != 0 || d.block_remat != 0)
+    return fail(MFMG_ERR_INVALID_ARGUMENT,
+                "fused_attention and block_remat apply to transformer problems");
   if (d.optimizer != MFMG_OPT_SGD && d.optimizer != MFMG_OPT_ADAM)
     return fail(MFMG_ERR_INVALID_ARGUMENT, "unknown optimizer %d", d.optimizer);
   if (d.precision != MFMG_PREC_FP32 && d.precision != MFMG_PREC_BF16)

@@ -554,10 +554,16 @@ __global__ void __launch_bounds__(1024) adam_reduce_kernel(const float* __restri
 // validation batch.  Forward unroll with theta_t checkpoints, then the
 // reverse sweep with the dual pass (r, rdot) = (X theta - y, X v):
 // g = (2/N) X^T r, H v = (2/N) X^T rdot.
+// 1024 threads; each batch is staged in LDS (when it fits in 64 KB) with
+// 16-byte loads, residuals take one wave per row (lanes over the features,
+// wave reductions), and X^T r takes 64 features x 16 row groups per pass with
+// an ordered sum of the 16 partials.
 // ------------------------------------------------------------------------------------
 constexpr int LR_MAXD = 256;
 constexpr int LR_MAXR = 1024;
 constexpr int LR_MAXT = 64;
+constexpr int LR_THREADS = 1024;
+constexpr int LR_STAGE = 16384;  // floats of one batch staged in LDS (64 KB)
 
 struct LinregArgs {
   const float* theta0;
@@ -572,12 +578,87 @@ struct LinregArgs {
   float* ckpt;  // (T + 1) x d
 };
 
-__global__ void __launch_bounds__(256) linreg_kernel(LinregArgs a) {
+// X rows x d (row-major) into LDS when it fits, else left in global memory.
+__device__ const float* lr_stage(const float* X, int rows, int d, float* stage) {
+  const int n = rows * d;
+  if (n > LR_STAGE) return X;
+  __syncthreads();  // the previous batch's readers are done
+  if ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0) {
+    const float4* X4 = reinterpret_cast<const float4*>(X);
+    float4* S4 = reinterpret_cast<float4*>(stage);
+    for (int i = threadIdx.x; i < n / 4; i += LR_THREADS) S4[i] = X4[i];
+  } else {
+    for (int i = threadIdx.x; i < n; i += LR_THREADS) stage[i] = X[i];
+  }
+  __syncthreads();
+  return stage;
+}
+
+// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when u): one wave per row.
+// Returns this thread's share of sum_n r[n]^2 (lane 0 of each wave).
+__device__ float lr_rows(const float* X, const float* __restrict__ y, const float* w,
+                         const float* u, int rows, int d, float* r, float* rd) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float sq = 0.0f;
+  for (int n = wave; n < rows; n += LR_THREADS / 64) {
+    float s = 0.0f, sd = 0.0f;
+    for (int j = lane; j < d; j += 64) {
+      const float x = X[n * d + j];
+      s += x * w[j];
+      if (u) sd += x * u[j];
+    }
+    s = wave_sum(s);
+    if (u) sd = wave_sum(sd);
+    if (lane == 0) {
+      const float res = s - y[n];
+      r[n] = res;
+      if (u) rd[n] = sd;
+      sq += res * res;
+    }
+  }
+  __syncthreads();
+  return sq;
+}
+
+// out[j] = sum_n X[n][j] v[n] (and out2 with v2 when v2), j < d.
+__device__ void lr_cols(const float* X, const float* v, const float* v2, int rows, int d,
+                        float* part, float* part2, float* out, float* out2) {
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  for (int j0 = 0; j0 < d; j0 += 64) {
+    const int j = j0 + c;
+    float s = 0.0f, s2 = 0.0f;
+    if (j < d) {
+      for (int n = q; n < rows; n += 16) {
+        const float x = X[n * d + j];
+        s += x * v[n];
+        if (v2) s2 += x * v2[n];
+      }
+    }
+    part[q * 64 + c] = s;
+    if (v2) part2[q * 64 + c] = s2;
+    __syncthreads();
+    if (threadIdx.x < 64 && j < d) {
+      float a = 0.0f, b = 0.0f;
+      for (int k = 0; k < 16; ++k) {
+        a += part[k * 64 + c];
+        if (v2) b += part2[k * 64 + c];
+      }
+      out[j] = a;
+      if (v2) out2[j] = b;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
+  __shared__ __attribute__((aligned(16))) float stage[LR_STAGE];
   __shared__ float th[LR_MAXD], tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD], vv[LR_MAXD];
+  __shared__ float gs[LR_MAXD], hs[LR_MAXD];
   __shared__ float r[LR_MAXR], rd[LR_MAXR];
-  __shared__ float red[256];
+  __shared__ float part[16 * 64], part2[16 * 64];
+  __shared__ float red[LR_THREADS / 64];
   const int tid = threadIdx.x, d = a.d;
-  for (int j = tid; j < d; j += 256) {
+  for (int j = tid; j < d; j += LR_THREADS) {
     th[j] = a.theta0[j];
     lam[j] = expf(a.eta[j]);
     eb[j] = 0.0f;
@@ -586,81 +667,50 @@ __global__ void __launch_bounds__(256) linreg_kernel(LinregArgs a) {
   __syncthreads();
   // forward unroll
   for (int t = 0; t < a.T; ++t) {
-    const float* X = a.xs[t];
-    const float* y = a.ys[t];
+    const float* X = lr_stage(a.xs[t], a.rows, d, stage);
     const float inv = 2.0f / a.rows;
-    for (int n = tid; n < a.rows; n += 256) {
-      float s = -y[n];
-      for (int j = 0; j < d; ++j) s += X[(long)n * d + j] * th[j];
-      r[n] = s;
-    }
-    __syncthreads();
-    for (int j = tid; j < d; j += 256) {
-      float g = 0.0f;
-      for (int n = 0; n < a.rows; ++n) g += X[(long)n * d + j] * r[n];
-      th[j] -= lam[j] * inv * g;
+    lr_rows(X, a.ys[t], th, nullptr, a.rows, d, r, nullptr);
+    lr_cols(X, r, nullptr, a.rows, d, part, nullptr, gs, nullptr);
+    for (int j = tid; j < d; j += LR_THREADS) {
+      th[j] -= lam[j] * inv * gs[j];
       a.ckpt[(long)(t + 1) * d + j] = th[j];
     }
     __syncthreads();
   }
   // validation loss and its gradient (the seed of the reverse sweep)
   {
+    const float* X = lr_stage(a.vx, a.vrows, d, stage);
     const float inv = 2.0f / a.vrows;
-    float ls = 0.0f;
-    for (int n = tid; n < a.vrows; n += 256) {
-      float s = -a.vy[n];
-      for (int j = 0; j < d; ++j) s += a.vx[(long)n * d + j] * th[j];
-      r[n] = s;
-      ls += s * s;
+    const float sq = lr_rows(X, a.vy, th, nullptr, a.vrows, d, r, nullptr);
+    if ((tid & 63) == 0) red[tid >> 6] = sq;
+    lr_cols(X, r, nullptr, a.vrows, d, part, nullptr, gs, nullptr);
+    if (tid == 0 && a.val_loss) {
+      float ls = 0.0f;
+      for (int k = 0; k < LR_THREADS / 64; ++k) ls += red[k];
+      *a.val_loss = ls / a.vrows;
     }
-    red[tid] = ls;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-      if (tid < o) red[tid] += red[tid + o];
-      __syncthreads();
-    }
-    if (tid == 0 && a.val_loss) *a.val_loss = red[0] / a.vrows;
-    for (int j = tid; j < d; j += 256) {
-      float g = 0.0f;
-      for (int n = 0; n < a.vrows; ++n) g += a.vx[(long)n * d + j] * r[n];
-      tb[j] = inv * g;
-    }
+    for (int j = tid; j < d; j += LR_THREADS) tb[j] = inv * gs[j];
     __syncthreads();
   }
-  // reverse sweep
+  // reverse sweep: v = -exp(eta) bar theta_{i+1}; bar theta_i = bar theta_{i+1} + H v;
+  // bar eta += -exp(eta) g_i bar theta_{i+1}
   for (int i = a.T - 1; i >= 0; --i) {
-    const float* X = a.xs[i];
-    const float* y = a.ys[i];
     const float inv = 2.0f / a.rows;
-    for (int j = tid; j < d; j += 256) {
+    for (int j = tid; j < d; j += LR_THREADS) {
       th[j] = a.ckpt[(long)i * d + j];
       vv[j] = -lam[j] * tb[j];
     }
-    __syncthreads();
-    for (int n = tid; n < a.rows; n += 256) {
-      float s = -y[n], sd = 0.0f;
-      for (int j = 0; j < d; ++j) {
-        const float x = X[(long)n * d + j];
-        s += x * th[j];
-        sd += x * vv[j];
-      }
-      r[n] = s;
-      rd[n] = sd;
-    }
-    __syncthreads();
-    for (int j = tid; j < d; j += 256) {
-      float g = 0.0f, hv = 0.0f;
-      for (int n = 0; n < a.rows; ++n) {
-        const float x = X[(long)n * d + j];
-        g += x * r[n];
-        hv += x * rd[n];
-      }
-      eb[j] += -lam[j] * inv * g * tb[j];
-      tb[j] += inv * hv;
+    const float* X = lr_stage(a.xs[i], a.rows, d, stage);  // its barriers publish th, vv
+    if (a.rows * d > LR_STAGE) __syncthreads();
+    lr_rows(X, a.ys[i], th, vv, a.rows, d, r, rd);
+    lr_cols(X, r, rd, a.rows, d, part, part2, gs, hs);
+    for (int j = tid; j < d; j += LR_THREADS) {
+      eb[j] += -lam[j] * inv * gs[j] * tb[j];
+      tb[j] += inv * hs[j];
     }
     __syncthreads();
   }
-  for (int j = tid; j < d; j += 256) a.d_eta[j] = eb[j];
+  for (int j = tid; j < d; j += LR_THREADS) a.d_eta[j] = eb[j];
 }
 
 __global__ void fill_kernel(float* p, long n, float v) {
@@ -854,7 +904,7 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   a.d_eta = d_eta;
   a.val_loss = val_loss;
   a.ckpt = scratch;
-  hipLaunchKernelGGL(linreg_kernel, dim3(1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(linreg_kernel, dim3(1), dim3(LR_THREADS), 0, s, a);
   return hipGetLastError();
 }
 

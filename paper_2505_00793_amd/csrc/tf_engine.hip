@@ -47,7 +47,7 @@ struct Carver {
 constexpr int MAXB = 16;
 
 struct Lay {
-  int d, H, dh, F, V, S, Bt, Bv, L, mh, VE, fused;
+  int d, H, dh, F, V, S, Bt, Bv, L, mh, VE, fused, remat;
   float eps, lr;
   double base;
   long emb, ln1g[MAXB], ln1b[MAXB], wqkv[MAXB], wo[MAXB], ln2g[MAXB], ln2b[MAXB], w1[MAXB],
@@ -74,6 +74,7 @@ Lay make_lay(const mfmg_problem_desc& D) {
   y.mh = D.meta_hidden;
   y.VE = D.precision == MFMG_PREC_BF16 ? 8 : 4;
   y.fused = D.fused_attention;
+  y.remat = D.block_remat;
   y.eps = D.ln_eps;
   y.lr = D.sgd_lr;
   y.base = D.rope_base;
@@ -183,11 +184,38 @@ void carve_act(const Lay& y, Carver& c, Act<T>& a) {
   auto OPT = [&](long n) { return c.take<T>(n); };
   a.ids = c.take<int>(N);
   a.labels = c.take<int>(N);
+  // The residual stream: h[2b] enters block b, h[2b + 1] is its middle (after
+  // attention), h[2L] enters the final LayerNorm.  With block rematerialisation
+  // the block inputs are kept and one buffer holds every block's middle.
   for (int k = 0; k <= 2 * y.L; ++k) {
+    if (y.remat && (k & 1) && k > 1) {
+      a.h[k] = a.h[1];
+      a.hd[k] = a.hd[1];
+      continue;
+    }
     a.h[k] = F32(N * d);
     a.hd[k] = F32(N * d);
   }
+  // Per-block activations: one set per block, or with block rematerialisation
+  // one set that every block's (re)computed forward fills in turn.
   for (int b = 0; b < y.L; ++b) {
+    if (y.remat && b > 0) {
+      a.xh1[b] = a.xh1[0]; a.xhd1[b] = a.xhd1[0]; a.rs1[b] = a.rs1[0]; a.c1[b] = a.c1[0];
+      a.xh2[b] = a.xh2[0]; a.xhd2[b] = a.xhd2[0]; a.rs2[b] = a.rs2[0]; a.c2[b] = a.c2[0];
+      a.a1[b] = a.a1[0]; a.a1T[b] = a.a1T[0]; a.a1d[b] = a.a1d[0]; a.a1dT[b] = a.a1dT[0];
+      a.a2[b] = a.a2[0]; a.a2T[b] = a.a2T[0]; a.a2d[b] = a.a2d[0]; a.a2dT[b] = a.a2dT[0];
+      a.Q[b] = a.Q[0]; a.QT[b] = a.QT[0]; a.K[b] = a.K[0]; a.KT[b] = a.KT[0];
+      a.Vv[b] = a.Vv[0]; a.VT[b] = a.VT[0];
+      a.Qd[b] = a.Qd[0]; a.QdT[b] = a.QdT[0]; a.Kd[b] = a.Kd[0]; a.KdT[b] = a.KdT[0];
+      a.Vd[b] = a.Vd[0]; a.VdT[b] = a.VdT[0];
+      a.P32[b] = a.P32[0]; a.Pd32[b] = a.Pd32[0];
+      a.Pb[b] = a.Pb[0]; a.PbT[b] = a.PbT[0]; a.Pdb[b] = a.Pdb[0]; a.PdbT[b] = a.PdbT[0];
+      a.lse[b] = a.lse[0]; a.cst[b] = a.cst[0];
+      a.O[b] = a.O[0]; a.OT[b] = a.OT[0]; a.Od[b] = a.Od[0]; a.OdT[b] = a.OdT[0];
+      a.Z1[b] = a.Z1[0]; a.Z1d[b] = a.Z1d[0];
+      a.A1[b] = a.A1[0]; a.A1T[b] = a.A1T[0]; a.A1d[b] = a.A1d[0]; a.A1dT[b] = a.A1dT[0];
+      continue;
+    }
     a.xh1[b] = F32(N * d); a.xhd1[b] = F32(N * d); a.rs1[b] = F32(N); a.c1[b] = F32(N);
     a.xh2[b] = F32(N * d); a.xhd2[b] = F32(N * d); a.rs2[b] = F32(N); a.c2[b] = F32(N);
     a.a1[b] = OPT(N * y.ld(d)); a.a1T[b] = OPT(d * y.ld(N));
@@ -509,12 +537,34 @@ struct TfEng {
   // Forward (dual when v) of Bn sequences through the decoder up to the logits.
   hipError_t forward(const Ops<T>& th, const Ops<T>* v, int Bn, const Act<T>& a) const {
     const bool dual = v != nullptr;
+    const int d = y.d, N = Bn * y.S;
+    HC(gather_rows(a.ids, N, d, th.emb, dual ? v->emb : nullptr, a.h[0], dual ? a.hd[0] : nullptr, s));
+    for (int b = 0; b < y.L; ++b) HC(block_forward(th, v, Bn, b, true, a));
+    // final LayerNorm -> af, logits = af U
+    LnArgs ln;
+    ln.x = a.h[2 * y.L]; ln.xd = a.hd[2 * y.L];
+    ln.g = th.lnf[0]; ln.b = th.lnf[1];
+    ln.gd = dual ? v->lnf[0] : nullptr; ln.bd = dual ? v->lnf[1] : nullptr;
+    ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xhf; ln.xhd = a.xhdf; ln.rstd = a.rsf; ln.c = a.cf;
+    ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
+    HC(ln_operands(ln, a.af, a.afd, a.afT, a.afdT));
+    HC(store(op(a.af, dual ? a.afd : nullptr, th.UT, dual ? v->UT : nullptr, (int)y.ld(d),
+                (int)y.ld(d), N, y.V, d),
+             fl(dual), a.logits, a.logitsd, y.V, 0, 1.0f, dual));
+    return hipSuccess;
+  }
+
+  // Block b's forward from its input h[2b] (and tangent): everything its
+  // backward reads, and with `output` also the block's output h[2b + 2] (the
+  // rematerialising pass before the block's backward skips that last product).
+  hipError_t block_forward(const Ops<T>& th, const Ops<T>* v, int Bn, int b, bool output,
+                           const Act<T>& a) const {
+    const bool dual = v != nullptr;
     const int d = y.d, S = y.S, H = y.H, dh = y.dh, F = y.F;
     const int N = Bn * S, BH = Bn * H;
     const long hrow = (long)S * y.ld(dh), hcol = (long)dh * y.ld(S), pS = (long)S * y.ld(S);
     const float scale = 1.0f / std::sqrt((float)dh);
-    HC(gather_rows(a.ids, N, d, th.emb, dual ? v->emb : nullptr, a.h[0], dual ? a.hd[0] : nullptr, s));
-    for (int b = 0; b < y.L; ++b) {
+    {
       // LayerNorm 1 -> a1
       LnArgs ln;
       ln.x = a.h[2 * b]; ln.xd = a.hd[2 * b];
@@ -617,7 +667,7 @@ struct TfEng {
                            fl(dual), e, s));
       }
       // h_out = h_mid + A1 W2
-      {
+      if (output) {
         EpiResid e;
         e.H = a.h[2 * b + 1]; e.Hd = a.hd[2 * b + 1]; e.Ho = a.h[2 * b + 2]; e.Hdo = a.hd[2 * b + 2];
         e.M = N; e.N = d; e.dual = dual;
@@ -626,17 +676,6 @@ struct TfEng {
                          fl(dual), e, s));
       }
     }
-    // final LayerNorm -> af, logits = af U
-    LnArgs ln;
-    ln.x = a.h[2 * y.L]; ln.xd = a.hd[2 * y.L];
-    ln.g = th.lnf[0]; ln.b = th.lnf[1];
-    ln.gd = dual ? v->lnf[0] : nullptr; ln.bd = dual ? v->lnf[1] : nullptr;
-    ln.y = a.y32; ln.yd = a.yd32; ln.xh = a.xhf; ln.xhd = a.xhdf; ln.rstd = a.rsf; ln.c = a.cf;
-    ln.N = N; ln.d = d; ln.dual = dual; ln.eps = y.eps;
-    HC(ln_operands(ln, a.af, a.afd, a.afT, a.afdT));
-    HC(store(op(a.af, dual ? a.afd : nullptr, th.UT, dual ? v->UT : nullptr, (int)y.ld(d),
-                (int)y.ld(d), N, y.V, d),
-             fl(dual), a.logits, a.logitsd, y.V, 0, 1.0f, dual));
     return hipSuccess;
   }
 
@@ -700,6 +739,10 @@ struct TfEng {
                    nullptr, nullptr, y.lnfg, y.lnfb, out ? out->lnf[0] : nullptr,
                    out ? out->lnf[1] : nullptr));
     for (int b = y.L - 1; b >= 0; --b) {
+      // block rematerialisation: the shared buffers hold the last block's
+      // activations from the forward; every other block is recomputed from its
+      // input h[2b] before its backward
+      if (y.remat && b < y.L - 1) HC(block_forward(th, v, Bn, b, false, a));
       // ---- MLP: h_out = h_mid + GELU(a2 W1) W2
       HC(dh_operands(N, dual, a));
       HC(gemm_param<T>(wsk(op(a.A1T[b], dual ? a.A1dT[b] : nullptr, a.dhbT, dual ? a.dhdbT : nullptr,
@@ -956,6 +999,7 @@ const char* tf_validate(const mfmg_problem_desc& D) {
   if (!(D.ln_eps > 0.f) || !(D.rope_base > 0.f) || !std::isfinite(D.sgd_lr))
     return "ln_eps and rope_base must be > 0, sgd_lr finite";
   if (D.fused_attention != 0 && D.fused_attention != 1) return "fused_attention must be 0 or 1";
+  if (D.block_remat != 0 && D.block_remat != 1) return "block_remat must be 0 or 1";
   if (D.fused_attention &&
       (D.precision != MFMG_PREC_BF16 || !attn_fused_supported(D.seq, dh)))
     return "fused attention needs bf16 operands, head dim 64 and seq a multiple of 64";

@@ -21,7 +21,8 @@ def desc_of(cfg: W.Config):
                            d_model=cfg.d_model, n_heads=cfg.n_heads, d_ff=cfg.d_ff,
                            vocab=cfg.vocab, seq=cfg.seq, n_blocks=cfg.n_blocks,
                            meta_hidden=cfg.meta_hidden, ln_eps=cfg.ln_eps,
-                           rope_base=cfg.rope_base, fused_attention=cfg.fused_attention)
+                           rope_base=cfg.rope_base, fused_attention=cfg.fused_attention,
+                           block_remat=cfg.block_remat)
     return M.make_desc(widths=cfg.widths, act=cfg.act, loss=cfg.loss, optimizer=cfg.optimizer,
                        meta=cfg.meta, precision=cfg.precision, has_bias=cfg.has_bias,
                        rows=cfg.rows, val_rows=cfg.val_rows, sgd_lr=cfg.sgd_lr,

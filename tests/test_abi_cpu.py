@@ -90,6 +90,8 @@ def test_create_rejects_bad_descriptions(L, field, value, status):
     (W.C5, {"meta": W.META_MAML, "optimizer": W.OPT_ADAM}, 2),   # MAML is SGD only
     (W.C4, {"meta": W.META_MAML}, 2),                  # and MLP only
     (W.C5, {"fused_attention": 1}, 1),                  # attention options are transformer only
+    (W.C5, {"block_remat": 1}, 1),
+    (W.C4, {"block_remat": 2}, 2),
     (W.C4, {"fused_attention": 2}, 2),
     (W.C4.with_(precision=W.PREC_FP32), {"fused_attention": 1}, 2),   # bf16 operands only
     (W.C4.with_(n_heads=4), {"fused_attention": 1}, 2),               # head dim 128
@@ -191,3 +193,21 @@ def test_check_finite_validates(L):
     assert L.mfmg_check_finite(FAKE + 2, 10, ctypes.byref(n), FAKE, 256, None) == \
         M.ERR_INVALID_ARGUMENT
     assert n.value == 7   # untouched on a validation error
+
+
+def test_block_remat_dynamic_memory_flat_in_depth():
+    """With block rematerialisation the transformer's dynamic bytes grow with the
+    number of blocks only by the kept block inputs (the residual stream and its
+    tangent, float32: 8 bytes per token and model dimension per block); without
+    it every block's activations are kept (size query only, no GPU)."""
+    T = 8
+    size = lambda L, r: M.Problem(desc_of(W.C4.with_(n_blocks=L, block_remat=r,
+                                                     fused_attention=1))).mfmg_query_sizes(T)
+    N, d = W.C4.val_rows * W.C4.seq, W.C4.d_model
+    for L in (4, 8):
+        grow = size(L + 4, 1).dynamic_bytes - size(L, 1).dynamic_bytes
+        assert abs(grow - 4 * 8 * N * d) <= 4 * 8 * 256
+        assert size(L, 1).static_bytes == size(L, 0).static_bytes
+    assert size(8, 1).dynamic_bytes < 1.06 * size(4, 1).dynamic_bytes
+    assert size(8, 0).dynamic_bytes > 1.5 * size(4, 0).dynamic_bytes
+    assert size(4, 1).dynamic_bytes < 0.65 * size(4, 0).dynamic_bytes

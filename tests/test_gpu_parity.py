@@ -393,3 +393,43 @@ def test_check_finite():
     cfg = W.SMALL["c5_small"]
     got, _, _ = run_meta(cfg, W.make_inputs(cfg))
     assert M().mfmg_check_finite(torch.from_numpy(got.astype(np.float32)).cuda()) == 0
+
+
+@pytest.mark.parametrize("name", ["c2_mlp_tanh_lossweights", "c5_mid", "c3_small", "c4_small"])
+def test_peak_bytes_match_device_allocations(name):
+    """The peak bytes mfmg_meta_grad reports (computed on the host: its inputs,
+    outputs and the workspace it uses) against a measurement: the device bytes
+    requested from torch's allocator for exactly those buffers, at its peak
+    while the call runs, and the device's free memory, which the call leaves
+    unchanged (it allocates nothing)."""
+    import gc
+    cfg = cfg_of(name)
+    inp = W.make_inputs(cfg)
+    gc.collect()
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_stats()["requested_bytes.all.current"]
+    P = M().Problem(desc_of(cfg))
+    dev = to_device(inp)
+    if cfg.kind == W.KIND_TRANSFORMER:
+        dev["ys"], dev["vy"] = [None] * len(dev["xs"]), None
+    d = torch.empty(W.n_eta(cfg), device="cuda")
+    vl = torch.empty(1, device="cuda")
+    need = P.mfmg_query_sizes(cfg.T).workspace_bytes
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+
+    def call():
+        return P.mfmg_meta_grad(dev["theta0"], dev["opt_state0"], dev["eta"], dev["xs"],
+                                dev["ys"], dev["vx"], dev["vy"], d, vl, ws=ws)
+
+    call()   # a first call loads the library's code objects onto the device
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    free0, _ = torch.cuda.mem_get_info()
+    peak = call()
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    held = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
+    print(f"\n[peak bytes] {name}: library {peak} requested from torch {held} free before/after "
+          f"{free0}/{free1}", flush=True)
+    assert free1 == free0
+    assert held == peak

@@ -335,3 +335,58 @@ def test_tf_meta_grad_full_size_bf16_T8():
     assert np.all(np.isfinite(got))
     assert max(errs) <= tol_of(cfg)
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
+
+
+# ---------------------------------------------------------------------------------------
+# Block rematerialisation (Section 4): each block's forward is recomputed from its
+# input at the start of its backward, in the unroll, the seed and the dual reverse sweep
+# ---------------------------------------------------------------------------------------
+REMAT_CASES = {"c4_small_fp32": W.SMALL["c4_small"].with_(precision=W.PREC_FP32),
+               "c4_small": W.SMALL["c4_small"], "c4_mid": W.SMALL["c4_mid"],
+               "c4_fused": W.SMALL["c4_fused"], "c4_fused64": W.SMALL["c4_fused64"]}
+
+
+@pytest.mark.parametrize("name", list(REMAT_CASES))
+def test_tf_block_remat_meta_grad(name):
+    """The meta-gradient with block rematerialisation: bit-identical to keeping
+    every block's activations (the same kernels recompute the same values), and
+    against the oracle (float64, or its bf16 emulation) at the stated tolerance."""
+    base = REMAT_CASES[name]
+    inp = W.make_inputs(base)
+    print(f"\n[tf block remat] {name} blocks={base.n_blocks} T={base.T}", flush=True)
+    d0, V0, _ = run_meta_tf(base, inp)
+    d1, V1, _ = run_meta_tf(base.with_(block_remat=1), inp)
+    ref, Vref = oracle.meta_grad_checkpointed(base, inp, bf16=base.precision == W.PREC_BF16)
+    errs = group_errors(base, d1, ref)
+    print(f"  bit-identical {np.array_equal(d0, d1)}; vs oracle {['%.2e' % e for e in errs]}",
+          flush=True)
+    assert np.array_equal(d0, d1) and V0 == V1
+    assert max(errs) <= tol_of(base)
+    assert abs(V1 - Vref) <= tol_of(base) * abs(Vref)
+
+
+@pytest.mark.parametrize("name", ["c4_small", "c4_fused"])
+def test_tf_block_remat_single_step(name):
+    """The inner step and the forward-over-reverse pass with block rematerialisation."""
+    cfg = W.SMALL[name].with_(block_remat=1)
+    prec = "bf16_fused" if cfg.fused_attention else "bf16"
+    check_inner_step(cfg, prec)
+    check_hvp(cfg, prec)
+
+
+def test_tf_block_remat_full_size():
+    """The full transformer workload at T=2 (fused attention): rematerialised
+    blocks give the same bits as kept ones, match the bf16 emulation at 2e-2,
+    and use less dynamic memory."""
+    base = W.C4.with_(T=2, fused_attention=1)
+    inp = W.make_inputs(base, T=2)
+    print("\n[tf block remat] full size T=2 fused attention", flush=True)
+    d0, V0, peak0 = run_meta_tf(base, inp)
+    d1, V1, peak1 = run_meta_tf(base.with_(block_remat=1), inp)
+    ref, Vref = oracle.meta_grad_checkpointed(base, inp, bf16=True)
+    errs = group_errors(base, d1, ref)
+    print(f"  bit-identical {np.array_equal(d0, d1)}; vs oracle {['%.2e' % e for e in errs]}; "
+          f"peak {peak0 / 1e9:.3f} -> {peak1 / 1e9:.3f} GB", flush=True)
+    assert np.array_equal(d0, d1) and V0 == V1
+    assert max(errs) <= tol_of(base)
+    assert peak1 < peak0

@@ -68,6 +68,7 @@ class Config:
     map_steps: int = 0                     # M of the toy map (LOSS_MAPMSE)
     ckpt_segment: int = 0                  # GPU static-memory segments (0: keep every step)
     fused_attention: int = 0               # transformer, bf16: fused causal attention (no S^2 buffers)
+    block_remat: int = 0                   # transformer: recompute each block in its backward
     # transformer
     d_model: int = 0
     n_heads: int = 0
