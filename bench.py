@@ -273,6 +273,74 @@ def pmc_mfma_summary(csv_path: str, out_name: str, command: str):
     print(path)
 
 
+def pmc_traffic_summary(fetch_csv: str, write_csv: str, copy_bytes: int, regex: str, label: str,
+                        command: str):
+    """HBM bytes per dispatch of every kernel whose name matches `regex`, from two
+    rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) made with --copy-bytes, each
+    counter scaled by its reading for the plain copy; written to
+    profiles/LABEL_hbm_counters.md."""
+    import csv
+    import re
+
+    def load(path, counter):
+        per = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            per.setdefault(r["Dispatch_Id"], [r["Kernel_Name"], 0.0])[1] += float(r["Counter_Value"])
+        return list(per.values())
+
+    stats = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = load(path, counter)
+        copies = sorted((v for n, v in rows if "copyBuffer" in n), reverse=True)[:3]
+        factor = (copy_bytes / 1024.0) / (sum(copies) / len(copies))
+        for n, v in rows:
+            if re.search(regex, n):
+                k = stats.setdefault(n, {}).setdefault(counter, [0, 0.0, factor])
+                k[0] += 1
+                k[1] += v
+    body = [f"# HBM traffic counters: {label}", "", "Commands (repository root, one MI355X), "
+            "one counter per pass:", "", "```", command, "```", "",
+            f"Each counter is scaled by its reading for a plain device copy of {copy_bytes} "
+            "bytes (`__amd_rocclr_copyBuffer`, which reads and writes exactly that many bytes) "
+            "and averaged over the kernel's dispatches.", "",
+            "| kernel | dispatches | FETCH (KB / dispatch) | WRITE (KB / dispatch) |",
+            "|---|---:|---:|---:|"]
+    for name, c in sorted(stats.items()):
+        short = re.sub(r"^void |mfmg::\(anonymous namespace\)::|\(mfmg::.*$|\(.*$", "", name)
+        f = c.get("FETCH_SIZE", [1, 0.0, 1.0])
+        w = c.get("WRITE_SIZE", [1, 0.0, 1.0])
+        body.append(f"| `{short[:100]}` | {f[0]} | {f[1] / f[0] * 1.024 * f[2]:.1f} | "
+                    f"{w[1] / w[0] * 1.024 * w[2]:.1f} |")
+    path = os.path.join(ROOT, "profiles", f"{label}_hbm_counters.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(body) + "\n")
+    print(path)
+
+
+def trace_summary(stats_csv: str, label: str, title: str, command: str, top: int = 25):
+    """profiles/LABEL_kernel_trace.md from rocprofv3's run_kernel_stats.csv: the
+    kernels by total time, with calls and average duration."""
+    import csv
+    import re
+    rows = list(csv.DictReader(open(stats_csv)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    body = [f"# Kernel trace: {title}", "", "Command (repository root, one MI355X):", "", "```",
+            command, "```", "", "The table is `run_kernel_stats.csv` of that run.", "",
+            "| kernel | calls | avg (us) | total (ms) | % |", "|---|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        name = re.sub(r"^void |mfmg::\(anonymous namespace\)::|\(mfmg::.*$|\(.*$", "",
+                      r["Name"])
+        name = name.replace("unsigned short", "bf16")
+        body.append(f"| `{name[:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                    f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.1f} |")
+    path = os.path.join(ROOT, "profiles", f"{label}_kernel_trace.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(body) + "\n")
+    print(path)
+
+
 def desc_of(cfg: W.Config):
     from paper_2505_00793_amd import _lib as M
     if cfg.kind == W.KIND_TRANSFORMER:
@@ -570,6 +638,13 @@ def main():
                     help="write the HBM counter summary of --pmc-class from two rocprofv3 "
                          "--pmc runs (made with --copy-bytes) and exit; no GPU needed")
     ap.add_argument("--pmc-class", default="dual_bwd_weight_gemm_reverse")
+    ap.add_argument("--trace-summary", nargs=3, metavar=("STATS_CSV", "LABEL", "TITLE"),
+                    help="write profiles/LABEL_kernel_trace.md from rocprofv3's kernel stats "
+                         "and exit; no GPU needed")
+    ap.add_argument("--pmc-traffic-summary", nargs=4,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "REGEX", "LABEL"),
+                    help="write profiles/LABEL_hbm_counters.md for the kernels matching REGEX "
+                         "and exit; no GPU needed")
     ap.add_argument("--pmc-mfma-summary", nargs=2, metavar=("CSV", "NAME"),
                     help="write profiles/gemm_mfma_counters_NAME.md from a rocprofv3 --pmc run "
                          "of MfmaUtil and MfmaFlopsBF16 and exit; no GPU needed")
@@ -587,6 +662,13 @@ def main():
     ap.add_argument("--seq", type=int, default=0, choices=[0, *W.C4_LONG_S],
                     help="c4_long_context: time this sequence length and --attention form only")
     args = ap.parse_args()
+    if args.trace_summary:
+        trace_summary(*args.trace_summary, command=args.pmc_command)
+        return
+    if args.pmc_traffic_summary:
+        f_csv, w_csv, rx, label = args.pmc_traffic_summary
+        pmc_traffic_summary(f_csv, w_csv, args.copy_bytes or (1 << 30), rx, label, args.pmc_command)
+        return
     if args.pmc_mfma_summary:
         pmc_mfma_summary(args.pmc_mfma_summary[0], args.pmc_mfma_summary[1], args.pmc_command)
         return
@@ -604,10 +686,6 @@ def main():
     if args.config == "c4_long_context":
         bench_long_context(args)
         return
-    if args.config != W.C5.name:
-        bench_config(args.config, args)
-        return
-
     import torch
     from paper_2505_00793_amd import _lib as M
 
@@ -619,6 +697,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         torch.cuda.empty_cache()
+
+    if args.config != W.C5.name:
+        bench_config(args.config, args)
+        return
 
     cfg = W.C5.with_(T=args.T)
     T = args.T
