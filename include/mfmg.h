@@ -270,6 +270,28 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t problem, const float* theta0, const fl
                            const mfmg_batch* val_batch, float* d_eta_out, float* val_loss_out,
                            size_t* peak_bytes_out, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation and outputs as mfmg_meta_grad, with the workspace taken from a
+ * static scratch array inside the library instead of a caller buffer.  No
+ * device memory is allocated or freed by the call.  Each GPU the library runs
+ * on holds one MFMG_NOALLOC_SCRATCH_BYTES array from the first use of the
+ * library on it until the process ends; its address is looked up on the
+ * first call per device (a HIP runtime query, no allocation).
+ *   Limit: problems whose mfmg_query_sizes(problem, T).workspace_bytes exceeds
+ *   MFMG_NOALLOC_SCRATCH_BYTES are rejected with MFMG_ERR_WORKSPACE before
+ *   anything is enqueued (small MLPs and transformers; not the 8 x 4096 one).
+ *   Every call on one GPU shares its array, whose contents persist between
+ *   calls: calls that overlap in time on one GPU (on different streams or
+ *   threads) race and give undefined results.  Arguments and outputs as for
+ *   mfmg_meta_grad. */
+#define MFMG_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+mfmg_status mfmg_meta_grad_noalloc(mfmg_problem_t problem, const float* theta0,
+                                   const float* opt_state0, const float* eta,
+                                   const mfmg_batch* train_batches, int T,
+                                   const mfmg_batch* val_batch, float* d_eta_out,
+                                   float* val_loss_out, size_t* peak_bytes_out, void* stream);
+
 /* Non-finite check of a result, e.g. d_eta_out of mfmg_meta_grad (whose
  * calls never inspect their outputs: that would need a host synchronisation
  * inside the call).  Counts the NaN and infinite entries of x (dev, n floats)

@@ -20,8 +20,9 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_NUMERIC =
 EXPORTED = [
     "mfmg_problem_create", "mfmg_problem_destroy", "mfmg_query_sizes", "mfmg_inner_step",
     "mfmg_hvp_fwd_over_rev", "mfmg_meta_grad", "mfmg_status_string", "mfmg_last_error_message",
-    "mfmg_timing_enable", "mfmg_timing_read", "mfmg_check_finite",
+    "mfmg_timing_enable", "mfmg_timing_read", "mfmg_check_finite", "mfmg_meta_grad_noalloc",
 ]
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024   # MFMG_NOALLOC_SCRATCH_BYTES
 
 
 class mfmg_problem_desc(ctypes.Structure):
@@ -79,6 +80,9 @@ def lib() -> ctypes.CDLL:
     L.mfmg_meta_grad.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, P(mfmg_batch), c_int,
                                  P(mfmg_batch), c_void_p, c_void_p, P(c_size_t), c_void_p,
                                  c_size_t, c_void_p]
+    L.mfmg_meta_grad_noalloc.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, P(mfmg_batch),
+                                         c_int, P(mfmg_batch), c_void_p, c_void_p, P(c_size_t),
+                                         c_void_p]
     L.mfmg_check_finite.argtypes = [c_void_p, c_size_t, P(c_size_t), c_void_p, c_size_t,
                                     c_void_p]
     L.mfmg_status_string.argtypes = [c_int]
@@ -89,7 +93,7 @@ def lib() -> ctypes.CDLL:
     L.mfmg_timing_read.argtypes = [c_int, P(c_int), P(c_double)]
     for name in ("mfmg_problem_create", "mfmg_query_sizes", "mfmg_inner_step",
                  "mfmg_hvp_fwd_over_rev", "mfmg_meta_grad", "mfmg_timing_enable",
-                 "mfmg_timing_read", "mfmg_check_finite"):
+                 "mfmg_timing_read", "mfmg_check_finite", "mfmg_meta_grad_noalloc"):
         getattr(L, name).restype = c_int
     _lib = L
     return L
@@ -191,6 +195,18 @@ class Problem:
         check(lib().mfmg_meta_grad(self._h, _ptr(theta0), _ptr(opt_state0), _ptr(eta), arr, T,
                                    ctypes.byref(vb), _ptr(d_eta_out), _ptr(val_loss_out),
                                    ctypes.byref(peak), _ptr(ws), ws.numel(), _stream()))
+        return peak.value
+
+    def mfmg_meta_grad_noalloc(self, theta0, opt_state0, eta, xs, ys, vx, vy, d_eta_out,
+                               val_loss_out=None) -> int:
+        """mfmg_meta_grad on the library's static scratch (no workspace); returns peak bytes."""
+        T = len(xs)
+        arr = (mfmg_batch * T)(*[_batch(x, y) for x, y in zip(xs, ys)])
+        vb = _batch(vx, vy)
+        peak = c_size_t(0)
+        check(lib().mfmg_meta_grad_noalloc(self._h, _ptr(theta0), _ptr(opt_state0), _ptr(eta),
+                                           arr, T, ctypes.byref(vb), _ptr(d_eta_out),
+                                           _ptr(val_loss_out), ctypes.byref(peak), _stream()))
         return peak.value
 
 

@@ -1093,6 +1093,33 @@ mfmg_status meta_grad_run(mfmg_problem_t p, const float* theta0, const float* op
                          val_loss_out, (char*)ws, s);
 }
 
+// Scratch of mfmg_meta_grad_noalloc: device memory of the code object, one copy
+// per GPU, held until the process ends.  In host code `scratch` names a
+// host-side stand-in; its device address on the current GPU comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+static __device__ __align__(256) unsigned char scratch[MFMG_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+mfmg_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(MFMG_ERR_UNSUPPORTED, "device index %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    HIPCHK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr || !aligned(ptr, 256))
+      return fail(MFMG_ERR_HIP, "no 256-byte-aligned address for the static scratch");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return MFMG_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1104,6 +1131,24 @@ mfmg_status mfmg_meta_grad(mfmg_problem_t p, const float* theta0, const float* o
   size_t need = 0;
   TRY(check_meta_args(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out, &need));
   TRY(check_ws(ws, ws_bytes, need));
+  return meta_grad_run(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out,
+                       val_loss_out, peak_bytes_out, need, ws, stream);
+}
+
+mfmg_status mfmg_meta_grad_noalloc(mfmg_problem_t p, const float* theta0,
+                                   const float* opt_state0, const float* eta,
+                                   const mfmg_batch* train_batches, int T,
+                                   const mfmg_batch* val_batch, float* d_eta_out,
+                                   float* val_loss_out, size_t* peak_bytes_out, void* stream) {
+  size_t need = 0;
+  TRY(check_meta_args(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out, &need));
+  if (need > (size_t)MFMG_NOALLOC_SCRATCH_BYTES)
+    return fail(MFMG_ERR_WORKSPACE,
+                "this problem needs %zu bytes of scratch at T = %d; the static scratch of "
+                "mfmg_meta_grad_noalloc holds %zu (use mfmg_meta_grad with a workspace)",
+                need, T, (size_t)MFMG_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  TRY(scratch_of_current_device(&ws));
   return meta_grad_run(p, theta0, opt_state0, eta, train_batches, T, val_batch, d_eta_out,
                        val_loss_out, peak_bytes_out, need, ws, stream);
 }

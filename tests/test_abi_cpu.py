@@ -195,6 +195,25 @@ def test_check_finite_validates(L):
     assert n.value == 7   # untouched on a validation error
 
 
+def test_noalloc_rejects_oversized_problems_before_any_device_work(L):
+    """mfmg_meta_grad_noalloc checks the problem's workspace against its static
+    scratch on the host: a problem that needs more is refused with
+    MFMG_ERR_WORKSPACE (fake device pointers, never dereferenced)."""
+    p = M.Problem(desc_of(W.C5))
+    assert p.mfmg_query_sizes(2).workspace_bytes > M.NOALLOC_SCRATCH_BYTES
+    b = (M.mfmg_batch * 2)(*[M.mfmg_batch(FAKE, FAKE, W.C5.rows) for _ in range(2)])
+    vb = M.mfmg_batch(FAKE, FAKE, W.C5.val_rows)
+    peak = ctypes.c_size_t(0)
+    st = L.mfmg_meta_grad_noalloc(p.handle, ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), b,
+                                  2, ctypes.byref(vb), ctypes.c_void_p(FAKE), None,
+                                  ctypes.byref(peak), None)
+    assert st == M.ERR_WORKSPACE
+    assert b"static scratch" in L.mfmg_last_error_message()
+    assert L.mfmg_meta_grad_noalloc(p.handle, ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE),
+                                    b, 0, ctypes.byref(vb), ctypes.c_void_p(FAKE), None,
+                                    ctypes.byref(peak), None) == M.ERR_INVALID_ARGUMENT
+
+
 def test_block_remat_dynamic_memory_flat_in_depth():
     """With block rematerialisation the transformer's dynamic bytes grow with the
     number of blocks only by the kept block inputs (the residual stream and its
