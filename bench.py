@@ -261,10 +261,10 @@ def pmc_mfma_summary(csv_path: str, out_name: str, command: str):
             "|---|---:|---:|---:|---:|---:|"]
     for name, k in rows:
         short = re.sub(r"^void |\(mfmg::GemmOperands.*$|mfmg::\(anonymous namespace\)::", "", name)
-        short = re.sub(r"<unsigned short>|unsigned short", "bf16", short)[:110]
+        short = short.replace("unsigned short", "bf16")[:110]
         us = k["ns"] / k["n"] / 1e3 if k["ns"] else float("nan")
         gf = k["flops"] / k["n"] / 1e9
-        tf = gf / us * 1e-3 if k["ns"] else float("nan")
+        tf = gf / us * 1e3 if k["ns"] else float("nan")   # GFLOP per us = PFLOP/s
         body.append(f"| `{short}` | {k['n']} | {k['util'] / k['n']:.1f} | {gf:.2f} | {us:.1f} | "
                     f"{tf:.0f} |")
     path = os.path.join(ROOT, "profiles", f"gemm_mfma_counters_{out_name}.md")
@@ -377,15 +377,35 @@ def cpu_model() -> str:
     return "unknown"
 
 
+def oracle_meta_grad_logged(cfg: W.Config, inp: dict):
+    """oracle.meta_grad_checkpointed, step by step through the oracle's own
+    functions, logging each step (a whole float64 meta-gradient of the large
+    workloads takes minutes on the host)."""
+    import torch
+    from oracle.metagrad import _Inputs, reverse_step, seed, unroll
+    I = _Inputs(cfg, inp)
+    thetas, opts, _, _ = unroll(cfg, inp)
+    log(f"[bench]   oracle: forward unroll of {I.T} steps done")
+    V, thbar = seed(cfg, I, thetas[-1], False)
+    obar = None if opts[-1] is None else torch.zeros_like(opts[-1])
+    etabar = torch.zeros_like(I.eta)
+    for i in reversed(range(I.T)):
+        thbar, obar, d = reverse_step(cfg, I, i, thetas[i], opts[i], thbar, obar, False)
+        etabar = etabar + d
+        log(f"[bench]   oracle: reverse step {i} done")
+    if cfg.meta == W.META_MAML:
+        etabar = etabar + thbar
+    return etabar.numpy(), float(V.detach())
+
+
 def cpu_baseline(cfg: W.Config, inp: dict, runs: int = 1):
     """The float64 reverse-over-reverse oracle (step-checkpointed) on the host
     cores: `runs` whole meta-gradients of the workload, timed; 1 / median."""
     import torch
-    import oracle
     times = []
     for _ in range(runs):
         t0 = time.perf_counter()
-        oracle.meta_grad_checkpointed(cfg, inp)
+        oracle_meta_grad_logged(cfg, inp)
         times.append(time.perf_counter() - t0)
     med = sorted(times)[len(times) // 2]
     return {"value": 1.0 / med, "unit": "meta-gradients/s", "cores": torch.get_num_threads(),
