@@ -156,15 +156,18 @@ typedef struct {
   int d_model, n_heads, d_ff, vocab, seq, n_blocks, meta_hidden;
   float ln_eps, rope_base;
   int map_steps;                       /* MFMG_LOSS_MAPMSE: M, 1..1024 */
-  /* Static-memory reduction for SGD (MLP kind): 0 keeps the operand
-   * checkpoint of every theta_t (memory linear in T).  k >= 1 keeps float32
-   * theta only at t = k, 2k, .. and a ring of k + 1 operand checkpoints, and
+  /* Static-memory reduction (MLP kind): 0 keeps the checkpoint of every
+   * theta_t (memory linear in T).  k >= 1 keeps float32 theta (and Adam's m
+   * and v) only at t = k, 2k, .. and a ring of k + 1 states (operand copies;
+   * for Adam also float32 theta, m, v and k saved inner gradients), and
    * recomputes each segment's states (the same kernels on the same inputs, so
    * the result is bit-identical) when the reverse sweep enters it: static
    * memory ~ (T/k + k) parameter copies, one extra forward inner step per
-   * recomputed state.  A two-level form of the rematerialisation schedules
-   * the appendix on static device memory proposes (whose logarithmic form
-   * needs a recursive schedule).  Ignored for Adam and when k >= T. */
+   * recomputed state (Adam: per state of the segment, since the gradient of
+   * its last step is read before that step's dual pass).  A two-level form of
+   * the rematerialisation schedules the appendix on static device memory
+   * proposes (whose logarithmic form needs a recursive schedule).  Ignored
+   * when k >= T. */
   int ckpt_segment;
   /* Transformer kind only.  0 materialises each block's attention
    * probabilities P and their tangent (B*H*S^2 per block, kept from the

@@ -162,10 +162,13 @@ struct MetaPlan {
   int seg;                          // 0, or the segment length k of recomputed checkpoints
   std::vector<OperandSet<T>> slot;  // T + 1 operand checkpoints, or a ring of k + 1
   std::vector<float*> ck;           // segments: theta_{s k} (float32), s = 1 .. ceil(T/k) - 1
+  std::vector<float*> ckm, ckv;     // segments, Adam: m_{s k}, v_{s k}
   float* run[2];                    // SGD: theta_{t+1} (float32), ping-pong
   float* thetabar;
   OperandSet<T> v[2];               // tangent operand copies, ping-pong
-  std::vector<float*> th, m, vv, g; // Adam checkpoints: theta_t, m_t, v_t (t = 0..T), g_t
+  // Adam checkpoints: theta_t, m_t, v_t (t = 0..T) and g_t (t < T); with
+  // segments a ring of k + 1 states and k gradients (see the *_at helpers)
+  std::vector<float*> th, m, vv, g;
   float* mbar;
   float* vbar;
   float* partial;
@@ -183,10 +186,10 @@ int adam_blocks(const mfmg_problem* p, int l) {
 }
 
 // Segment length of the recomputed checkpoints for T inner steps (0: every
-// step's operands are kept).  SGD only: Adam's reverse step reads m_t, v_t, g_t.
+// step's state is kept).
 int seg_of(const mfmg_problem* p, int T) {
   const int k = p->d.ckpt_segment;
-  return (k > 0 && k < T && !p->adam()) ? k : 0;
+  return (k > 0 && k < T) ? k : 0;
 }
 
 template <typename T>
@@ -206,10 +209,20 @@ void plan_meta(const mfmg_problem* p, int T_, char* base, MetaPlan<T>& mp) {
   mp.slot.resize(nslot);
   for (int t = 0; t < nslot; ++t) carve_opset(p, c, mp.slot[t]);
   mp.ck.clear();
+  mp.ckm.clear();
+  mp.ckv.clear();
   if (mp.seg) {
     const int nseg = (T_ + mp.seg - 1) / mp.seg;
     mp.ck.assign(nseg, nullptr);
     for (int q = 1; q < nseg; ++q) mp.ck[q] = c.take<float>(n);
+    if (p->adam()) {
+      mp.ckm.assign(nseg, nullptr);
+      mp.ckv.assign(nseg, nullptr);
+      for (int q = 1; q < nseg; ++q) {
+        mp.ckm[q] = c.take<float>(n);
+        mp.ckv[q] = c.take<float>(n);
+      }
+    }
   }
   mp.run[0] = mp.run[1] = nullptr;
   if (!p->adam()) {
@@ -221,16 +234,20 @@ void plan_meta(const mfmg_problem* p, int T_, char* base, MetaPlan<T>& mp) {
   if (!p->adam()) carve_opset(p, c, mp.v[1]);
   mp.mbar = mp.vbar = mp.partial = nullptr;
   if (p->adam()) {
-    mp.th.assign(T_ + 1, nullptr);
-    mp.m.assign(T_ + 1, nullptr);
-    mp.vv.assign(T_ + 1, nullptr);
-    mp.g.assign(T_, nullptr);
-    for (int t = 1; t <= T_; ++t) mp.th[t] = c.take<float>(n);
-    for (int t = 0; t <= T_; ++t) {
+    // states t = 0..T (theta_0 is the caller's), or a ring of k + 1 states and
+    // k gradients with segments
+    const int ns = mp.seg ? mp.seg + 1 : T_ + 1;
+    const int ng = mp.seg ? mp.seg : T_;
+    mp.th.assign(ns, nullptr);
+    mp.m.assign(ns, nullptr);
+    mp.vv.assign(ns, nullptr);
+    mp.g.assign(ng, nullptr);
+    for (int t = mp.seg ? 0 : 1; t < ns; ++t) mp.th[t] = c.take<float>(n);
+    for (int t = 0; t < ns; ++t) {
       mp.m[t] = c.take<float>(n);
       mp.vv[t] = c.take<float>(n);
     }
-    for (int t = 0; t < T_; ++t) mp.g[t] = c.take<float>(n);
+    for (int t = 0; t < ng; ++t) mp.g[t] = c.take<float>(n);
     mp.mbar = c.take<float>(n);
     mp.vbar = c.take<float>(n);
     int off = 0;
@@ -505,20 +522,30 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
 
   // Operand checkpoint of theta_t: slot t, or with segments the ring entry
   // t mod (k + 1), which holds one segment's states plus theta_T at once.
+  // Adam's float32 states (theta_t, m_t, v_t) use the same ring, its saved
+  // gradients g_t the ring t mod k.
   const int k = mp.seg;
   auto sl = [&](int t) -> const OperandSet<T>& { return mp.slot[k ? t % (k + 1) : t]; };
+  auto st_of = [&](int t) { return k ? t % (k + 1) : t; };
+  auto th_at = [&](int t) -> float* {
+    return t == 0 ? const_cast<float*>(theta0) : mp.th[st_of(t)];
+  };
+  auto g_at = [&](int t) -> float* { return mp.g[k ? t % k : t]; };
+  // Adam: m_0, v_0 into state t (the optimiser state at the start)
+  auto adam_init = [&](int t) -> mfmg_status {
+    if (opt0) {
+      HIPCHK(copy(opt0, mp.m[st_of(t)], n, s));
+      HIPCHK(copy(opt0 + n, mp.vv[st_of(t)], n, s));
+    } else {
+      HIPCHK(fill(mp.m[st_of(t)], n, 0.0f, s));
+      HIPCHK(fill(mp.vv[st_of(t)], n, 0.0f, s));
+    }
+    return MFMG_OK;
+  };
 
   // prologue
   TRY(E.to_ops(theta0, sl(0)));
-  if (adam) {
-    if (opt0) {
-      HIPCHK(copy(opt0, mp.m[0], n, s));
-      HIPCHK(copy(opt0 + n, mp.vv[0], n, s));
-    } else {
-      HIPCHK(fill(mp.m[0], n, 0.0f, s));
-      HIPCHK(fill(mp.vv[0], n, 0.0f, s));
-    }
-  }
+  if (adam) TRY(adam_init(0));
 
   // One forward inner step t from the float32 theta_t at th: the update writes
   // theta_{t+1} to th_next and its operand copies to checkpoint t + 1.
@@ -529,13 +556,13 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
     TRY(E.head(batches[t], R, false, alpha, nullptr, nullptr, a));
     ParamArgs<T> P = param_base<T>(p, mode_of(p, 0), eta);
     if (adam) {
-      P.theta = t == 0 ? theta0 : mp.th[t];
-      P.theta_next = mp.th[t + 1];
-      P.m_in = mp.m[t];
-      P.v_in = mp.vv[t];
-      P.m_out = mp.m[t + 1];
-      P.v_out = mp.vv[t + 1];
-      P.g_save = mp.g[t];
+      P.theta = th_at(t);
+      P.theta_next = th_at(t + 1);
+      P.m_in = mp.m[st_of(t)];
+      P.v_in = mp.vv[st_of(t)];
+      P.m_out = mp.m[st_of(t + 1)];
+      P.v_out = mp.vv[st_of(t + 1)];
+      P.g_save = g_at(t);
       bias_corr(p, t, &P.k1, &P.k2);
     } else {
       P.theta = th;
@@ -555,7 +582,8 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
   // start goes to its float32 checkpoint instead.
   auto other = [&](const float* th) { return th == mp.run[0] ? mp.run[1] : mp.run[0]; };
 
-  // forward unroll with checkpoints
+  // forward unroll with checkpoints (with segments, Adam copies the state at
+  // each segment start out of the ring)
   {
     const float* th = theta0;
     for (int t = 0; t < T_; ++t) {
@@ -563,6 +591,12 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
       if (!adam) nx = (k && (t + 1) % k == 0 && t + 1 < T_) ? mp.ck[(t + 1) / k] : other(th);
       TRY(fwd_step(t, th, nx));
       th = nx;
+      if (adam && k && (t + 1) % k == 0 && t + 1 < T_) {
+        const int q = (t + 1) / k, r = st_of(t + 1);
+        HIPCHK(copy(mp.th[r], mp.ck[q], n, s));
+        HIPCHK(copy(mp.m[r], mp.ckm[q], n, s));
+        HIPCHK(copy(mp.vv[r], mp.ckv[q], n, s));
+      }
     }
   }
 
@@ -596,12 +630,27 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
     // inputs, so the operand copies are bit-identical to the unroll's)
     if (k && (i + 1) % k == 0 && i + 1 < T_) {
       const int s0 = i + 1 - k;
-      const float* th = s0 == 0 ? theta0 : mp.ck[s0 / k];
-      TRY(E.to_ops(th, sl(s0)));
-      for (int t = s0; t < i; ++t) {
-        float* nx = other(th);
-        TRY(fwd_step(t, th, nx));
-        th = nx;
+      if (adam) {
+        // the segment's start state back into the ring, then its steps s0..i
+        // (step i too: its inner gradient is read before the dual pass)
+        if (s0 == 0) {
+          TRY(adam_init(0));
+        } else {
+          const int r = st_of(s0), q = s0 / k;
+          HIPCHK(copy(mp.ck[q], mp.th[r], n, s));
+          HIPCHK(copy(mp.ckm[q], mp.m[r], n, s));
+          HIPCHK(copy(mp.ckv[q], mp.vv[r], n, s));
+        }
+        TRY(E.to_ops(th_at(s0), sl(s0)));
+        for (int t = s0; t <= i; ++t) TRY(fwd_step(t, nullptr, nullptr));
+      } else {
+        const float* th = s0 == 0 ? theta0 : mp.ck[s0 / k];
+        TRY(E.to_ops(th, sl(s0)));
+        for (int t = s0; t < i; ++t) {
+          float* nx = other(th);
+          TRY(fwd_step(t, th, nx));
+          th = nx;
+        }
       }
     }
     if (adam) {
@@ -622,10 +671,10 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
         A.k1 = k1;
         A.k2 = k2;
         A.eta = eta;
-        A.theta = i == 0 ? theta0 : mp.th[i];
-        A.m = mp.m[i];
-        A.v = mp.vv[i];
-        A.g = mp.g[i];
+        A.theta = th_at(i);
+        A.m = mp.m[st_of(i)];
+        A.v = mp.vv[st_of(i)];
+        A.g = g_at(i);
         A.thetabar = mp.thetabar;
         A.mbar = mp.mbar;
         A.vbar = mp.vbar;

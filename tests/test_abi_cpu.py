@@ -117,6 +117,16 @@ def test_segment_checkpoints_shrink_static_memory():
     # 32 + 1 operand checkpoints (4 B per weight) against 6 + 1 and 5 float32 thetas
     saved = full.static_bytes - seg.static_bytes
     assert abs(saved - (26 * 4 * n - 5 * 4 * n)) < 0.01 * saved
+    # Adam (c3) at T = 16, bytes per parameter: every step kept = 17 operand
+    # checkpoints (4) + theta_1..16 (4) + m, v for 17 states (8) + 16 gradients (4)
+    # = 332; segments of 4 = a ring of 5 operand checkpoints, theta, m, v (16 each)
+    # + 4 gradients (4) + theta, m, v at 3 segment starts (12) = 132
+    full = M.Problem(desc_of(W.C3)).mfmg_query_sizes(16)
+    seg = M.Problem(desc_of(W.C3.with_(ckpt_segment=4))).mfmg_query_sizes(16)
+    n = W.n_theta(W.C3)
+    assert full.dynamic_bytes == seg.dynamic_bytes
+    saved = full.static_bytes - seg.static_bytes
+    assert abs(saved - (332 - 132) * n) < 0.01 * saved
 
 
 def test_fused_attention_drops_quadratic_buffers():
