@@ -554,16 +554,17 @@ __global__ void __launch_bounds__(1024) adam_reduce_kernel(const float* __restri
 // validation batch.  Forward unroll with theta_t checkpoints, then the
 // reverse sweep with the dual pass (r, rdot) = (X theta - y, X v):
 // g = (2/N) X^T r, H v = (2/N) X^T rdot.
-// 1024 threads; each batch is staged in LDS (when it fits in 64 KB) with
-// 16-byte loads, residuals take one wave per row (lanes over the features,
-// wave reductions), and X^T r takes 64 features x 16 row groups per pass with
-// an ordered sum of the 16 partials.
+// 1024 threads; each batch is staged in LDS (when it fits in 64 KB) with rows
+// padded to d + 1 floats, residuals take one thread per row (a serial dot
+// product over the features: the padding keeps the threads of a wave on
+// distinct banks), and X^T r takes 64 features x 16 row groups per pass with an
+// ordered sum of the 16 partials.
 // ------------------------------------------------------------------------------------
 constexpr int LR_MAXD = 256;
 constexpr int LR_MAXR = 1024;
 constexpr int LR_MAXT = 64;
 constexpr int LR_THREADS = 1024;
-constexpr int LR_STAGE = 16384;  // floats of one batch staged in LDS (64 KB)
+constexpr int LR_STAGE = 16640;  // floats of one batch staged in LDS, rows padded (65 KB)
 
 struct LinregArgs {
   const float* theta0;
@@ -578,43 +579,48 @@ struct LinregArgs {
   float* ckpt;  // (T + 1) x d
 };
 
-// X rows x d (row-major) into LDS when it fits, else left in global memory.
-__device__ const float* lr_stage(const float* X, int rows, int d, float* stage) {
+// Row stride of a staged batch (padded), or of the batch in global memory.
+__device__ __forceinline__ int lr_pitch(int rows, int d) {
+  return rows * (d + 1) <= LR_STAGE ? d + 1 : d;
+}
+
+// X rows x d (row-major) into LDS with rows padded to d + 1 floats when it fits
+// (else left in global memory), and the targets y into ys.
+__device__ const float* lr_stage(const float* X, const float* __restrict__ y, int rows, int d,
+                                 float* stage, float* ys) {
   const int n = rows * d;
-  if (n > LR_STAGE) return X;
   __syncthreads();  // the previous batch's readers are done
-  if ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0) {
-    const float4* X4 = reinterpret_cast<const float4*>(X);
-    float4* S4 = reinterpret_cast<float4*>(stage);
-    for (int i = threadIdx.x; i < n / 4; i += LR_THREADS) S4[i] = X4[i];
-  } else {
-    for (int i = threadIdx.x; i < n; i += LR_THREADS) stage[i] = X[i];
+  for (int i = threadIdx.x; i < rows; i += LR_THREADS) ys[i] = y[i];
+  if (lr_pitch(rows, d) == d) {
+    __syncthreads();
+    return X;
+  }
+  for (int i = threadIdx.x; i < n; i += LR_THREADS) {
+    const int row = i / d;
+    stage[i + row] = X[i];   // row * (d + 1) + (i - row * d)
   }
   __syncthreads();
   return stage;
 }
 
-// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when u): one wave per row.
-// Returns this thread's share of sum_n r[n]^2 (lane 0 of each wave).
-__device__ float lr_rows(const float* X, const float* __restrict__ y, const float* w,
+// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when u): one thread per row.
+// Returns this thread's share of sum_n r[n]^2.
+__device__ float lr_rows(const float* X, const float* y, const float* w,
                          const float* u, int rows, int d, float* r, float* rd) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int pitch = lr_pitch(rows, d);
   float sq = 0.0f;
-  for (int n = wave; n < rows; n += LR_THREADS / 64) {
+  for (int n = threadIdx.x; n < rows; n += LR_THREADS) {
+    const float* xr = X + n * pitch;
     float s = 0.0f, sd = 0.0f;
-    for (int j = lane; j < d; j += 64) {
-      const float x = X[n * d + j];
+    for (int j = 0; j < d; ++j) {
+      const float x = xr[j];
       s += x * w[j];
       if (u) sd += x * u[j];
     }
-    s = wave_sum(s);
-    if (u) sd = wave_sum(sd);
-    if (lane == 0) {
-      const float res = s - y[n];
-      r[n] = res;
-      if (u) rd[n] = sd;
-      sq += res * res;
-    }
+    const float res = s - y[n];
+    r[n] = res;
+    if (u) rd[n] = sd;
+    sq += res * res;
   }
   __syncthreads();
   return sq;
@@ -624,12 +630,13 @@ __device__ float lr_rows(const float* X, const float* __restrict__ y, const floa
 __device__ void lr_cols(const float* X, const float* v, const float* v2, int rows, int d,
                         float* part, float* part2, float* out, float* out2) {
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int pitch = lr_pitch(rows, d);
   for (int j0 = 0; j0 < d; j0 += 64) {
     const int j = j0 + c;
     float s = 0.0f, s2 = 0.0f;
     if (j < d) {
       for (int n = q; n < rows; n += 16) {
-        const float x = X[n * d + j];
+        const float x = X[n * pitch + j];
         s += x * v[n];
         if (v2) s2 += x * v2[n];
       }
@@ -654,7 +661,7 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __shared__ __attribute__((aligned(16))) float stage[LR_STAGE];
   __shared__ float th[LR_MAXD], tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD], vv[LR_MAXD];
   __shared__ float gs[LR_MAXD], hs[LR_MAXD];
-  __shared__ float r[LR_MAXR], rd[LR_MAXR];
+  __shared__ float r[LR_MAXR], rd[LR_MAXR], ys[LR_MAXR];
   __shared__ float part[16 * 64], part2[16 * 64];
   __shared__ float red[LR_THREADS / 64];
   const int tid = threadIdx.x, d = a.d;
@@ -667,9 +674,9 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __syncthreads();
   // forward unroll
   for (int t = 0; t < a.T; ++t) {
-    const float* X = lr_stage(a.xs[t], a.rows, d, stage);
+    const float* X = lr_stage(a.xs[t], a.ys[t], a.rows, d, stage, ys);
     const float inv = 2.0f / a.rows;
-    lr_rows(X, a.ys[t], th, nullptr, a.rows, d, r, nullptr);
+    lr_rows(X, ys, th, nullptr, a.rows, d, r, nullptr);
     lr_cols(X, r, nullptr, a.rows, d, part, nullptr, gs, nullptr);
     for (int j = tid; j < d; j += LR_THREADS) {
       th[j] -= lam[j] * inv * gs[j];
@@ -679,9 +686,9 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   }
   // validation loss and its gradient (the seed of the reverse sweep)
   {
-    const float* X = lr_stage(a.vx, a.vrows, d, stage);
+    const float* X = lr_stage(a.vx, a.vy, a.vrows, d, stage, ys);
     const float inv = 2.0f / a.vrows;
-    const float sq = lr_rows(X, a.vy, th, nullptr, a.vrows, d, r, nullptr);
+    const float sq = wave_sum(lr_rows(X, ys, th, nullptr, a.vrows, d, r, nullptr));
     if ((tid & 63) == 0) red[tid >> 6] = sq;
     lr_cols(X, r, nullptr, a.vrows, d, part, nullptr, gs, nullptr);
     if (tid == 0 && a.val_loss) {
@@ -700,9 +707,8 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
       th[j] = a.ckpt[(long)i * d + j];
       vv[j] = -lam[j] * tb[j];
     }
-    const float* X = lr_stage(a.xs[i], a.rows, d, stage);  // its barriers publish th, vv
-    if (a.rows * d > LR_STAGE) __syncthreads();
-    lr_rows(X, a.ys[i], th, vv, a.rows, d, r, rd);
+    const float* X = lr_stage(a.xs[i], a.ys[i], a.rows, d, stage, ys);  // publishes th, vv
+    lr_rows(X, ys, th, vv, a.rows, d, r, rd);
     lr_cols(X, r, rd, a.rows, d, part, part2, gs, hs);
     for (int j = tid; j < d; j += LR_THREADS) {
       eb[j] += -lam[j] * inv * gs[j] * tb[j];
