@@ -334,15 +334,17 @@ def test_meta_grad_parity_full_size_bf16(name, T):
     assert abs(V - Vref) <= tol_of(cfg) * abs(Vref)
 
 
-def test_meta_grad_parity_full_size_fp32_gelu():
+@pytest.mark.parametrize("T", [2, 8])
+def test_meta_grad_parity_full_size_fp32_gelu(T):
     """The full 8 x 4096 network and every kernel shape of the bf16 workload, with a
     smooth activation (GELU) and float32 operands, against the unrounded float64
-    oracle at the float32 tolerance.  (With ReLU, float32 and float64 already put
-    a handful of near-zero pre-activations on different sides of the kink, which
-    moves whole gradient columns by ~1e-3 at this width.)"""
-    cfg = W.C5.with_(T=2, precision=W.PREC_FP32, act=W.ACT_GELU)
-    inp = W.make_inputs(cfg, T=2)
-    print("\n[meta_grad full fp32] 8 x 4096 GELU T=2", flush=True)
+    oracle at the float32 tolerance, at T=2 and at the bench's T=8.  (With ReLU,
+    float32 and float64 already put a handful of near-zero pre-activations on
+    different sides of the kink, which moves whole gradient columns by ~1e-3 at
+    this width.)"""
+    cfg = W.C5.with_(T=T, precision=W.PREC_FP32, act=W.ACT_GELU)
+    inp = W.make_inputs(cfg, T=T)
+    print(f"\n[meta_grad full fp32] 8 x 4096 GELU T={T}", flush=True)
     got, V, peak = run_meta(cfg, inp)
     ref, Vref = oracle.meta_grad_checkpointed(cfg, inp)
     err = relerr(got, ref)
