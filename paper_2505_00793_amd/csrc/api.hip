@@ -422,36 +422,30 @@ struct Eng {
       P.ldW = (int)p->ld(nout);
       P.ldWT = (int)p->ld(nin);
       set_out(P, l);
-      {
-        GemmOperands<T> op;
-        op.A = l == 0 ? a.XT : a.AT[l - 1];
-        op.Ad = (dual && l > 0) ? a.AdT[l - 1] : nullptr;
-        op.B = a.dZT[cur];
-        op.Bd = dual ? a.dZdT[cur] : nullptr;
-        op.lda = op.ldb = (int)p->ld(R);
-        op.M = nin;
-        op.N = nout;
-        op.K = R;
-        const int flags = (need_c1 ? G_C1 : 0) | (dual ? (G_BD | (l > 0 ? G_AD : 0)) : 0);
-        TimingScope ts(dual ? (flags == (G_C1 | G_AD | G_BD) ? 8 : 5) : 2, s);
-        HIPCHK(gemm_param<T>(op, flags, P, s));
-      }
-      if (p->d.has_bias) {
-        TimingScope ts(7, s);
-        HIPCHK(bias_reduce<T>(a.dZT[cur], dual ? a.dZdT[cur] : nullptr, (int)p->ld(R), R, P, s));
-      }
+      // backward-weight product G = A^T dZ (and its tangent), parameter epilogue
+      GemmOperands<T> opw;
+      opw.A = l == 0 ? a.XT : a.AT[l - 1];
+      opw.Ad = (dual && l > 0) ? a.AdT[l - 1] : nullptr;
+      opw.B = a.dZT[cur];
+      opw.Bd = dual ? a.dZdT[cur] : nullptr;
+      opw.lda = opw.ldb = (int)p->ld(R);
+      opw.M = nin;
+      opw.N = nout;
+      opw.K = R;
+      const int flags_w = (need_c1 ? G_C1 : 0) | (dual ? (G_BD | (l > 0 ? G_AD : 0)) : 0);
+      // backward-data product dA = dZ W^T (and its tangent), activation epilogue
+      GemmOperands<T> opd;
+      EpiActBwd<T> e;
+      const int flags_d = G_C1 | (dual ? (G_AD | G_BD) : 0);
       if (l > 0) {
-        GemmOperands<T> op;
-        op.A = a.dZ[cur];
-        op.Ad = dual ? a.dZd[cur] : nullptr;
-        op.B = th.W[l];
-        op.Bd = dual ? v->W[l] : nullptr;
-        op.lda = op.ldb = (int)p->ld(nout);
-        op.M = R;
-        op.N = nin;
-        op.K = nout;
-        const int flags = G_C1 | (dual ? (G_AD | G_BD) : 0);
-        EpiActBwd<T> e;
+        opd.A = a.dZ[cur];
+        opd.Ad = dual ? a.dZd[cur] : nullptr;
+        opd.B = th.W[l];
+        opd.Bd = dual ? v->W[l] : nullptr;
+        opd.lda = opd.ldb = (int)p->ld(nout);
+        opd.M = R;
+        opd.N = nin;
+        opd.K = nout;
         e.Zp = a.Z[l - 1];
         e.Zdp = a.Zd[l - 1];
         e.act = p->d.act;
@@ -464,8 +458,25 @@ struct Eng {
         e.dZdT = a.dZdT[cur ^ 1];
         e.ld = (int)p->ld(nin);
         e.ldT = (int)p->ld(R);
-        TimingScope ts(dual ? 4 : 1, s);
-        HIPCHK(gemm_act_bwd<T>(op, flags, e, s));
+      }
+      // the two products are independent: small ones share one launch
+      const bool paired = l > 0 && gemm_pairs<T>(opw, flags_w, opd, flags_d);
+      if (paired) {
+        TimingScope ts(dual ? 8 : 2, s);
+        HIPCHK(gemm_param_and_act_bwd<T>(opw, flags_w, P, opd, flags_d, e, s));
+      } else {
+        TimingScope ts(dual ? (flags_w == (G_C1 | G_AD | G_BD) ? 8 : 5) : 2, s);
+        HIPCHK(gemm_param<T>(opw, flags_w, P, s));
+      }
+      if (p->d.has_bias) {
+        TimingScope ts(7, s);
+        HIPCHK(bias_reduce<T>(a.dZT[cur], dual ? a.dZdT[cur] : nullptr, (int)p->ld(R), R, P, s));
+      }
+      if (l > 0) {
+        if (!paired) {
+          TimingScope ts(dual ? 4 : 1, s);
+          HIPCHK(gemm_act_bwd<T>(opd, flags_d, e, s));
+        }
         cur ^= 1;
       }
     }

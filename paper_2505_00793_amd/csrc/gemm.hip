@@ -355,11 +355,10 @@ struct Smem {
 // each XCD a contiguous range of tiles, then walk tiles in groups of 8 tile
 // rows so that neighbouring tiles share A and B panels in that XCD's L2.
 template <int BM, int BN>
-__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
+__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0, int pid) {
   const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = (N + BN - 1) / BN;
   const int nt = tiles_m * tiles_n;
-  int pid = blockIdx.x;
   if ((nt & 7) == 0) pid = (pid & 7) * (nt >> 3) + (pid >> 3);
   constexpr int GM = 8;
   const int group = pid / (GM * tiles_n);
@@ -368,6 +367,10 @@ __device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
   const int within = pid - group * GM * tiles_n;
   m0 = (first_m + within % gsz) * BM;
   n0 = (within / gsz) * BN;
+}
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
+  tile_origin<BM, BN>(M, N, m0, n0, (int)blockIdx.x);
 }
 
 // Position of element (row, col) in the epilogue staging buffer: rows padded
@@ -764,7 +767,8 @@ struct DmaTile {
 // eight waves meet at one barrier per k step and all of them walk the epilogue.
 // ------------------------------------------------------------------------------------
 template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
-__global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi epi) {
+__device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, const Epi& epi,
+                                             int pid, int bz, char* smem) {
   typedef DmaSmem<FLAGS, BM, BN, BK, NST, 1> SM;
   constexpr bool HC1 = (FLAGS & G_C1) != 0;
   constexpr bool HAD = (FLAGS & G_AD) != 0;
@@ -776,7 +780,6 @@ __global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi e
   constexpr int NCH = CPR / 4;
   static_assert(NST >= 2 && SM::LPW * (NST - 2) < 64, "pipeline depth");
 
-  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   float* S1 = reinterpret_cast<float*>(smem);
   float* S2 = S1 + BM * Stage<BN>::SLD;
 
@@ -784,8 +787,7 @@ __global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi e
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int m0, n0;
-  tile_origin<BM, BN>(op.M, op.N, m0, n0);
-  const int bz = blockIdx.y;
+  tile_origin<BM, BN>(op.M, op.N, m0, n0, pid);
   const int K = op.K;
   const int nk = (K + BK - 1) / BK;
 
@@ -882,6 +884,45 @@ __global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi e
     lds_barrier();
   }
   walk_tile<FLAGS, BN, BM, 512>(S1, S2, m0, n0, bz, epi);
+}
+
+template <int FLAGS, int BM, int BN, int BK, int NST, class Epi>
+__global__ void __launch_bounds__(512) gemm_nt_ws(GemmOperands<bf16_t> op, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) char smem[DmaSmem<FLAGS, BM, BN, BK, NST, 1>::BYTES];
+  gemm_ws_tile<FLAGS, BM, BN, BK, NST, Epi>(op, epi, (int)blockIdx.x, (int)blockIdx.y, smem);
+}
+
+// Two independent products in one launch, for products too small to fill the
+// chip alone (at most two workgroups per compute unit between them): a layer's
+// backward-weight product (parameter epilogue) and its backward-data product
+// (activation epilogue).  Workgroup ids alternate between runs of G1 tiles of
+// the first product and G2 of the second, so both run at once.
+template <int F1, int BM1, int BN1, int NST1, class E1, int F2, int BM2, int BN2, int NST2,
+          class E2>
+__global__ void __launch_bounds__(512) gemm_pair_ws(GemmOperands<bf16_t> op1, E1 epi1, int t1,
+                                                    int g1, GemmOperands<bf16_t> op2, E2 epi2,
+                                                    int t2, int g2) {
+  constexpr int B1 = DmaSmem<F1, BM1, BN1, 64, NST1, 1>::BYTES;
+  constexpr int B2 = DmaSmem<F2, BM2, BN2, 64, NST2, 1>::BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[B1 > B2 ? B1 : B2];
+  const int b = (int)blockIdx.x;
+  const int period = g1 + g2;
+  const int cyc = min(t1 / g1, t2 / g2);
+  int which, j;
+  if (b < cyc * period) {
+    const int q = b / period, r = b % period;
+    which = r < g1 ? 0 : 1;
+    j = which == 0 ? q * g1 + r : q * g2 + (r - g1);
+  } else {
+    const int r = b - cyc * period;
+    const int rest1 = t1 - cyc * g1;
+    which = r < rest1 ? 0 : 1;
+    j = which == 0 ? cyc * g1 + r : cyc * g2 + (r - rest1);
+  }
+  if (which == 0)
+    gemm_ws_tile<F1, BM1, BN1, 64, NST1, E1>(op1, epi1, j, 0, smem);
+  else
+    gemm_ws_tile<F2, BM2, BN2, 64, NST2, E2>(op2, epi2, j, 0, smem);
 }
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -1105,7 +1146,86 @@ hipError_t dispatch(const GemmOperands<T>& op, int flags, const Epi& epi, hipStr
   }
 }
 
+// The tile launch_sized picks for a bf16 product on the direct-to-LDS path:
+// 0 = 128 x 128, 1 = 128 x 64, 2 = 64 x 64, 3 = 64 x 32; -1 when it would not take
+// that path (float32, ragged k or strides, several batches, split-K).
+template <typename T>
+int dma_tile_kind(const GemmOperands<T>& o) {
+  if (sizeof(T) != 2 || o.batch != 1 || o.M <= 0 || o.N <= 0 || !dma_ok(o)) return -1;
+  if (o.ws && splitk_count(o.M, o.N, o.K) > 1) return -1;
+  if (cdiv(o.M, 128) * cdiv(o.N, 128) >= 192) return 0;
+  if (cdiv(o.M, 128) * cdiv(o.N, 64) >= 192) return 1;
+  if (cdiv(o.M, 64) * cdiv(o.N, 64) >= 192) return 2;
+  return 3;
+}
+
+template <int F1, int BM1, int BN1, class E1, int F2, int BM2, int BN2, class E2>
+hipError_t launch_pair(const GemmOperands<bf16_t>& o1, const E1& e1,
+                       const GemmOperands<bf16_t>& o2, const E2& e2, hipStream_t s) {
+  const int t1 = cdiv(o1.M, BM1) * cdiv(o1.N, BN1);
+  const int t2 = cdiv(o2.M, BM2) * cdiv(o2.N, BN2);
+  // runs of 8 tiles of the smaller product and about 8 x the ratio of the larger
+  int g1 = 8, g2 = 8;
+  if (t2 >= t1) g2 = 8 * max(1, (t2 + t1 / 2) / max(t1, 1));
+  else g1 = 8 * max(1, (t1 + t2 / 2) / max(t2, 1));
+  hipLaunchKernelGGL((gemm_pair_ws<F1, BM1, BN1, DmaShape<F1>::NST, E1, F2, BM2, BN2,
+                                   DmaShape<F2>::NST, E2>),
+                     dim3(t1 + t2), dim3(512), 0, s, o1, e1, t1, g1, o2, e2, t2, g2);
+  return hipGetLastError();
+}
+
+template <int FW, int FD, typename T>
+hipError_t pair_by_tiles(int kw, int kd, const GemmOperands<bf16_t>& ow, const ParamOp<T>& ew,
+                         const GemmOperands<bf16_t>& od, const ActBwdOp<T>& ed, hipStream_t s) {
+  if (kw == 2 && kd == 2)
+    return launch_pair<FW, 64, 64, ParamOp<T>, FD, 64, 64, ActBwdOp<T>>(ow, ew, od, ed, s);
+  if (kw == 2 && kd == 3)
+    return launch_pair<FW, 64, 64, ParamOp<T>, FD, 64, 32, ActBwdOp<T>>(ow, ew, od, ed, s);
+  if (kw == 3 && kd == 2)
+    return launch_pair<FW, 64, 32, ParamOp<T>, FD, 64, 64, ActBwdOp<T>>(ow, ew, od, ed, s);
+  return launch_pair<FW, 64, 32, ParamOp<T>, FD, 64, 32, ActBwdOp<T>>(ow, ew, od, ed, s);
+}
+
 }  // namespace
+
+template <typename T>
+bool gemm_pairs(const GemmOperands<T>& opw, int flags_w, const GemmOperands<T>& opd,
+                int flags_d) {
+  // products on 64 x 64 or 64 x 32 tiles (two workgroups fit on a compute unit)
+  // that together need at most two workgroups per compute unit
+  const int kw = dma_tile_kind(opw), kd = dma_tile_kind(opd);
+  if (kw < 2 || kd < 2) return false;
+  const bool flags_ok = (flags_w == G_C1 && flags_d == G_C1) ||
+                        (flags_w == (G_C1 | G_AD | G_BD) && flags_d == (G_C1 | G_AD | G_BD)) ||
+                        (flags_w == (G_AD | G_BD) && flags_d == (G_C1 | G_AD | G_BD));
+  const int tw = kw == 2 ? cdiv(opw.M, 64) * cdiv(opw.N, 64) : cdiv(opw.M, 64) * cdiv(opw.N, 32);
+  const int td = kd == 2 ? cdiv(opd.M, 64) * cdiv(opd.N, 64) : cdiv(opd.M, 64) * cdiv(opd.N, 32);
+  return flags_ok && tw + td <= 512;
+}
+
+template <typename T>
+hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const ParamArgs<T>& P,
+                                  const GemmOperands<T>& opd, int flags_d,
+                                  const EpiActBwd<T>& e, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (gemm_pairs(opw, flags_w, opd, flags_d)) {
+      const int kw = dma_tile_kind(opw), kd = dma_tile_kind(opd);
+      {
+        const ParamOp<T> ew{P, P.nin, P.nout};
+        const ActBwdOp<T> ed{e, e.M, e.N};
+        if (flags_w == G_C1 && flags_d == G_C1)
+          return pair_by_tiles<G_C1, G_C1, T>(kw, kd, opw, ew, opd, ed, s);
+        if (flags_w == (G_C1 | G_AD | G_BD) && flags_d == (G_C1 | G_AD | G_BD))
+          return pair_by_tiles<G_C1 | G_AD | G_BD, G_C1 | G_AD | G_BD, T>(kw, kd, opw, ew, opd, ed, s);
+        if (flags_w == (G_AD | G_BD) && flags_d == (G_C1 | G_AD | G_BD))
+          return pair_by_tiles<G_AD | G_BD, G_C1 | G_AD | G_BD, T>(kw, kd, opw, ew, opd, ed, s);
+      }
+    }
+  }
+  hipError_t r = gemm_param<T>(opw, flags_w, P, s);
+  if (r != hipSuccess) return r;
+  return gemm_act_bwd<T>(opd, flags_d, e, s);
+}
 
 long gemm_splitk_floats(int M, int N, int K) {
   const int S = splitk_count(M, N, K);
@@ -1161,5 +1281,10 @@ template hipError_t gemm_act_bwd<bf16_t>(const GemmOperands<bf16_t>&, int, const
 template hipError_t gemm_act_bwd<float>(const GemmOperands<float>&, int, const EpiActBwd<float>&, hipStream_t);
 template hipError_t gemm_param<bf16_t>(const GemmOperands<bf16_t>&, int, const ParamArgs<bf16_t>&, hipStream_t);
 template hipError_t gemm_param<float>(const GemmOperands<float>&, int, const ParamArgs<float>&, hipStream_t);
+
+template bool gemm_pairs<bf16_t>(const GemmOperands<bf16_t>&, int, const GemmOperands<bf16_t>&, int);
+template bool gemm_pairs<float>(const GemmOperands<float>&, int, const GemmOperands<float>&, int);
+template hipError_t gemm_param_and_act_bwd<bf16_t>(const GemmOperands<bf16_t>&, int, const ParamArgs<bf16_t>&, const GemmOperands<bf16_t>&, int, const EpiActBwd<bf16_t>&, hipStream_t);
+template hipError_t gemm_param_and_act_bwd<float>(const GemmOperands<float>&, int, const ParamArgs<float>&, const GemmOperands<float>&, int, const EpiActBwd<float>&, hipStream_t);
 
 }  // namespace mfmg

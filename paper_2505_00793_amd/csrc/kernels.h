@@ -180,6 +180,17 @@ hipError_t gemm_act_bwd(const GemmOperands<T>& op, int flags, const EpiActBwd<T>
 template <typename T>
 hipError_t gemm_param(const GemmOperands<T>& op, int flags, const ParamArgs<T>& P,
                       hipStream_t s);
+// A layer's backward-weight product (with the parameter epilogue) and its
+// backward-data product (with the activation epilogue), which are independent:
+// one launch running both when they are small (bf16 operands on 64-row tiles,
+// at most two workgroups per compute unit together), else the two launches
+// above in that order.
+template <typename T>
+bool gemm_pairs(const GemmOperands<T>& opw, int flags_w, const GemmOperands<T>& opd, int flags_d);
+template <typename T>
+hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const ParamArgs<T>& P,
+                                  const GemmOperands<T>& opd, int flags_d,
+                                  const EpiActBwd<T>& e, hipStream_t s);
 template <typename T>
 hipError_t gemm_store(const GemmOperands<T>& op, int flags, const EpiStore& e, hipStream_t s);
 template <typename T>
