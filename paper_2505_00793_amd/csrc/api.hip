@@ -133,11 +133,15 @@ void carve_act(const mfmg_problem* p, Carver& c, Act<T>& a, int R, bool dual) {
   a.X = c.take<T>((size_t)R * p->ld(p->w[0]));
   a.XT = c.take<T>((size_t)p->w[0] * p->ld(R));
   int maxw = 1;
+  // ReLU hidden layers keep no pre-activations: the backward reads the sign of
+  // their activations instead
+  const bool relu = p->d.act == MFMG_ACT_RELU;
   for (int l = 0; l < L; ++l) {
     const int nout = p->w[l + 1];
     if (nout > maxw) maxw = nout;
-    a.Z[l] = c.take<float>((size_t)R * nout);
-    a.Zd[l] = dual ? c.take<float>((size_t)R * nout) : nullptr;
+    const bool keep_z = !relu || l == L - 1;
+    a.Z[l] = keep_z ? c.take<float>((size_t)R * nout) : nullptr;
+    a.Zd[l] = (dual && keep_z) ? c.take<float>((size_t)R * nout) : nullptr;
     a.A[l] = a.AT[l] = a.Ad[l] = a.AdT[l] = nullptr;
     if (l < L - 1) {
       a.A[l] = c.take<T>((size_t)R * p->ld(nout));
@@ -448,6 +452,8 @@ struct Eng {
         opd.K = nout;
         e.Zp = a.Z[l - 1];
         e.Zdp = a.Zd[l - 1];
+        e.Ap = a.A[l - 1];
+        e.ldAp = (int)p->ld(nin);
         e.act = p->d.act;
         e.dual = dual;
         e.M = R;

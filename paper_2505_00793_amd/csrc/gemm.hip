@@ -104,8 +104,8 @@ struct ActFwdOp {
       z[k] = c1[k] + b[k];
       zd[k] = c2[k] + bd[k];
     }
-    st4(e.Z, (long)m * e.N + n, cnt, vec, z);
-    if (e.dual) st4(e.Zd, (long)m * e.N + n, cnt, vec, zd);
+    if (e.Z) st4(e.Z, (long)m * e.N + n, cnt, vec, z);
+    if (e.dual && e.Zd) st4(e.Zd, (long)m * e.N + n, cnt, vec, zd);
     if (e.last) return;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -136,8 +136,26 @@ struct ActBwdOp {
   };
   __device__ int n_trans() const { return e.dual ? 2 : 1; }
   __device__ bool aligned() const { return (e.N & 3) == 0; }
+  // 4 consecutive activations a[m][n..n+3] (n a multiple of 4) as floats
+  __device__ __forceinline__ void ld_act4(long idx, float* out) const {
+    if constexpr (sizeof(T) == 2) {
+      const uint2 v = *reinterpret_cast<const uint2*>(e.Ap + idx);
+      out[0] = bf2f((bf16_t)(v.x & 0xffffu)); out[1] = bf2f((bf16_t)(v.x >> 16));
+      out[2] = bf2f((bf16_t)(v.y & 0xffffu)); out[3] = bf2f((bf16_t)(v.y >> 16));
+    } else {
+      ld4v(reinterpret_cast<const float*>(e.Ap), idx, out);
+    }
+  }
   template <int NIT>
   __device__ __forceinline__ void load_rows(int bz, int m, int dm, int n, In (&in)[NIT]) const {
+    if (!e.Zp) {   // ReLU: the sign of the activation
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        ld_act4((long)(m + it * dm) * e.ldAp + n, in[it].z);
+        in[it].zd[0] = in[it].zd[1] = in[it].zd[2] = in[it].zd[3] = 0.f;
+      }
+      return;
+    }
 #pragma unroll
     for (int it = 0; it < NIT; ++it) ld4v(e.Zp, (long)(m + it * dm) * e.N + n, in[it].z);
     if (e.dual) {
@@ -163,8 +181,14 @@ struct ActBwdOp {
     const bool vec = cnt == 4 && (e.N & 3) == 0;
     In in;
     in.zd[0] = in.zd[1] = in.zd[2] = in.zd[3] = 0.f;
-    ld4(e.Zp, (long)m * e.N + n, cnt, vec, in.z);
-    if (e.dual) ld4(e.Zdp, (long)m * e.N + n, cnt, vec, in.zd);
+    if (e.Zp) {
+      ld4(e.Zp, (long)m * e.N + n, cnt, vec, in.z);
+      if (e.dual) ld4(e.Zdp, (long)m * e.N + n, cnt, vec, in.zd);
+    } else {   // ReLU: the sign of the activation
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        in.z[k] = k < cnt ? Elem<T>::to_float(e.Ap[(long)m * e.ldAp + n + k]) : 0.f;
+    }
     row_in(bz, m, n, cnt, in, c1, c2, t1, t2);
   }
   __device__ __forceinline__ void trans(int k, int bz, int n, int m, int cnt,

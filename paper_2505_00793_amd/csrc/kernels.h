@@ -41,8 +41,9 @@ long gemm_splitk_floats(int M, int N, int K);
 
 // Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
 // ad = act'(z) zd.  Hidden layers store z (and zd) in float32 for the
-// backward and a (ad) as operands in both layouts; the output layer stores the
-// logits z (and zd) only.
+// backward (not with ReLU: Z and Zd null, the backward reads the sign of a) and
+// a (ad) as operands in both layouts; the output layer stores the logits z (and
+// zd) only.
 template <typename T>
 struct EpiActFwd {
   const float* bias;     // [N] or null
@@ -58,11 +59,15 @@ struct EpiActFwd {
 
 // Backward-data of one layer: C1 = dA of the previous layer's output, C2 its
 // tangent.  dz = dA * act'(z), dzd = dAd * act'(z) + dA * act''(z) * zd, stored
-// as operands in both layouts.
+// as operands in both layouts.  For ReLU, act'(z) = [z > 0] = [a > 0] and
+// act'' = 0, so the previous layer's activation operand rows Ap can stand in for
+// its pre-activations (Zp and Zdp null).
 template <typename T>
 struct EpiActBwd {
-  const float* Zp;       // [M][N] pre-activations of the previous layer
-  const float* Zdp;      // [M][N] their tangents (dual)
+  const float* Zp;       // [M][N] pre-activations of the previous layer, or null
+  const float* Zdp;      // [M][N] their tangents (dual), or null
+  const T* Ap;           // ReLU without Zp: activations of the previous layer [M][ldAp]
+  int ldAp;
   int act, dual;
   int M, N;
   T* dZ;  T* dZT;        // [M][ld], [N][ldT]

@@ -750,7 +750,8 @@ struct TfEng {
                        fl(dual), matP(y.w2[b], F, d, out ? out->W[b][3] : nullptr, out ? out->WT[b][3] : nullptr), s));
       {
         EpiActBwd<T> e;
-        e.Zp = a.Z1[b]; e.Zdp = a.Z1d[b]; e.act = ACT_GELU; e.dual = dual; e.M = N; e.N = F;
+        e.Zp = a.Z1[b]; e.Zdp = a.Z1d[b]; e.Ap = nullptr; e.ldAp = 0;
+        e.act = ACT_GELU; e.dual = dual; e.M = N; e.N = F;
         e.dZ = a.dZ1; e.dZT = a.dZ1T; e.dZd = a.dZ1d; e.dZdT = a.dZ1dT;
         e.ld = (int)y.ld(F); e.ldT = (int)y.ld(N);
         HC(gemm_act_bwd<T>(op(a.dhb, dual ? a.dhdb : nullptr, th.W[b][3], dual ? v->W[b][3] : nullptr,
