@@ -138,9 +138,12 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ a0
   }
 }
 
-// bf16 version for rows, cols and both leading dimensions multiples of 8: a
-// 64 x 64 tile goes in with one 16-byte load per 8 elements and out with one
-// 16-byte store per 8 transposed elements.
+// bf16 version: a 64 x 64 tile goes in with one 16-byte load per 8 elements
+// and out with one 16-byte store per 8 transposed elements.  Requires rows, ld,
+// ldT and the batch strides to be multiples of 8 and ld >= roundup8(cols): cols
+// itself may be ragged, in which case the loads read the rows' padding up to
+// the next multiple of 8 (those lanes land in LDS but are never stored) and the
+// output rows past cols are skipped.
 // blockIdx.z = job * batch + matrix; matrix m of job j is src[j] + m s_src.
 __global__ void __launch_bounds__(256) transpose_bf16_kernel(TrJobs J, int batch, int rows,
                                                              int cols, int ld, int ldT,

@@ -225,8 +225,8 @@ struct ConvJobs {
   T* dstT[CONV_MAX_JOBS] = {};
 };
 // Transposed copies of bf16 matrices: up to TR_MAX_JOBS of one shape, each a
-// batch of matrices at strides s_src / s_dst (rows, cols, leading dimensions and
-// strides multiples of 8).
+// batch of matrices at strides s_src / s_dst (rows, leading dimensions and
+// strides multiples of 8; cols may be ragged when ld >= cols rounded up to 8).
 constexpr int TR_MAX_JOBS = 6;
 struct TrJobs {
   int n = 0;
