@@ -15,6 +15,7 @@
 //                   epilogue adds H v to bar theta and accumulates d eta
 //                   (eq. bptt_recur with eq. vhp_to_hvp / eq. vmp_to_mvp)
 // No host synchronisation happens inside a call.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -115,6 +116,8 @@ struct Act {  // one inner step's activations, up to R rows (the dynamic memory)
   T* dZd[2];
   T* dZdT[2];
   float* loss_rows;
+  float* skws;   // split-K partial sums of the float32 forward products (or null)
+  long skws_n;
 };
 
 template <typename T>
@@ -159,6 +162,16 @@ void carve_act(const mfmg_problem* p, Carver& c, Act<T>& a, int R, bool dual) {
     a.dZdT[k] = dual ? c.take<T>((size_t)maxw * p->ld(R)) : nullptr;
   }
   a.loss_rows = c.take<float>(R);
+  // float32 forward products with few output tiles and a long k run split-K
+  long ws = 0;
+  if (!p->bf16()) {
+    for (int l = 0; l < L; ++l) {
+      ws = std::max(ws, gemm_splitk_fwd_f32_floats(p->d.rows, p->w[l + 1], p->w[l]));
+      ws = std::max(ws, gemm_splitk_fwd_f32_floats(p->d.val_rows, p->w[l + 1], p->w[l]));
+    }
+  }
+  a.skws_n = ws;
+  a.skws = ws > 0 ? c.take<float>(ws) : nullptr;
 }
 
 template <typename T>
@@ -357,6 +370,8 @@ struct Eng {
       op.M = R;
       op.N = nout;
       op.K = nin;
+      op.ws = a.skws;
+      op.ws_floats = a.skws_n;
       const int flags = G_C1 | (dual ? (G_BD | (l > 0 ? G_AD : 0)) : 0);
       EpiActFwd<T> e;
       e.bias = th.b[l];

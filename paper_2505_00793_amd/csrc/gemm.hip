@@ -1041,6 +1041,17 @@ int splitk_count(int M, int N, int K) {
   return S;
 }
 
+// Float32 products with at most 8 output tiles of 64 x 64 and a long k (c2's
+// first layer, 128 x 256 over 784: 8 workgroups would each walk all of k): up
+// to 8 k slices, each at least 64 deep and a multiple of 4.
+int splitk_count_small(int M, int N, int K) {
+  const int tiles = cdiv(M, 64) * cdiv(N, 64);
+  if (M <= 0 || N <= 0 || tiles > 8 || K < 512) return 1;
+  int S = 8;
+  while (S > 1 && (K % S != 0 || (K / S) % 4 != 0 || K / S < 64)) --S;
+  return S;
+}
+
 // One workgroup per 16 x 64 output tile, one thread per 4 columns of a row;
 // the transposed outputs go through an LDS copy of the tile.
 template <class Epi>
@@ -1104,6 +1115,8 @@ __global__ void __launch_bounds__(256) splitk_epilogue(const float* __restrict__
 
 template <class E> struct IsParamOp : std::false_type {};
 template <typename T> struct IsParamOp<ParamOp<T>> : std::true_type {};
+template <class E> struct IsActFwdOp : std::false_type {};
+template <typename T> struct IsActFwdOp<ActFwdOp<T>> : std::true_type {};
 
 template <typename T, int FLAGS, class Epi>
 hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipStream_t s) {
@@ -1137,6 +1150,13 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
   if constexpr (IsParamOp<Epi>::value) {
     if (op.ws && op.batch == 1) {
       const int S = splitk_count(op.M, op.N, op.K);
+      if (S > 1 && op.ws_floats >= 2L * S * op.M * op.N)
+        return launch_splitk<T, FLAGS>(op, epi, S, s);
+    }
+  }
+  if constexpr (sizeof(T) == 4 && IsActFwdOp<Epi>::value) {
+    if (op.ws && op.batch == 1) {
+      const int S = splitk_count_small(op.M, op.N, op.K);
       if (S > 1 && op.ws_floats >= 2L * S * op.M * op.N)
         return launch_splitk<T, FLAGS>(op, epi, S, s);
     }
@@ -1253,6 +1273,11 @@ hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const
 
 long gemm_splitk_floats(int M, int N, int K) {
   const int S = splitk_count(M, N, K);
+  return S > 1 ? 2L * S * M * N : 0;
+}
+
+long gemm_splitk_fwd_f32_floats(int M, int N, int K) {
+  const int S = splitk_count_small(M, N, K);
   return S > 1 ? 2L * S * M * N : 0;
 }
 

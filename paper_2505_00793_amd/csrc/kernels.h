@@ -38,6 +38,10 @@ struct GemmOperands {
 // uses for split-K when given it; 0 when it runs without (bf16 operands, one
 // batch).
 long gemm_splitk_floats(int M, int N, int K);
+// Workspace (floats) that a float32 forward product (activation epilogue) of an
+// M x N output over K uses for split-K when given it (few output tiles, long k);
+// 0 when it runs without.
+long gemm_splitk_fwd_f32_floats(int M, int N, int K);
 
 // Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
 // ad = act'(z) zd.  Hidden layers store z (and zd) in float32 for the

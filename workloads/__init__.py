@@ -141,6 +141,11 @@ TOY_SMALL_BASE = Config(name="toy", cfg_id=0, act=ACT_NONE, loss=LOSS_MAPMSE, op
 SMALL: Dict[str, Config] = {
     "c1_small": C1.with_(name="c1_small", cfg_id=101, rows=100, val_rows=77, T=3, widths=(37, 1)),
     "c2_small": C2.with_(name="c2_small", cfg_id=102, widths=(150, 70, 13), rows=70, val_rows=90, T=3),
+    # a float32 first layer with a long contraction and few output tiles: the
+    # training forward products run split-K (8 slices of 76), the validation
+    # ones (more tiles) do not
+    "c2_splitk": C2.with_(name="c2_splitk", cfg_id=126, widths=(608, 72, 10), rows=36,
+                          val_rows=300, T=3),
     "c3_small": C3.with_(name="c3_small", cfg_id=103, widths=(136, 200, 72, 10), rows=150,
                          val_rows=96, T=4),
     "c5_small": C5.with_(name="c5_small", cfg_id=105, widths=(200, 300, 260, 37), rows=130,
