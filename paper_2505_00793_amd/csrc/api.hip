@@ -688,8 +688,9 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
     if (adam) {
       float k1, k2;
       bias_corr(p, i, &k1, &k2);
+      AdamVjpArgs<T> AL[MFMG_MAX_LAYERS];
       for (int l = 0; l < p->L; ++l) {
-        AdamVjpArgs<T> A;
+        AdamVjpArgs<T>& A = AL[l];
         A.layer = l;
         A.n_layers = p->L;
         A.nin = p->w[l];
@@ -715,12 +716,9 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
         A.vb = mp.v[0].b[l];
         A.ldW = (int)p->ld(A.nout);
         A.ldWT = (int)p->ld(A.nin);
-        A.partial = mp.partial + 2 * (size_t)mp.part_off[l];
-        int used = mp.part_off[l + 1] - mp.part_off[l];  // capacity in, blocks used out
-        TimingScope ts(7, s);
-        HIPCHK(adam_vjp<T>(A, &used, s));
       }
       TimingScope ts(7, s);
+      HIPCHK(adam_vjp<T>(AL, p->L, mp.part_off, mp.partial, s));
       HIPCHK(adam_reduce(mp.partial, mp.part_off, p->L, first, d_eta, s));
     }
     TRY(E.load_x(static_cast<const float*>(batches[i].x), R, a));

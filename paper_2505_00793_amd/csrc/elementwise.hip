@@ -459,15 +459,15 @@ __device__ __forceinline__ void adam_vjp_elem(const AdamVjpArgs<T>& a, long idx,
 }
 
 template <typename T>
-__global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpArgs<T> a, float* partial) {
+__device__ void adam_vjp_block(const AdamVjpArgs<T>& a, int blk, float* partial) {
   __shared__ float tile[16][65];
   __shared__ float red0[256], red1[256];
   const int tiles_n = (a.nout + 63) / 64;
   const int tiles = ((a.nin + 15) / 16) * tiles_n;
   const int tid = threadIdx.x;
   float pe = 0.0f, po = 0.0f;
-  if ((int)blockIdx.x < tiles) {
-    const int r0 = (blockIdx.x / tiles_n) * 16, c0 = (blockIdx.x % tiles_n) * 64;
+  if (blk < tiles) {
+    const int r0 = (blk / tiles_n) * 16, c0 = (blk % tiles_n) * 64;
     const int tx = tid & 63, ty = tid >> 6;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -487,7 +487,7 @@ __global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpArgs<T> a, float* 
       if (nn < a.nout && mm < a.nin) a.vWT[(long)nn * a.ldWT + mm] = Elem<T>::from_float(tile[rr][c]);
     }
   } else {
-    const long e = (long)(blockIdx.x - tiles) * 256 + tid;
+    const long e = (long)(blk - tiles) * 256 + tid;
     if (a.b_off >= 0 && e < a.nout) {
       float vg = 0.0f;
       adam_vjp_elem(a, a.b_off + e, vg, pe, po);
@@ -505,9 +505,26 @@ __global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpArgs<T> a, float* 
     __syncthreads();
   }
   if (tid == 0) {
-    partial[2 * blockIdx.x] = red0[0];
-    partial[2 * blockIdx.x + 1] = red1[0];
+    partial[0] = red0[0];
+    partial[1] = red1[0];
   }
+}
+
+// The Adam reverse of every layer of one step in one launch: workgroups
+// off[l] .. off[l + 1] - 1 take layer l, each writing its partial pair at its
+// own index.
+template <typename T>
+struct AdamVjpLayers {
+  AdamVjpArgs<T> a[MFMG_MAX_LAYERS];
+  int off[MFMG_MAX_LAYERS + 1];
+  int L;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256) adam_vjp_kernel(AdamVjpLayers<T> A, float* partial) {
+  int l = 0;
+  while (l + 1 < A.L && (int)blockIdx.x >= A.off[l + 1]) ++l;
+  adam_vjp_block(A.a[l], (int)blockIdx.x - A.off[l], partial + 2 * (long)blockIdx.x);
 }
 
 struct Offsets {
@@ -557,10 +574,14 @@ __global__ void __launch_bounds__(1024) adam_reduce_kernel(const float* __restri
 // validation batch.  Forward unroll with theta_t checkpoints, then the
 // reverse sweep with the dual pass (r, rdot) = (X theta - y, X v):
 // g = (2/N) X^T r, H v = (2/N) X^T rdot.
-// 1024 threads; each batch is staged in LDS (when it fits in 64 KB) with rows
-// padded to d + 1 floats, residuals take one thread per row (a serial dot
-// product over the features: the padding keeps the threads of a wave on
-// distinct banks), and X^T r takes 64 features x 16 row groups per pass with an
+// 1024 threads.  The batches are used in the order of the sweep: the T
+// training batches, the validation batch, then the training batches again in
+// reverse.  Each is staged in LDS (when it fits in 65 KB) with rows padded to
+// d + 1 floats; the next batch's values are loaded into registers while the
+// current one is used, so the sweep waits on global memory only for the first.
+// The checkpoints theta_t stay in LDS when (T + 1) d <= 4096.  Residuals take
+// four threads per row (a serial dot product over a quarter of the features,
+// then a 4-lane sum), X^T r takes 64 features x 16 row groups per pass with an
 // ordered sum of the 16 partials.
 // ------------------------------------------------------------------------------------
 constexpr int LR_MAXD = 256;
@@ -568,6 +589,8 @@ constexpr int LR_MAXR = 1024;
 constexpr int LR_MAXT = 64;
 constexpr int LR_THREADS = 1024;
 constexpr int LR_STAGE = 16640;  // floats of one batch staged in LDS, rows padded (65 KB)
+constexpr int LR_PF = (LR_STAGE + LR_THREADS - 1) / LR_THREADS;  // prefetched floats per thread
+constexpr int LR_CKPT = 4096;    // floats of checkpoints kept in LDS
 
 struct LinregArgs {
   const float* theta0;
@@ -587,74 +610,129 @@ __device__ __forceinline__ int lr_pitch(int rows, int d) {
   return rows * (d + 1) <= LR_STAGE ? d + 1 : d;
 }
 
-// X rows x d (row-major) into LDS with rows padded to d + 1 floats when it fits
-// (else left in global memory), and the targets y into ys.
-__device__ const float* lr_stage(const float* X, const float* __restrict__ y, int rows, int d,
-                                 float* stage, float* ys) {
-  const int n = rows * d;
-  __syncthreads();  // the previous batch's readers are done
-  for (int i = threadIdx.x; i < rows; i += LR_THREADS) ys[i] = y[i];
-  if (lr_pitch(rows, d) == d) {
-    __syncthreads();
-    return X;
-  }
-  for (int i = threadIdx.x; i < n; i += LR_THREADS) {
-    const int row = i / d;
-    stage[i + row] = X[i];   // row * (d + 1) + (i - row * d)
-  }
-  __syncthreads();
-  return stage;
+// Batch k of the sweep (k = 0 .. 2T).
+struct LrBatch {
+  const float* X;
+  const float* y;
+  int rows;
+};
+__device__ __forceinline__ LrBatch lr_batch(const LinregArgs& a, int k) {
+  if (k < a.T) return {a.xs[k], a.ys[k], a.rows};
+  if (k == a.T) return {a.vx, a.vy, a.vrows};
+  return {a.xs[2 * a.T - k], a.ys[2 * a.T - k], a.rows};
 }
 
-// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when u): one thread per row.
-// Returns this thread's share of sum_n r[n]^2.
-__device__ float lr_rows(const float* X, const float* y, const float* w,
-                         const float* u, int rows, int d, float* r, float* rd) {
-  const int pitch = lr_pitch(rows, d);
-  float sq = 0.0f;
-  for (int n = threadIdx.x; n < rows; n += LR_THREADS) {
-    const float* xr = X + n * pitch;
-    float s = 0.0f, sd = 0.0f;
-    for (int j = 0; j < d; ++j) {
-      const float x = xr[j];
-      s += x * w[j];
-      if (u) sd += x * u[j];
+// Registers holding one batch on its way to LDS: element tid + u * LR_THREADS
+// of X (when the batch is staged) and y[tid].  The loads are unconditional (an
+// index past the end reads the last element) so that a register is never both
+// cleared and loaded: the compiler would then wait for every load in flight.
+struct LrRegs {
+  float x[LR_PF];
+  float y;
+};
+__device__ __forceinline__ void lr_load(const LrBatch& b, int d, LrRegs& g) {
+  const int tid = threadIdx.x;
+  if (lr_pitch(b.rows, d) != d) {
+    const int n = b.rows * d;
+#pragma unroll
+    for (int u = 0; u < LR_PF; ++u) g.x[u] = b.X[min(tid + u * LR_THREADS, n - 1)];
+  }
+  g.y = b.y[min(tid, b.rows - 1)];
+}
+// Registers -> LDS (rows padded).  Callers synchronise before (the previous
+// batch's readers are done) and after.
+__device__ __forceinline__ void lr_commit(const LrBatch& b, int d, const LrRegs& g, float* stage,
+                                          float* ys) {
+  const int tid = threadIdx.x;
+  if (tid < b.rows) ys[tid] = g.y;
+  if (lr_pitch(b.rows, d) == d) return;
+  // element i = row * d + col goes to row * (d + 1) + col = i + row; row and col
+  // advance by LR_THREADS elements per step without a division
+  const int n = b.rows * d;
+  const int qd = LR_THREADS / d, rd = LR_THREADS - qd * d;
+  int row = tid / d, col = tid - row * d;
+#pragma unroll
+  for (int u = 0; u < LR_PF; ++u) {
+    const int i = tid + u * LR_THREADS;
+    if (i < n) stage[i + row] = g.x[u];
+    row += qd;
+    col += rd;
+    if (col >= d) {
+      col -= d;
+      ++row;
     }
-    const float res = s - y[n];
-    r[n] = res;
-    if (u) rd[n] = sd;
-    sq += res * res;
+  }
+}
+
+// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when DU): four threads per row,
+// each over a quarter of the features.  Returns this thread's share of
+// sum_n r[n]^2 (on the first thread of each row).  X is the staged batch in
+// LDS or the batch in global memory; the two are separate instantiations so
+// that every access has a known address space (a flat access would wait for
+// the next batch's loads).
+template <bool DU>
+__device__ float lr_rows(const float* X, int pitch, const float* y, const float* w,
+                         const float* u, int rows, int d, float* r, float* rd) {
+  const int q = threadIdx.x & 3;
+  const int jq = (d + 3) / 4, j0 = q * jq, j1 = min(d, j0 + jq);
+  float sq = 0.0f;
+  for (int nb = 0; nb < rows; nb += LR_THREADS / 4) {
+    const int n = nb + (threadIdx.x >> 2);
+    float s = 0.0f, sd = 0.0f;
+    if (n < rows) {
+      const float* xr = X + n * pitch;
+#pragma unroll 8
+      for (int j = j0; j < j1; ++j) {
+        const float x = xr[j];
+        s += x * w[j];
+        if (DU) sd += x * u[j];
+      }
+    }
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    if (DU) {
+      sd += __shfl_xor(sd, 1, 64);
+      sd += __shfl_xor(sd, 2, 64);
+    }
+    if (n < rows && q == 0) {
+      const float res = s - y[n];
+      r[n] = res;
+      if (DU) rd[n] = sd;
+      sq += res * res;
+    }
   }
   __syncthreads();
   return sq;
 }
 
-// out[j] = sum_n X[n][j] v[n] (and out2 with v2 when v2), j < d.
-__device__ void lr_cols(const float* X, const float* v, const float* v2, int rows, int d,
-                        float* part, float* part2, float* out, float* out2) {
+// out[j] = sum_n X[n][j] v[n] (and out2 with v2 when DU), j < d.
+template <bool DU>
+__device__ void lr_cols(const float* X, int pitch, const float* v, const float* v2, int rows,
+                        int d, float* part, float* part2, float* out, float* out2) {
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int pitch = lr_pitch(rows, d);
   for (int j0 = 0; j0 < d; j0 += 64) {
     const int j = j0 + c;
     float s = 0.0f, s2 = 0.0f;
     if (j < d) {
+#pragma unroll 8
       for (int n = q; n < rows; n += 16) {
         const float x = X[n * pitch + j];
         s += x * v[n];
-        if (v2) s2 += x * v2[n];
+        if (DU) s2 += x * v2[n];
       }
     }
     part[q * 64 + c] = s;
-    if (v2) part2[q * 64 + c] = s2;
+    if (DU) part2[q * 64 + c] = s2;
     __syncthreads();
     if (threadIdx.x < 64 && j < d) {
       float a = 0.0f, b = 0.0f;
+#pragma unroll
       for (int k = 0; k < 16; ++k) {
         a += part[k * 64 + c];
-        if (v2) b += part2[k * 64 + c];
+        if (DU) b += part2[k * 64 + c];
       }
       out[j] = a;
-      if (v2) out2[j] = b;
+      if (DU) out2[j] = b;
     }
     __syncthreads();
   }
@@ -662,63 +740,89 @@ __device__ void lr_cols(const float* X, const float* v, const float* v2, int row
 
 __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __shared__ __attribute__((aligned(16))) float stage[LR_STAGE];
+  __shared__ float ck[LR_CKPT];
   __shared__ float th[LR_MAXD], tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD], vv[LR_MAXD];
   __shared__ float gs[LR_MAXD], hs[LR_MAXD];
   __shared__ float r[LR_MAXR], rd[LR_MAXR], ys[LR_MAXR];
   __shared__ float part[16 * 64], part2[16 * 64];
   __shared__ float red[LR_THREADS / 64];
-  const int tid = threadIdx.x, d = a.d;
+  const int tid = threadIdx.x, d = a.d, T = a.T;
+  const bool ck_lds = (long)(T + 1) * d <= LR_CKPT;
+  LrRegs g;
+  lr_load(lr_batch(a, 0), d, g);
   for (int j = tid; j < d; j += LR_THREADS) {
     th[j] = a.theta0[j];
     lam[j] = expf(a.eta[j]);
     eb[j] = 0.0f;
-    a.ckpt[j] = th[j];
+    if (ck_lds) ck[j] = th[j];
+    else a.ckpt[j] = th[j];
+  }
+  for (int k = 0; k <= 2 * T; ++k) {
+    const LrBatch b = lr_batch(a, k);
+    const int i = k < T ? k : 2 * T - k;   // training step of a forward or reverse phase
+    if (k > T) {
+      for (int j = tid; j < d; j += LR_THREADS) {
+        th[j] = ck_lds ? ck[i * d + j] : a.ckpt[(long)i * d + j];
+        vv[j] = -lam[j] * tb[j];
+      }
+    }
+    __syncthreads();   // the previous batch's readers are done; th, vv published
+    lr_commit(b, d, g, stage, ys);
+    if (k < 2 * T) lr_load(lr_batch(a, k + 1), d, g);   // in flight during this phase
+    __syncthreads();
+    const int pitch = lr_pitch(b.rows, d);
+    const bool staged = pitch != d;
+    const float inv = 2.0f / b.rows;
+    if (k < T) {
+      // forward unroll step
+      if (staged) {
+        lr_rows<false>(stage, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
+        lr_cols<false>(stage, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
+      } else {
+        lr_rows<false>(b.X, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
+        lr_cols<false>(b.X, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
+      }
+      for (int j = tid; j < d; j += LR_THREADS) {
+        th[j] -= lam[j] * inv * gs[j];
+        if (ck_lds) ck[(k + 1) * d + j] = th[j];
+        else a.ckpt[(long)(k + 1) * d + j] = th[j];
+      }
+    } else if (k == T) {
+      // validation loss and its gradient (the seed of the reverse sweep)
+      float sq;
+      if (staged) {
+        sq = lr_rows<false>(stage, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
+        lr_cols<false>(stage, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
+      } else {
+        sq = lr_rows<false>(b.X, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
+        lr_cols<false>(b.X, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
+      }
+      sq = wave_sum(sq);
+      if ((tid & 63) == 0) red[tid >> 6] = sq;
+      __syncthreads();
+      if (tid == 0 && a.val_loss) {
+        float ls = 0.0f;
+        for (int w = 0; w < LR_THREADS / 64; ++w) ls += red[w];
+        *a.val_loss = ls / b.rows;
+      }
+      for (int j = tid; j < d; j += LR_THREADS) tb[j] = inv * gs[j];
+    } else {
+      // reverse step i: v = -exp(eta) bar theta_{i+1}; bar theta_i = bar theta_{i+1} + H v;
+      // bar eta += -exp(eta) g_i bar theta_{i+1}
+      if (staged) {
+        lr_rows<true>(stage, pitch, ys, th, vv, b.rows, d, r, rd);
+        lr_cols<true>(stage, pitch, r, rd, b.rows, d, part, part2, gs, hs);
+      } else {
+        lr_rows<true>(b.X, pitch, ys, th, vv, b.rows, d, r, rd);
+        lr_cols<true>(b.X, pitch, r, rd, b.rows, d, part, part2, gs, hs);
+      }
+      for (int j = tid; j < d; j += LR_THREADS) {
+        eb[j] += -lam[j] * inv * gs[j] * tb[j];
+        tb[j] += inv * hs[j];
+      }
+    }
   }
   __syncthreads();
-  // forward unroll
-  for (int t = 0; t < a.T; ++t) {
-    const float* X = lr_stage(a.xs[t], a.ys[t], a.rows, d, stage, ys);
-    const float inv = 2.0f / a.rows;
-    lr_rows(X, ys, th, nullptr, a.rows, d, r, nullptr);
-    lr_cols(X, r, nullptr, a.rows, d, part, nullptr, gs, nullptr);
-    for (int j = tid; j < d; j += LR_THREADS) {
-      th[j] -= lam[j] * inv * gs[j];
-      a.ckpt[(long)(t + 1) * d + j] = th[j];
-    }
-    __syncthreads();
-  }
-  // validation loss and its gradient (the seed of the reverse sweep)
-  {
-    const float* X = lr_stage(a.vx, a.vy, a.vrows, d, stage, ys);
-    const float inv = 2.0f / a.vrows;
-    const float sq = wave_sum(lr_rows(X, ys, th, nullptr, a.vrows, d, r, nullptr));
-    if ((tid & 63) == 0) red[tid >> 6] = sq;
-    lr_cols(X, r, nullptr, a.vrows, d, part, nullptr, gs, nullptr);
-    if (tid == 0 && a.val_loss) {
-      float ls = 0.0f;
-      for (int k = 0; k < LR_THREADS / 64; ++k) ls += red[k];
-      *a.val_loss = ls / a.vrows;
-    }
-    for (int j = tid; j < d; j += LR_THREADS) tb[j] = inv * gs[j];
-    __syncthreads();
-  }
-  // reverse sweep: v = -exp(eta) bar theta_{i+1}; bar theta_i = bar theta_{i+1} + H v;
-  // bar eta += -exp(eta) g_i bar theta_{i+1}
-  for (int i = a.T - 1; i >= 0; --i) {
-    const float inv = 2.0f / a.rows;
-    for (int j = tid; j < d; j += LR_THREADS) {
-      th[j] = a.ckpt[(long)i * d + j];
-      vv[j] = -lam[j] * tb[j];
-    }
-    const float* X = lr_stage(a.xs[i], a.ys[i], a.rows, d, stage, ys);  // publishes th, vv
-    lr_rows(X, ys, th, vv, a.rows, d, r, rd);
-    lr_cols(X, r, rd, a.rows, d, part, part2, gs, hs);
-    for (int j = tid; j < d; j += LR_THREADS) {
-      eb[j] += -lam[j] * inv * gs[j] * tb[j];
-      tb[j] += inv * hs[j];
-    }
-    __syncthreads();
-  }
   for (int j = tid; j < d; j += LR_THREADS) a.d_eta[j] = eb[j];
 }
 
@@ -868,13 +972,22 @@ hipError_t loss_reduce(const float* loss_rows, const float* alpha_logits, int ro
 }
 
 template <typename T>
-// *blocks: in, how many blocks the partial buffer holds; out, how many were used
-// (16 x 64 tiles of W, then 256 bias entries per block).
-hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks, hipStream_t s) {
-  const long nb = (long)cdiv(a.nin, 16) * cdiv(a.nout, 64) + (a.b_off >= 0 ? cdiv(a.nout, 256) : 0);
-  if (nb > *blocks) return hipErrorInvalidValue;
-  *blocks = (int)nb;
-  hipLaunchKernelGGL(adam_vjp_kernel<T>, dim3(nb), dim3(256), 0, s, a, a.partial);
+hipError_t adam_vjp(const AdamVjpArgs<T>* a, int L, const int* part_off, float* partial,
+                    hipStream_t s) {
+  if (L < 1 || L > MFMG_MAX_LAYERS) return hipErrorInvalidValue;
+  AdamVjpLayers<T> A;
+  A.L = L;
+  A.off[0] = 0;
+  for (int l = 0; l < L; ++l) {
+    // 16 x 64 tiles of W, then 256 bias entries per workgroup
+    const long nb = (long)cdiv(a[l].nin, 16) * cdiv(a[l].nout, 64) +
+                    (a[l].b_off >= 0 ? cdiv(a[l].nout, 256) : 0);
+    if (nb != part_off[l + 1] - part_off[l] || part_off[l] != A.off[l])
+      return hipErrorInvalidValue;
+    A.a[l] = a[l];
+    A.off[l + 1] = A.off[l] + (int)nb;
+  }
+  hipLaunchKernelGGL(adam_vjp_kernel<T>, dim3(A.off[L]), dim3(256), 0, s, A, partial);
   return hipGetLastError();
 }
 
@@ -925,7 +1038,7 @@ template hipError_t bias_reduce<bf16_t>(const bf16_t*, const bf16_t*, int, int, 
 template hipError_t bias_reduce<float>(const float*, const float*, int, int, const ParamArgs<float>&, hipStream_t);
 template hipError_t loss_head<bf16_t>(const LossArgs<bf16_t>&, hipStream_t);
 template hipError_t loss_head<float>(const LossArgs<float>&, hipStream_t);
-template hipError_t adam_vjp<bf16_t>(const AdamVjpArgs<bf16_t>&, int*, hipStream_t);
-template hipError_t adam_vjp<float>(const AdamVjpArgs<float>&, int*, hipStream_t);
+template hipError_t adam_vjp<bf16_t>(const AdamVjpArgs<bf16_t>*, int, const int*, float*, hipStream_t);
+template hipError_t adam_vjp<float>(const AdamVjpArgs<float>*, int, const int*, float*, hipStream_t);
 
 }  // namespace mfmg

@@ -987,6 +987,17 @@ struct DmaShape {
   static constexpr int NST = NOPS <= 2 ? 4 : NOPS == 3 ? 3 : 2;
 };
 
+// Pipeline depth of the small tiles (64 x 64, 64 x 32), whose products are
+// bound by load latency rather than by delivery: as many stages as fit in an
+// LDS budget per workgroup (144 KB with one workgroup per compute unit, 72 KB
+// with two), 2 to 8.
+template <int FLAGS, int BM, int BN, int BUDGET>
+struct DmaDepth {
+  static constexpr int STAGE = DmaSmem<FLAGS, BM, BN, 64, 2, 1>::STAGE_BYTES;
+  static constexpr int N0 = BUDGET / STAGE;
+  static constexpr int NST = BM > 64 ? DmaShape<FLAGS>::NST : N0 < 2 ? 2 : N0 > 8 ? 8 : N0;
+};
+
 template <typename T>
 bool dma_operand_ok(const T* p, int rows, int ld, int K, long stride) {
   if (!p) return true;
@@ -1009,6 +1020,14 @@ hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
     typedef DmaShape<FLAGS> DS;
     if (dma_ok(op)) {
+      if constexpr (BM == 64) {
+        if (tiles * op.batch <= 256) {   // one workgroup per compute unit: a deeper ring
+          constexpr int NST = DmaDepth<FLAGS, BM, BN, 147456>::NST;
+          hipLaunchKernelGGL((gemm_nt_ws<FLAGS, BM, BN, DS::BK, NST, Epi>), dim3(tiles, op.batch),
+                             dim3(512), 0, s, op, epi);
+          return hipGetLastError();
+        }
+      }
       hipLaunchKernelGGL((gemm_nt_ws<FLAGS, BM, BN, DS::BK, DS::NST, Epi>), dim3(tiles, op.batch),
                          dim3(512), 0, s, op, epi);
       return hipGetLastError();
@@ -1212,8 +1231,9 @@ hipError_t launch_pair(const GemmOperands<bf16_t>& o1, const E1& e1,
   int g1 = 8, g2 = 8;
   if (t2 >= t1) g2 = 8 * max(1, (t2 + t1 / 2) / max(t1, 1));
   else g1 = 8 * max(1, (t1 + t2 / 2) / max(t2, 1));
-  hipLaunchKernelGGL((gemm_pair_ws<F1, BM1, BN1, DmaShape<F1>::NST, E1, F2, BM2, BN2,
-                                   DmaShape<F2>::NST, E2>),
+  // at most two workgroups per compute unit: 72 KB rings
+  hipLaunchKernelGGL((gemm_pair_ws<F1, BM1, BN1, DmaDepth<F1, BM1, BN1, 73728>::NST, E1, F2, BM2,
+                                   BN2, DmaDepth<F2, BM2, BN2, 73728>::NST, E2>),
                      dim3(t1 + t2), dim3(512), 0, s, o1, e1, t1, g1, o2, e2, t2, g2);
   return hipGetLastError();
 }

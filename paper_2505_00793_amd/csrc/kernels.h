@@ -271,10 +271,14 @@ struct AdamVjpArgs {
   const float* theta; const float* m; const float* v; const float* g;   // step i state
   float* thetabar; float* mbar; float* vbar;                            // in/out
   T* vW; T* vWT; float* vb; int ldW, ldWT;                              // tangent out
-  float* partial;                // [blocks][2]: (eta_l partial, omega partial)
 };
+// The Adam reverse of layers 0 .. L-1 of one step in one launch.  partial:
+// [blocks][2] (eta_l partial, omega partial); layer l owns blocks
+// part_off[l] .. part_off[l + 1] - 1, which must be its 16 x 64 tiles of W plus
+// its bias blocks of 256 entries.
 template <typename T>
-hipError_t adam_vjp(const AdamVjpArgs<T>& a, int* blocks_used, hipStream_t s);
+hipError_t adam_vjp(const AdamVjpArgs<T>* a, int L, const int* part_off, float* partial,
+                    hipStream_t s);
 
 // d_eta[layer] (+)= sum partial[l][.][0]; d_eta[L] (+)= sum of all partial[.][1].
 hipError_t adam_reduce(const float* partial, const int* block_offsets, int n_layers, int first,

@@ -140,6 +140,10 @@ TOY_SMALL_BASE = Config(name="toy", cfg_id=0, act=ACT_NONE, loss=LOSS_MAPMSE, op
 # seconds, each spanning several GEMM tiles plus a ragged tail.
 SMALL: Dict[str, Config] = {
     "c1_small": C1.with_(name="c1_small", cfg_id=101, rows=100, val_rows=77, T=3, widths=(37, 1)),
+    # batches too large to stage in LDS (read from global memory), rows past 256
+    "c1_wide": C1.with_(name="c1_wide", cfg_id=127, rows=1000, val_rows=700, T=3, widths=(130, 1)),
+    # checkpoints too many for LDS ((T + 1) d > 4096), staged batches
+    "c1_long": C1.with_(name="c1_long", cfg_id=128, rows=120, val_rows=128, T=33, widths=(131, 1)),
     "c2_small": C2.with_(name="c2_small", cfg_id=102, widths=(150, 70, 13), rows=70, val_rows=90, T=3),
     # a float32 first layer with a long contraction and few output tiles: the
     # training forward products run split-K (8 slices of 76), the validation
