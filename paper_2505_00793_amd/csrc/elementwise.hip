@@ -574,22 +574,26 @@ __global__ void __launch_bounds__(1024) adam_reduce_kernel(const float* __restri
 // validation batch.  Forward unroll with theta_t checkpoints, then the
 // reverse sweep with the dual pass (r, rdot) = (X theta - y, X v):
 // g = (2/N) X^T r, H v = (2/N) X^T rdot.
-// 1024 threads.  The batches are used in the order of the sweep: the T
+// 512 threads.  The batches are used in the order of the sweep: the T
 // training batches, the validation batch, then the training batches again in
-// reverse.  Each is staged in LDS (when it fits in 65 KB) with rows padded to
-// d + 1 floats; the next batch's values are loaded into registers while the
-// current one is used, so the sweep waits on global memory only for the first.
-// The checkpoints theta_t stay in LDS when (T + 1) d <= 4096.  Residuals take
-// four threads per row (a serial dot product over a quarter of the features,
-// then a 4-lane sum), X^T r takes 64 features x 16 row groups per pass with an
-// ordered sum of the 16 partials.
+// reverse.  Each is staged in LDS (when it fits in 80 KB) with rows padded to a
+// pitch of 16 (mod 32) floats, so that the four rows a quarter-wave reads with
+// 16-byte accesses fall on distinct banks; the next batch's values are loaded
+// into registers while the current one is used, so the sweep waits on global
+// memory only for the first.  The checkpoints theta_t stay in LDS when
+// (T + 1) d <= 4096.  Residuals take four threads per row (every fourth 16-byte
+// group of the row, then a sum over the four lanes), X^T r takes 64 features x
+// 8 row groups per pass with an ordered sum of the 8 partials.
 // ------------------------------------------------------------------------------------
 constexpr int LR_MAXD = 256;
 constexpr int LR_MAXR = 1024;
 constexpr int LR_MAXT = 64;
-constexpr int LR_THREADS = 1024;
-constexpr int LR_STAGE = 16640;  // floats of one batch staged in LDS, rows padded (65 KB)
-constexpr int LR_PF = (LR_STAGE + LR_THREADS - 1) / LR_THREADS;  // prefetched floats per thread
+constexpr int LR_THREADS = 512;
+constexpr int LR_RG = LR_THREADS / 64;   // row groups of the column pass
+constexpr int LR_YPT = LR_MAXR / LR_THREADS;  // targets per thread
+constexpr int LR_STAGE = 20480;  // floats of one batch staged in LDS, rows padded (80 KB)
+constexpr int LR_PF = LR_STAGE / LR_THREADS;  // prefetched floats per thread (n <= LR_STAGE)
+constexpr int LR_PF4 = LR_PF / 4;             // prefetched 16-byte groups per thread
 constexpr int LR_CKPT = 4096;    // floats of checkpoints kept in LDS
 
 struct LinregArgs {
@@ -598,6 +602,7 @@ struct LinregArgs {
   const float* xs[LR_MAXT];  // device pointers of the T training batches
   const float* ys[LR_MAXT];
   int T, rows, d, vrows;
+  int vec;                   // every batch 16-byte aligned and d % 4 == 0
   const float* vx;
   const float* vy;
   float* d_eta;
@@ -605,9 +610,13 @@ struct LinregArgs {
   float* ckpt;  // (T + 1) x d
 };
 
-// Row stride of a staged batch (padded), or of the batch in global memory.
-__device__ __forceinline__ int lr_pitch(int rows, int d) {
-  return rows * (d + 1) <= LR_STAGE ? d + 1 : d;
+// Padded row pitch of a staged batch: d rounded up to 4, then to 16 (mod 32).
+__host__ __device__ __forceinline__ int lr_spitch(int d) {
+  const int p = (d + 3) & ~3;
+  return p + ((16 - (p & 31)) & 31);
+}
+__host__ __device__ __forceinline__ bool lr_staged(int rows, int d) {
+  return rows * lr_spitch(d) <= LR_STAGE;
 }
 
 // Batch k of the sweep (k = 0 .. 2T).
@@ -622,78 +631,114 @@ __device__ __forceinline__ LrBatch lr_batch(const LinregArgs& a, int k) {
   return {a.xs[2 * a.T - k], a.ys[2 * a.T - k], a.rows};
 }
 
-// Registers holding one batch on its way to LDS: element tid + u * LR_THREADS
-// of X (when the batch is staged) and y[tid].  The loads are unconditional (an
-// index past the end reads the last element) so that a register is never both
-// cleared and loaded: the compiler would then wait for every load in flight.
+// Registers holding one batch on its way to LDS: 16-byte group tid + u *
+// LR_THREADS of X (vec), or element tid + u * LR_THREADS, and y[tid].  The
+// loads are unconditional (an index past the end reads the last element) so
+// that a register is never both cleared and loaded: the compiler would then
+// wait for every load in flight.
 struct LrRegs {
-  float x[LR_PF];
-  float y;
+  float x[LR_PF];   // vec: group u in x[4u .. 4u + 3]
+  float y[LR_YPT];
 };
-__device__ __forceinline__ void lr_load(const LrBatch& b, int d, LrRegs& g) {
+__device__ __forceinline__ void lr_load(const LrBatch& b, int d, bool vec, LrRegs& g) {
   const int tid = threadIdx.x;
-  if (lr_pitch(b.rows, d) != d) {
+  if (lr_staged(b.rows, d)) {
     const int n = b.rows * d;
+    if (vec) {
+      const float4* X4 = reinterpret_cast<const float4*>(b.X);
 #pragma unroll
-    for (int u = 0; u < LR_PF; ++u) g.x[u] = b.X[min(tid + u * LR_THREADS, n - 1)];
+      for (int u = 0; u < LR_PF4; ++u) {
+        const float4 v = X4[min(tid + u * LR_THREADS, n / 4 - 1)];
+        g.x[4 * u] = v.x; g.x[4 * u + 1] = v.y; g.x[4 * u + 2] = v.z; g.x[4 * u + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < LR_PF; ++u) g.x[u] = b.X[min(tid + u * LR_THREADS, n - 1)];
+    }
   }
-  g.y = b.y[min(tid, b.rows - 1)];
-}
-// Registers -> LDS (rows padded).  Callers synchronise before (the previous
-// batch's readers are done) and after.
-__device__ __forceinline__ void lr_commit(const LrBatch& b, int d, const LrRegs& g, float* stage,
-                                          float* ys) {
-  const int tid = threadIdx.x;
-  if (tid < b.rows) ys[tid] = g.y;
-  if (lr_pitch(b.rows, d) == d) return;
-  // element i = row * d + col goes to row * (d + 1) + col = i + row; row and col
-  // advance by LR_THREADS elements per step without a division
-  const int n = b.rows * d;
-  const int qd = LR_THREADS / d, rd = LR_THREADS - qd * d;
-  int row = tid / d, col = tid - row * d;
 #pragma unroll
-  for (int u = 0; u < LR_PF; ++u) {
-    const int i = tid + u * LR_THREADS;
-    if (i < n) stage[i + row] = g.x[u];
-    row += qd;
-    col += rd;
-    if (col >= d) {
-      col -= d;
-      ++row;
+  for (int v = 0; v < LR_YPT; ++v) g.y[v] = b.y[min(tid + v * LR_THREADS, b.rows - 1)];
+}
+// Registers -> LDS (padded rows; the padding columns stay zero).  Callers
+// synchronise before (the previous batch's readers are done) and after.
+__device__ __forceinline__ void lr_commit(const LrBatch& b, int d, bool vec, const LrRegs& g,
+                                          float* stage, float* ys) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int v = 0; v < LR_YPT; ++v)
+    if (tid + v * LR_THREADS < b.rows) ys[tid + v * LR_THREADS] = g.y[v];
+  if (!lr_staged(b.rows, d)) return;
+  const int n = b.rows * d, P = lr_spitch(d);
+  // element i = row * d + col goes to row * P + col; row and col advance by the
+  // elements of one step without a division
+  if (vec) {
+    const int st = 4 * LR_THREADS;
+    const int qd = st / d, rd = st - qd * d;
+    int row = 4 * tid / d, col = 4 * tid - row * d;
+#pragma unroll
+    for (int u = 0; u < LR_PF4; ++u) {
+      if (4 * (tid + u * LR_THREADS) < n)
+        *reinterpret_cast<float4*>(stage + row * P + col) =
+            make_float4(g.x[4 * u], g.x[4 * u + 1], g.x[4 * u + 2], g.x[4 * u + 3]);
+      row += qd;
+      col += rd;
+      while (col >= d) {
+        col -= d;
+        ++row;
+      }
+    }
+  } else {
+    const int qd = LR_THREADS / d, rd = LR_THREADS - qd * d;
+    int row = tid / d, col = tid - row * d;
+#pragma unroll
+    for (int u = 0; u < LR_PF; ++u) {
+      if (tid + u * LR_THREADS < n) stage[row * P + col] = g.x[u];
+      row += qd;
+      col += rd;
+      if (col >= d) {
+        col -= d;
+        ++row;
+      }
     }
   }
 }
 
-// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when DU): four threads per row,
-// each over a quarter of the features.  Returns this thread's share of
-// sum_n r[n]^2 (on the first thread of each row).  X is the staged batch in
-// LDS or the batch in global memory; the two are separate instantiations so
-// that every access has a known address space (a flat access would wait for
-// the next batch's loads).
+// Sum over the four lanes of a quad (DPP quad permutations, no LDS traffic).
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));  // [1,0,3,2]
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));  // [2,3,0,1]
+  return v;
+}
+
+// r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when DU).  Staged batches: four
+// threads per row, thread q taking 16-byte groups q, q + 4, ... of the row (w
+// and u zero past d, like the row's padding); batches in global memory: one
+// thread per row.  Returns this thread's share of sum_n r[n]^2.
 template <bool DU>
-__device__ float lr_rows(const float* X, int pitch, const float* y, const float* w,
-                         const float* u, int rows, int d, float* r, float* rd) {
+__device__ float lr_rows_staged(const float* X, int P, const float* y, const float* w,
+                                const float* u, int rows, int d, float* r, float* rd) {
   const int q = threadIdx.x & 3;
-  const int jq = (d + 3) / 4, j0 = q * jq, j1 = min(d, j0 + jq);
+  const int g4 = (d + 3) >> 2;
   float sq = 0.0f;
   for (int nb = 0; nb < rows; nb += LR_THREADS / 4) {
     const int n = nb + (threadIdx.x >> 2);
     float s = 0.0f, sd = 0.0f;
     if (n < rows) {
-      const float* xr = X + n * pitch;
-#pragma unroll 8
-      for (int j = j0; j < j1; ++j) {
-        const float x = xr[j];
-        s += x * w[j];
-        if (DU) sd += x * u[j];
+      const float4* xr = reinterpret_cast<const float4*>(X + n * P);
+      const float4* w4 = reinterpret_cast<const float4*>(w);
+      const float4* u4 = reinterpret_cast<const float4*>(u);
+#pragma unroll 2
+      for (int j = q; j < g4; j += 4) {
+        const float4 x = xr[j], ww = w4[j];
+        s += x.x * ww.x + x.y * ww.y + x.z * ww.z + x.w * ww.w;
+        if (DU) {
+          const float4 uu = u4[j];
+          sd += x.x * uu.x + x.y * uu.y + x.z * uu.z + x.w * uu.w;
+        }
       }
     }
-    s += __shfl_xor(s, 1, 64);
-    s += __shfl_xor(s, 2, 64);
-    if (DU) {
-      sd += __shfl_xor(sd, 1, 64);
-      sd += __shfl_xor(sd, 2, 64);
-    }
+    s = quad_sum(s);
+    if (DU) sd = quad_sum(sd);
     if (n < rows && q == 0) {
       const float res = s - y[n];
       r[n] = res;
@@ -704,19 +749,42 @@ __device__ float lr_rows(const float* X, int pitch, const float* y, const float*
   __syncthreads();
   return sq;
 }
-
-// out[j] = sum_n X[n][j] v[n] (and out2 with v2 when DU), j < d.
 template <bool DU>
-__device__ void lr_cols(const float* X, int pitch, const float* v, const float* v2, int rows,
-                        int d, float* part, float* part2, float* out, float* out2) {
+__device__ float lr_rows_global(const float* X, const float* y, const float* w, const float* u,
+                                int rows, int d, float* r, float* rd) {
+  float sq = 0.0f;
+  for (int n = threadIdx.x; n < rows; n += LR_THREADS) {
+    const float* xr = X + (long)n * d;
+    float s = 0.0f, sd = 0.0f;
+    for (int j = 0; j < d; ++j) {
+      const float x = xr[j];
+      s += x * w[j];
+      if (DU) sd += x * u[j];
+    }
+    const float res = s - y[n];
+    r[n] = res;
+    if (DU) rd[n] = sd;
+    sq += res * res;
+  }
+  __syncthreads();
+  return sq;
+}
+
+// out[j] = sum_n X[n][j] v[n] (and out2 with v2 when DU), j < d; X has row
+// pitch P (LDS or global memory: separate instantiations, so that every access
+// has a known address space; a flat access would wait for the next batch's
+// loads).
+template <bool DU>
+__device__ void lr_cols(const float* X, int P, const float* v, const float* v2, int rows, int d,
+                        float* part, float* part2, float* out, float* out2) {
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
   for (int j0 = 0; j0 < d; j0 += 64) {
     const int j = j0 + c;
     float s = 0.0f, s2 = 0.0f;
     if (j < d) {
-#pragma unroll 8
-      for (int n = q; n < rows; n += 16) {
-        const float x = X[n * pitch + j];
+#pragma unroll 4
+      for (int n = q; n < rows; n += LR_RG) {
+        const float x = X[(long)n * P + j];
         s += x * v[n];
         if (DU) s2 += x * v2[n];
       }
@@ -727,7 +795,7 @@ __device__ void lr_cols(const float* X, int pitch, const float* v, const float* 
     if (threadIdx.x < 64 && j < d) {
       float a = 0.0f, b = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
+      for (int k = 0; k < LR_RG; ++k) {
         a += part[k * 64 + c];
         if (DU) b += part2[k * 64 + c];
       }
@@ -738,24 +806,102 @@ __device__ void lr_cols(const float* X, int pitch, const float* v, const float* 
   }
 }
 
+// The column pass of a staged batch (row pitch P, a multiple of 4, zero past
+// d): each thread takes a 16-byte group of 4 columns and every 32nd row, 16
+// groups (64 columns) per round; the 32 partials of a column are then summed in
+// order, 8 at a time by the 4 lanes of a quad, then across the quad.
+constexpr int LR_CG = 16;                     // column groups per round
+constexpr int LR_CRG = LR_THREADS / LR_CG;    // row groups
+template <bool DU>
+__device__ void lr_cols_staged(const float* X, int P, const float* v, const float* v2, int rows,
+                               int d, float* part, float* part2, float* out, float* out2) {
+  const int cg = threadIdx.x % LR_CG, q = threadIdx.x / LR_CG;
+  for (int j0 = 0; j0 < d; j0 += 4 * LR_CG) {
+    const int j = j0 + 4 * cg;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f), s2 = s;
+    if (j < d) {
+#pragma unroll 4
+      for (int n = q; n < rows; n += LR_CRG) {
+        const float4 x = *reinterpret_cast<const float4*>(X + n * P + j);
+        const float vn = v[n];
+        s.x += x.x * vn; s.y += x.y * vn; s.z += x.z * vn; s.w += x.w * vn;
+        if (DU) {
+          const float un = v2[n];
+          s2.x += x.x * un; s2.y += x.y * un; s2.z += x.z * un; s2.w += x.w * un;
+        }
+      }
+    }
+    reinterpret_cast<float4*>(part)[q * LR_CG + cg] = s;
+    if (DU) reinterpret_cast<float4*>(part2)[q * LR_CG + cg] = s2;
+    __syncthreads();
+    if (threadIdx.x < 4 * 4 * LR_CG) {
+      // column c = threadIdx.x / 4 of the round, partials h * 8 .. h * 8 + 7
+      const int c = threadIdx.x >> 2, h = threadIdx.x & 3;
+      float a = 0.0f, b = 0.0f;
+#pragma unroll
+      for (int k = 0; k < LR_CRG / 4; ++k) {
+        a += part[(h * (LR_CRG / 4) + k) * 4 * LR_CG + c];
+        if (DU) b += part2[(h * (LR_CRG / 4) + k) * 4 * LR_CG + c];
+      }
+      a = quad_sum(a);
+      if (DU) b = quad_sum(b);
+      if (h == 0 && j0 + c < d) {
+        out[j0 + c] = a;
+        if (DU) out2[j0 + c] = b;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// One pass over batch b: residuals, then X^T r (and the tangents when DU).
+template <bool DU>
+__device__ float lr_pass(const LrBatch& b, int d, const float* stage, const float* ys,
+                         const float* w, const float* u, float* r, float* rd, float* part,
+                         float* part2, float* g, float* h) {
+  float sq;
+  if (lr_staged(b.rows, d)) {
+    const int P = lr_spitch(d);
+    sq = lr_rows_staged<DU>(stage, P, ys, w, u, b.rows, d, r, rd);
+    lr_cols_staged<DU>(stage, P, r, rd, b.rows, d, part, part2, g, h);
+  } else {
+    sq = lr_rows_global<DU>(b.X, ys, w, u, b.rows, d, r, rd);
+    lr_cols<DU>(b.X, d, r, rd, b.rows, d, part, part2, g, h);
+  }
+  return sq;
+}
+
 __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __shared__ __attribute__((aligned(16))) float stage[LR_STAGE];
   __shared__ float ck[LR_CKPT];
-  __shared__ float th[LR_MAXD], tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD], vv[LR_MAXD];
+  __shared__ __attribute__((aligned(16))) float th[LR_MAXD], vv[LR_MAXD];
+  __shared__ float tb[LR_MAXD], lam[LR_MAXD], eb[LR_MAXD];
   __shared__ float gs[LR_MAXD], hs[LR_MAXD];
   __shared__ float r[LR_MAXR], rd[LR_MAXR], ys[LR_MAXR];
-  __shared__ float part[16 * 64], part2[16 * 64];
+  constexpr int NPART = LR_CRG * 4 * LR_CG > LR_RG * 64 ? LR_CRG * 4 * LR_CG : LR_RG * 64;
+  __shared__ __attribute__((aligned(16))) float part[NPART], part2[NPART];
   __shared__ float red[LR_THREADS / 64];
   const int tid = threadIdx.x, d = a.d, T = a.T;
+  const bool vec = a.vec != 0;
   const bool ck_lds = (long)(T + 1) * d <= LR_CKPT;
   LrRegs g;
-  lr_load(lr_batch(a, 0), d, g);
-  for (int j = tid; j < d; j += LR_THREADS) {
-    th[j] = a.theta0[j];
-    lam[j] = expf(a.eta[j]);
-    eb[j] = 0.0f;
-    if (ck_lds) ck[j] = th[j];
-    else a.ckpt[j] = th[j];
+  lr_load(lr_batch(a, 0), d, vec, g);
+  {
+    // the columns d .. (d rounded up to 4) - 1 of every row that can be staged
+    // stay zero (the 16-byte groups of the residual pass read them)
+    const int P = lr_spitch(d), pad = ((d + 3) & ~3) - d;
+    for (int i = tid; i < (LR_STAGE / P) * pad; i += LR_THREADS)
+      stage[(i / pad) * P + d + i % pad] = 0.0f;
+  }
+  for (int j = tid; j < LR_MAXD; j += LR_THREADS) {
+    th[j] = j < d ? a.theta0[j] : 0.0f;
+    vv[j] = 0.0f;
+    if (j < d) {
+      lam[j] = expf(a.eta[j]);
+      eb[j] = 0.0f;
+      if (ck_lds) ck[j] = th[j];
+      else a.ckpt[j] = th[j];
+    }
   }
   for (int k = 0; k <= 2 * T; ++k) {
     const LrBatch b = lr_batch(a, k);
@@ -767,21 +913,13 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
       }
     }
     __syncthreads();   // the previous batch's readers are done; th, vv published
-    lr_commit(b, d, g, stage, ys);
-    if (k < 2 * T) lr_load(lr_batch(a, k + 1), d, g);   // in flight during this phase
+    lr_commit(b, d, vec, g, stage, ys);
+    if (k < 2 * T) lr_load(lr_batch(a, k + 1), d, vec, g);   // in flight during this phase
     __syncthreads();
-    const int pitch = lr_pitch(b.rows, d);
-    const bool staged = pitch != d;
     const float inv = 2.0f / b.rows;
     if (k < T) {
       // forward unroll step
-      if (staged) {
-        lr_rows<false>(stage, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
-        lr_cols<false>(stage, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
-      } else {
-        lr_rows<false>(b.X, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
-        lr_cols<false>(b.X, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
-      }
+      lr_pass<false>(b, d, stage, ys, th, nullptr, r, nullptr, part, nullptr, gs, nullptr);
       for (int j = tid; j < d; j += LR_THREADS) {
         th[j] -= lam[j] * inv * gs[j];
         if (ck_lds) ck[(k + 1) * d + j] = th[j];
@@ -789,14 +927,8 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
       }
     } else if (k == T) {
       // validation loss and its gradient (the seed of the reverse sweep)
-      float sq;
-      if (staged) {
-        sq = lr_rows<false>(stage, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
-        lr_cols<false>(stage, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
-      } else {
-        sq = lr_rows<false>(b.X, pitch, ys, th, nullptr, b.rows, d, r, nullptr);
-        lr_cols<false>(b.X, pitch, r, nullptr, b.rows, d, part, nullptr, gs, nullptr);
-      }
+      float sq = lr_pass<false>(b, d, stage, ys, th, nullptr, r, nullptr, part, nullptr, gs,
+                                nullptr);
       sq = wave_sum(sq);
       if ((tid & 63) == 0) red[tid >> 6] = sq;
       __syncthreads();
@@ -809,13 +941,7 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
     } else {
       // reverse step i: v = -exp(eta) bar theta_{i+1}; bar theta_i = bar theta_{i+1} + H v;
       // bar eta += -exp(eta) g_i bar theta_{i+1}
-      if (staged) {
-        lr_rows<true>(stage, pitch, ys, th, vv, b.rows, d, r, rd);
-        lr_cols<true>(stage, pitch, r, rd, b.rows, d, part, part2, gs, hs);
-      } else {
-        lr_rows<true>(b.X, pitch, ys, th, vv, b.rows, d, r, rd);
-        lr_cols<true>(b.X, pitch, r, rd, b.rows, d, part, part2, gs, hs);
-      }
+      lr_pass<true>(b, d, stage, ys, th, vv, r, rd, part, part2, gs, hs);
       for (int j = tid; j < d; j += LR_THREADS) {
         eb[j] += -lam[j] * inv * gs[j] * tb[j];
         tb[j] += inv * hs[j];
@@ -1021,6 +1147,9 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   a.rows = rows;
   a.d = d;
   a.vrows = vrows;
+  bool vec = (d % 4) == 0 && (reinterpret_cast<uintptr_t>(vx) & 15) == 0;
+  for (int t = 0; t < T; ++t) vec = vec && (reinterpret_cast<uintptr_t>(xs[t]) & 15) == 0;
+  a.vec = vec ? 1 : 0;
   a.vx = vx;
   a.vy = vy;
   a.d_eta = d_eta;

@@ -144,6 +144,8 @@ SMALL: Dict[str, Config] = {
     "c1_wide": C1.with_(name="c1_wide", cfg_id=127, rows=1000, val_rows=700, T=3, widths=(130, 1)),
     # checkpoints too many for LDS ((T + 1) d > 4096), staged batches
     "c1_long": C1.with_(name="c1_long", cfg_id=128, rows=120, val_rows=128, T=33, widths=(131, 1)),
+    # 16-byte loads (d % 4 == 0) whose steps wrap rows; the validation batch is unstaged
+    "c1_vec": C1.with_(name="c1_vec", cfg_id=129, rows=150, val_rows=200, T=4, widths=(100, 1)),
     "c2_small": C2.with_(name="c2_small", cfg_id=102, widths=(150, 70, 13), rows=70, val_rows=90, T=3),
     # a float32 first layer with a long contraction and few output tiles: the
     # training forward products run split-K (8 slices of 76), the validation
