@@ -480,6 +480,9 @@ struct Eng {
         e.ld = (int)p->ld(nin);
         e.ldT = (int)p->ld(R);
       }
+      // the bias entries: summed by the backward-weight GEMM on its
+      // direct-to-LDS path, else by a reduction over dZ^T
+      P.fuse_bias = p->d.has_bias && gemm_fuses_bias<T>(opw, flags_w) ? 1 : 0;
       // the two products are independent: small ones share one launch
       const bool paired = l > 0 && gemm_pairs<T>(opw, flags_w, opd, flags_d);
       if (paired) {
@@ -489,7 +492,7 @@ struct Eng {
         TimingScope ts(dual ? (flags_w == (G_C1 | G_AD | G_BD) ? 8 : 5) : 2, s);
         HIPCHK(gemm_param<T>(opw, flags_w, P, s));
       }
-      if (p->d.has_bias) {
+      if (p->d.has_bias && !P.fuse_bias) {
         TimingScope ts(7, s);
         HIPCHK(bias_reduce<T>(a.dZT[cur], dual ? a.dZdT[cur] : nullptr, (int)p->ld(R), R, P, s));
       }

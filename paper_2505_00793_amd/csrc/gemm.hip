@@ -35,6 +35,14 @@ namespace mfmg {
 namespace {
 
 
+// Sum of 8 bfloat16 values in float32, pairwise in a fixed order.
+__device__ __forceinline__ float sum8(const bf16x8& v) {
+  float x[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = (float)v[i];
+  return ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
+}
+
 __device__ __forceinline__ void mma(f32x4& acc, const bf16x8& a, const bf16x8& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
 }
@@ -237,7 +245,18 @@ struct ParamOp {
                                         const float* v) const {
     store_row4(P.outWT, (long)n * P.ldWT + m, cnt, v);
   }
+  __device__ bool fuse_bias() const { return P.fuse_bias != 0 && P.b_off >= 0; }
+  // bias entry n from its gradient g (and H v entry hv)
+  __device__ __forceinline__ void bias(int n, float g, float hv) const {
+    const float cv = param_elem(P, P.b_off + n, g, hv);
+    if (P.outb) P.outb[n] = cv;
+  }
 };
+
+template <class E> struct IsParamOp : std::false_type {};
+template <typename T> struct IsParamOp<ParamOp<T>> : std::true_type {};
+template <class E> struct IsActFwdOp : std::false_type {};
+template <typename T> struct IsActFwdOp<ActFwdOp<T>> : std::true_type {};
 
 struct StoreOp {
   EpiStore e;
@@ -846,6 +865,15 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
     lds_barrier();
   } else {
     const int wm = wave >> 1, wn = wave & 1;
+    // Parameter epilogues with fused bias: the waves of the first tile row that
+    // read the top half of A also sum the B rows (dZ^T, and Bd = its tangent)
+    // they read, in k order; the four lanes of a row then add their sums.
+    constexpr bool BIAS = IsParamOp<Epi>::value && SM::LB;
+    bool bias_w = false;
+    if constexpr (BIAS) bias_w = m0 == 0 && wm == 0 && bz == 0 && epi.fuse_bias();
+    float bsum[TN], bdsum[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bsum[j] = bdsum[j] = 0.0f;
     f32x4 acc1[TM][TN], acc2[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -899,6 +927,36 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
               if constexpr (HAD) mma(acc2[i][j], ad[f][i], b[f][j]);
               if constexpr (HBD) mma(acc2[i][j], a[f][i], bd[f][j]);
             }
+        if constexpr (BIAS) {
+          if (bias_w) {
+#pragma unroll
+            for (int f = 0; f < NF; ++f)
+#pragma unroll
+              for (int j = 0; j < TN; ++j) {
+                bsum[j] += sum8(b[f][j]);
+                if constexpr (SM::LBD) bdsum[j] += sum8(bd[f][j]);
+              }
+          }
+        }
+      }
+    }
+    if constexpr (BIAS) {
+      if (bias_w) {
+        // lanes l, l + 16, l + 32, l + 48 read the chunks of one row
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          bsum[j] += __shfl_xor(bsum[j], 16, 64);
+          bsum[j] += __shfl_xor(bsum[j], 32, 64);
+          bdsum[j] += __shfl_xor(bdsum[j], 16, 64);
+          bdsum[j] += __shfl_xor(bdsum[j], 32, 64);
+        }
+        if (lane < 16) {
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int n = n0 + wn * WTN + j * 16 + lane;
+            if (n < op.N) epi.bias(n, bsum[j], bdsum[j]);
+          }
+        }
       }
     }
     wait_vm_lgkm<0>();
@@ -1132,10 +1190,6 @@ __global__ void __launch_bounds__(256) splitk_epilogue(const float* __restrict__
   }
 }
 
-template <class E> struct IsParamOp : std::false_type {};
-template <typename T> struct IsParamOp<ParamOp<T>> : std::true_type {};
-template <class E> struct IsActFwdOp : std::false_type {};
-template <typename T> struct IsActFwdOp<ActFwdOp<T>> : std::true_type {};
 
 template <typename T, int FLAGS, class Epi>
 hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipStream_t s) {
@@ -1290,6 +1344,13 @@ hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const
   if (r != hipSuccess) return r;
   return gemm_act_bwd<T>(opd, flags_d, e, s);
 }
+
+template <typename T>
+bool gemm_fuses_bias(const GemmOperands<T>& op, int flags) {
+  return dma_tile_kind(op) >= 0 && (flags & (G_C1 | G_AD)) != 0;
+}
+template bool gemm_fuses_bias<bf16_t>(const GemmOperands<bf16_t>&, int);
+template bool gemm_fuses_bias<float>(const GemmOperands<float>&, int);
 
 long gemm_splitk_floats(int M, int N, int K) {
   const int S = splitk_count(M, N, K);

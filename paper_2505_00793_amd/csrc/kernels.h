@@ -42,6 +42,10 @@ long gemm_splitk_floats(int M, int N, int K);
 // M x N output over K uses for split-K when given it (few output tiles, long k);
 // 0 when it runs without.
 long gemm_splitk_fwd_f32_floats(int M, int N, int K);
+// Whether the parameter GEMM of op / flags (B = dZ^T, Bd = its tangent) runs on
+// the direct-to-LDS path that can sum the bias gradients of P.fuse_bias.
+template <typename T>
+bool gemm_fuses_bias(const GemmOperands<T>& op, int flags);
 
 // Forward of one layer: z = C1 + b, zd = C2 + bd (tangent), a = act(z),
 // ad = act'(z) zd.  Hidden layers store z (and zd) in float32 for the
@@ -159,6 +163,10 @@ struct ParamArgs {
   // tangent for P_SEED_SGD_* and P_REV_SGD_*); each may be null
   T* outW; T* outWT; float* outb;
   int ldW, ldWT;
+  // set by the host when the backward-weight GEMM also finishes the bias
+  // entries (its first row of tiles sums the rows of dZ^T it stages; see
+  // gemm_fuses_bias), so that no separate reduction runs
+  int fuse_bias;
 };
 
 template <typename T>
