@@ -87,6 +87,14 @@ struct mfmg_problem {
            d.precision == MFMG_PREC_FP32 && linreg_fits(T, d.rows, d.val_rows, w[0]);
   }
   int maxR() const { return d.rows > d.val_rows ? d.rows : d.val_rows; }
+  // Contraction of the last layer's backward-data product (over its outputs):
+  // with bf16 operands the width rounded up to 8, so that the product takes the
+  // direct-to-LDS path; the loss head writes the padding columns of dZ as zero
+  // and zero_last_pads clears those of the W copies.
+  int k_last() const {
+    const int c = w[L];
+    return bf16() && L >= 2 && c % 8 != 0 ? (c + 7) / 8 * 8 : c;
+  }
 };
 
 namespace {
@@ -416,6 +424,7 @@ struct Eng {
     la.ddT = a.dZdT[0];
     la.ld = (int)p->ld(C);
     la.ldT = (int)p->ld(R);
+    la.pad_to = p->k_last();
     la.loss_rows = a.loss_rows;
     la.mvp_rows = mvp_rows;
     la.deta_rows = deta_rows;
@@ -464,7 +473,7 @@ struct Eng {
         opd.lda = opd.ldb = (int)p->ld(nout);
         opd.M = R;
         opd.N = nin;
-        opd.K = nout;
+        opd.K = l == p->L - 1 ? p->k_last() : nout;
         e.Zp = a.Z[l - 1];
         e.Zdp = a.Zd[l - 1];
         e.Ap = a.A[l - 1];
@@ -514,6 +523,33 @@ struct Eng {
     if (st_ != MFMG_OK) return st_;      \
   } while (0)
 
+// Columns w[L] .. k_last() - 1 of the last layer's W copies (the B operand of
+// its backward-data product) set to zero in every operand set of a call;
+// nothing else writes there, so they stay zero for the whole call.
+template <typename T>
+mfmg_status zero_last_pads(const mfmg_problem* p, const std::vector<const OperandSet<T>*>& sets,
+                           hipStream_t s) {
+  const int l = p->L - 1, nout = p->w[p->L], kp = p->k_last();
+  if (kp == nout) return MFMG_OK;
+  ZeroColJobs J;
+  J.n = 0;
+  for (const OperandSet<T>* o : sets) {
+    if (!o || !o->W[l]) continue;
+    if (J.n == ZC_MAX_JOBS) {
+      HIPCHK(zero_cols(J, s));
+      J.n = 0;
+    }
+    J.p[J.n] = reinterpret_cast<uint16_t*>(o->W[l]);
+    J.rows[J.n] = p->w[l];
+    J.ld[J.n] = (int)p->ld(nout);
+    J.c0[J.n] = nout;
+    J.c1[J.n] = kp;
+    ++J.n;
+  }
+  if (J.n) HIPCHK(zero_cols(J, s));
+  return MFMG_OK;
+}
+
 template <typename T>
 ParamArgs<T> param_base(const mfmg_problem* p, int mode, const float* eta) {
   ParamArgs<T> P;
@@ -548,6 +584,13 @@ mfmg_status run_meta(const mfmg_problem* p, const float* theta0, const float* op
   plan_meta(p, T_, ws, mp);
   Eng<T> E{p, s};
   const Act<T>& a = mp.act;
+  {
+    std::vector<const OperandSet<T>*> sets;
+    for (const OperandSet<T>& o : mp.slot) sets.push_back(&o);
+    sets.push_back(&mp.v[0]);
+    if (!p->adam()) sets.push_back(&mp.v[1]);
+    TRY(zero_last_pads<T>(p, sets, s));
+  }
   const bool adam = p->adam();
   const bool wlog = p->d.meta == MFMG_META_EXAMPLE_WEIGHT_LOGITS;
   const bool maml = p->d.meta == MFMG_META_MAML;
@@ -758,6 +801,7 @@ mfmg_status run_inner_step(const mfmg_problem* p, const float* theta, const floa
   StepPlan<T> sp;
   plan_step(p, ws, sp);
   Eng<T> E{p, s};
+  TRY(zero_last_pads<T>(p, {&sp.th}, s));
   const int R = (int)b->rows;
   const long n = p->n_theta;
   const float* alpha =
@@ -789,6 +833,7 @@ mfmg_status run_hvp(const mfmg_problem* p, const float* theta, const float* eta,
   StepPlan<T> sp;
   plan_step(p, ws, sp);
   Eng<T> E{p, s};
+  TRY(zero_last_pads<T>(p, {&sp.th, &sp.v}, s));
   const int R = (int)b->rows;
   const float* alpha =
       p->d.meta == MFMG_META_EXAMPLE_WEIGHT_LOGITS ? eta + (long)step * p->d.rows : nullptr;

@@ -2,6 +2,8 @@
 //
 // All are HBM- or latency-bound: 64-lane wavefront reductions, coalesced
 // row-major traffic, LDS-staged transposes where a second layout is written.
+#include <algorithm>
+
 #include "kernels.h"
 #include "param_epi.h"
 
@@ -246,6 +248,12 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
   const int lane = threadIdx.x & 63;
   if (row >= a.rows) return;
   const int C = a.C;
+  // the row's padding columns C .. pad_to - 1 of dL/dz (and its tangent) are
+  // zero, so that a product may contract over them
+  if (C + lane < a.pad_to) {
+    a.d[(long)row * a.ld + C + lane] = Elem<T>::from_float(0.0f);
+    if (a.dual) a.dd[(long)row * a.ld + C + lane] = Elem<T>::from_float(0.0f);
+  }
   const float* z = a.Z + (long)row * C;
   const float* zd = a.dual ? a.Zd + (long)row * C : nullptr;
   float w = 1.0f;
@@ -952,6 +960,17 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   for (int j = tid; j < d; j += LR_THREADS) a.d_eta[j] = eb[j];
 }
 
+// Columns c0 .. c1 - 1 of rows 0 .. rows - 1 of each job's bf16 matrix set to
+// zero; one workgroup per job and 256 rows.
+__global__ void zero_cols_kernel(ZeroColJobs J) {
+  const int j = blockIdx.y;
+  if (j >= J.n) return;
+  const int w = J.c1[j] - J.c0[j];
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < (long)J.rows[j] * w;
+       i += (long)gridDim.x * 256)
+    J.p[j][(i / w) * J.ld[j] + J.c0[j] + i % w] = 0;
+}
+
 __global__ void fill_kernel(float* p, long n, float v) {
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) p[i] = v;
 }
@@ -982,6 +1001,20 @@ hipError_t count_nonfinite(const float* x, long n, unsigned long long* count, hi
   if (n > 0)
     hipLaunchKernelGGL(count_nonfinite_kernel, dim3(min(cdiv(n, 256), 4096)), dim3(256), 0, s, x,
                        n, count);
+  return hipGetLastError();
+}
+
+hipError_t zero_cols(const ZeroColJobs& J, hipStream_t s) {
+  if (J.n < 0 || J.n > ZC_MAX_JOBS) return hipErrorInvalidValue;
+  if (J.n == 0) return hipSuccess;
+  long most = 0;
+  for (int j = 0; j < J.n; ++j) {
+    if (!J.p[j] || J.rows[j] < 0 || J.c0[j] < 0 || J.c1[j] < J.c0[j] || J.c1[j] > J.ld[j])
+      return hipErrorInvalidValue;
+    most = std::max(most, (long)J.rows[j] * (J.c1[j] - J.c0[j]));
+  }
+  if (most == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_cols_kernel, dim3(min(cdiv(most, 256), 1024), J.n), dim3(256), 0, s, J);
   return hipGetLastError();
 }
 

@@ -183,6 +183,7 @@ struct LossArgs {
   T* d; T* dT;              // dL/dz in both layouts [rows][ld], [C][ldT]
   T* dd; T* ddT;            // its tangent (dual)
   int ld, ldT;
+  int pad_to;               // columns C .. pad_to - 1 of d (dd) are written as zero
   float* loss_rows;         // l_n (unweighted), or null
   float* mvp_rows;          // (1/N) ldot_n, or null
   float* deta_rows;         // sigmoid'(eta_n) (1/N) ldot_n, or null
@@ -304,6 +305,16 @@ bool linreg_fits(int T, int rows, int vrows, int d);
 // Fill / copy float arrays with kernels (no memset or memcpy nodes, so the
 // calls stay safe inside captured HIP graphs).
 hipError_t fill(float* p, long n, float v, hipStream_t s);
+
+// Zero columns c0 .. c1 - 1 (c1 <= ld) of up to ZC_MAX_JOBS bf16 matrices in one
+// launch (a fill kernel, no memset node).
+constexpr int ZC_MAX_JOBS = 48;
+struct ZeroColJobs {
+  int n;
+  uint16_t* p[ZC_MAX_JOBS];
+  int rows[ZC_MAX_JOBS], ld[ZC_MAX_JOBS], c0[ZC_MAX_JOBS], c1[ZC_MAX_JOBS];
+};
+hipError_t zero_cols(const ZeroColJobs& J, hipStream_t s);
 hipError_t copy(const float* src, float* dst, long n, hipStream_t s);
 
 // *count (device) = number of NaN or infinite entries of x[0..n).

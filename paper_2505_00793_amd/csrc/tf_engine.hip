@@ -687,7 +687,7 @@ struct TfEng {
     la.Z = a.logits; la.Zd = a.logitsd; la.labels = a.labels; la.targets = nullptr;
     la.alpha_logits = u;
     la.d = a.dz; la.dT = a.dzT; la.dd = a.dzd; la.ddT = a.dzdT;
-    la.ld = (int)y.ld(y.V); la.ldT = (int)y.ld(N);
+    la.ld = (int)y.ld(y.V); la.ldT = (int)y.ld(N); la.pad_to = y.V;
     la.loss_rows = a.loss_rows; la.mvp_rows = mvp; la.deta_rows = ubar;
     return loss_head<T>(la, s);
   }
