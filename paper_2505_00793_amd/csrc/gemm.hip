@@ -35,11 +35,28 @@ namespace mfmg {
 namespace {
 
 
-// Sum of 8 bfloat16 values in float32, pairwise in a fixed order.
-__device__ __forceinline__ float sum8(const bf16x8& v) {
+// 16 bytes of LDS read with an explicit ds_read_b128.  The compiler makes every
+// LDS read it emits in a wave with global-to-LDS loads in flight wait for all of
+// them (it cannot tell which LDS bytes they write); this one does not, so the
+// caller must know that the bytes it reads have landed, and must wait with
+// lds_read_wait() before using the value.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 lds_read16(const void* p) {
+  const unsigned a = (unsigned)reinterpret_cast<uintptr_t>(p);   // LDS offset: low 32 bits
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  return v;
+}
+__device__ __forceinline__ void lds_read_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Sum of 8 bfloat16 values (packed in 4 dwords) in float32, pairwise in a fixed order.
+__device__ __forceinline__ float sum8(const u32x4& u) {
   float x[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) x[i] = (float)v[i];
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(u[i] << 16);
+    x[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
+  }
   return ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
 }
 
@@ -246,10 +263,15 @@ struct ParamOp {
     store_row4(P.outWT, (long)n * P.ldWT + m, cnt, v);
   }
   __device__ bool fuse_bias() const { return P.fuse_bias != 0 && P.b_off >= 0; }
-  // bias entry n from its gradient g (and H v entry hv)
-  __device__ __forceinline__ void bias(int n, float g, float hv) const {
-    const float cv = param_elem(P, P.b_off + n, g, hv);
-    if (P.outb) P.outb[n] = cv;
+  // bias entry n: its inputs (loaded ahead), then the update from its gradient g
+  // (and H v entry hv)
+  __device__ __forceinline__ void bias_load(int n, ParamIn& in) const {
+    param_load(P, P.b_off + n, 1, in);
+  }
+  __device__ __forceinline__ void bias_finish(int n, const ParamIn& in, float g, float hv) const {
+    float g4[4] = {g, 0.f, 0.f, 0.f}, h4[4] = {hv, 0.f, 0.f, 0.f}, cv[4];
+    param_finish(P, P.b_off + n, 1, in, g4, h4, cv);
+    if (P.outb) P.outb[n] = cv[0];
   }
 };
 
@@ -853,27 +875,71 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
       if constexpr (SM::LB) tB.issue(st + SM::OFF_B, k0, K, pw);
       if constexpr (SM::LBD) tBd.issue(st + SM::OFF_BD, k0, K, pw);
     };
+    // Parameter epilogues with fused bias: every tile of a tile column stages
+    // the same B rows (dZ^T, and Bd = the tangent) over all of k, so the column's
+    // BN bias entries are shared out among its tiles_m tiles.  While the
+    // computing waves multiply step kt, loader threads add up this tile's share
+    // of the B and Bd rows, btpr threads per row, each over its 16-byte chunks
+    // in their order in LDS; the btpr partial sums of a row are then combined in
+    // lane order.  The entries' epilogue inputs are loaded before the loop.
+    constexpr bool BIAS = IsParamOp<Epi>::value && SM::LB;
+    const int lt = tid - 256;
+    bool bias_w = false;
+    int brow = 0, btpr = 1, bcpt = CPR;
+    float bsum = 0.0f, bdsum = 0.0f;
+    typename Epi::In bin;
+    if constexpr (BIAS) {
+      if (bz == 0 && epi.fuse_bias()) {
+        const int tiles_m = (op.M + BM - 1) / BM;
+        const int rpt = (BN + tiles_m - 1) / tiles_m;        // bias rows per tile
+        const int r0 = (m0 / BM) * rpt, nr = min(BN, r0 + rpt) - r0;
+        if (nr > 0) {
+          btpr = CPR;
+          while (btpr > 1 && nr * btpr > 256) btpr >>= 1;
+          bcpt = CPR / btpr;
+          brow = r0 + lt / btpr;
+          bias_w = lt < nr * btpr;
+          if (bias_w && lt % btpr == 0 && n0 + brow < op.N) epi.bias_load(n0 + brow, bin);
+        }
+      }
+    }
 #pragma unroll
     for (int s = 0; s < NST - 1; ++s) issue(s);
     for (int kt = 0; kt < nk; ++kt) {
       wait_vm_lgkm<SM::LPW * (NST - 2)>();   // this wave's loads of step kt have landed
       lds_barrier();                         // ... and every other wave's
       issue(kt + NST - 1);                   // past the last step: zero loads into a dead stage
+      if constexpr (BIAS) {
+        if (bias_w) {
+          // stage kt has landed (the wait and barrier above); the loads in
+          // flight write other stages
+          const char* st = smem + (kt % NST) * SM::STAGE_BYTES;
+          const int c0 = (lt % btpr) * bcpt;
+          for (int c = 0; c < bcpt; ++c) {
+            const int off = brow * ROWB + (c0 + c) * 16;
+            const u32x4 u = lds_read16(st + SM::OFF_B + off);
+            u32x4 ud = u;
+            if constexpr (SM::LBD) ud = lds_read16(st + SM::OFF_BD + off);
+            lds_read_wait();
+            bsum += sum8(u);
+            if constexpr (SM::LBD) bdsum += sum8(ud);
+          }
+        }
+      }
+    }
+    if constexpr (BIAS) {
+      // every lane takes part in the shuffles (idle ones add zeros to each other)
+      for (int o = 1; o < btpr; o <<= 1) {
+        bsum += __shfl_xor(bsum, o, 64);
+        bdsum += __shfl_xor(bdsum, o, 64);
+      }
+      if (bias_w && lt % btpr == 0 && n0 + brow < op.N) epi.bias_finish(n0 + brow, bin, bsum, bdsum);
     }
     wait_vm_lgkm<0>();
     lds_barrier();
     lds_barrier();
   } else {
     const int wm = wave >> 1, wn = wave & 1;
-    // Parameter epilogues with fused bias: the waves of the first tile row that
-    // read the top half of A also sum the B rows (dZ^T, and Bd = its tangent)
-    // they read, in k order; the four lanes of a row then add their sums.
-    constexpr bool BIAS = IsParamOp<Epi>::value && SM::LB;
-    bool bias_w = false;
-    if constexpr (BIAS) bias_w = m0 == 0 && wm == 0 && bz == 0 && epi.fuse_bias();
-    float bsum[TN], bdsum[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bsum[j] = bdsum[j] = 0.0f;
     f32x4 acc1[TM][TN], acc2[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -927,36 +993,6 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
               if constexpr (HAD) mma(acc2[i][j], ad[f][i], b[f][j]);
               if constexpr (HBD) mma(acc2[i][j], a[f][i], bd[f][j]);
             }
-        if constexpr (BIAS) {
-          if (bias_w) {
-#pragma unroll
-            for (int f = 0; f < NF; ++f)
-#pragma unroll
-              for (int j = 0; j < TN; ++j) {
-                bsum[j] += sum8(b[f][j]);
-                if constexpr (SM::LBD) bdsum[j] += sum8(bd[f][j]);
-              }
-          }
-        }
-      }
-    }
-    if constexpr (BIAS) {
-      if (bias_w) {
-        // lanes l, l + 16, l + 32, l + 48 read the chunks of one row
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          bsum[j] += __shfl_xor(bsum[j], 16, 64);
-          bsum[j] += __shfl_xor(bsum[j], 32, 64);
-          bdsum[j] += __shfl_xor(bdsum[j], 16, 64);
-          bdsum[j] += __shfl_xor(bdsum[j], 32, 64);
-        }
-        if (lane < 16) {
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int n = n0 + wn * WTN + j * 16 + lane;
-            if (n < op.N) epi.bias(n, bsum[j], bdsum[j]);
-          }
-        }
       }
     }
     wait_vm_lgkm<0>();
