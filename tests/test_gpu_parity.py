@@ -54,7 +54,7 @@ def run_meta(cfg, inp):
 
 
 META_CASES = ["c1_small", "c1_wide", "c1_long", "c1_vec", "c2_small", "c2_splitk", "c3_fp32", "c5_tanh_fp32",
-              "c5_gelu_fp32", "c5_small", "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml",
+              "c5_gelu_fp32", "c5_small", "c5_small_long", "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml",
               "c5_maml_r8_fp32", "toy_small", "toy_mid", "c1_linreg",
               "c2_mlp_tanh_lossweights"]
 

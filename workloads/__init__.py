@@ -156,6 +156,10 @@ SMALL: Dict[str, Config] = {
                          val_rows=96, T=4),
     "c5_small": C5.with_(name="c5_small", cfg_id=105, widths=(200, 300, 260, 37), rows=130,
                          val_rows=70, T=3),
+    # 50 steps: more operand sets (51 checkpoints + 2 tangents) than one launch of
+    # the padding-zeroing kernel takes; the 37-wide output layer contracts over 40
+    "c5_small_long": C5.with_(name="c5_small_long", cfg_id=132, widths=(200, 300, 260, 37),
+                              rows=130, val_rows=70, T=50),
     "c5_tanh_fp32": C5.with_(name="c5_tanh_fp32", cfg_id=106, widths=(40, 50, 7), act=ACT_TANH,
                              precision=PREC_FP32, rows=33, val_rows=20, T=3),
     "c5_gelu_fp32": C5.with_(name="c5_gelu_fp32", cfg_id=107, widths=(40, 50, 30, 7), act=ACT_GELU,
