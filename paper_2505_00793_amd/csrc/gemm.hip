@@ -1154,9 +1154,9 @@ int splitk_count(int M, int N, int K) {
   return S;
 }
 
-// Float32 products with at most 8 output tiles of 64 x 64 and a long k (c2's
-// first layer, 128 x 256 over 784: 8 workgroups would each walk all of k): up
-// to 8 k slices, each at least 64 deep and a multiple of 4.
+// Float32 products with at most 8 output tiles of 64 x 64 and a long k (say a
+// 784-deep first layer with 128 x 256 outputs: 8 workgroups would each walk all
+// of k): up to 8 k slices, each at least 64 deep and a multiple of 4.
 int splitk_count_small(int M, int N, int K) {
   const int tiles = cdiv(M, 64) * cdiv(N, 64);
   if (M <= 0 || N <= 0 || tiles > 8 || K < 512) return 1;
@@ -1226,7 +1226,6 @@ __global__ void __launch_bounds__(256) splitk_epilogue(const float* __restrict__
   }
 }
 
-
 template <typename T, int FLAGS, class Epi>
 hipError_t launch_splitk(const GemmOperands<T>& op, const Epi& epi, int S, hipStream_t s) {
   constexpr bool HC2 = (FLAGS & (G_AD | G_BD)) != 0;
@@ -1275,8 +1274,8 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
     // 128 x 64 on the direct-to-LDS path (each compute unit then loads 128 + 64
     // rows per k step for 8192 outputs against 2 x 128 for two 64 x 64 tiles),
     // else 64 x 64, or 64 x 32 on the direct-to-LDS path when 64 x 64 tiles
-    // would still leave compute units idle (c3's 512-row products: 256
-    // workgroups instead of 128, 5.8 instead of 6.3 ms per meta-gradient).
+    // would still leave compute units idle (512 x 1024 products: 256
+    // workgroups instead of 128).
     if (cdiv(op.M, 128) * cdiv(op.N, 128) * op.batch >= 192)
       return launch<T, FLAGS, 128, 128>(op, epi, s);
     if (cdiv(op.M, 128) * cdiv(op.N, 64) * op.batch >= 192 && dma_ok(op))
