@@ -107,7 +107,7 @@ extern "C" {
 typedef enum {
   MFMG_OK = 0,
   MFMG_ERR_INVALID_ARGUMENT = 1, /* a null/misaligned pointer, a bad size or shape */
-  MFMG_ERR_UNSUPPORTED = 2,      /* a valid combination this build does not implement */
+  MFMG_ERR_UNSUPPORTED = 2,      /* a valid combination the library does not implement */
   MFMG_ERR_WORKSPACE = 3,        /* ws_bytes smaller than mfmg_query_sizes reports */
   MFMG_ERR_HIP = 4,              /* a HIP runtime call failed while enqueueing */
   MFMG_ERR_NUMERIC = 5           /* mfmg_check_finite found a NaN or an infinity */
@@ -216,7 +216,7 @@ typedef struct {
 
 /* Validates `desc` and creates an immutable problem handle.  The handle holds
  * host memory only and may be shared by threads.  INVALID_ARGUMENT for a bad
- * description, UNSUPPORTED for a valid one this build does not implement. */
+ * description, UNSUPPORTED for a valid one the library does not implement. */
 mfmg_status mfmg_problem_create(const mfmg_problem_desc* desc, mfmg_problem_t* out);
 
 /* Releases a handle (NULL is ignored). */

@@ -94,7 +94,7 @@ class Config:
 
 
 # --------------------------------------------------------------------------------------
-# The five workloads.  Readings of unstated details are recorded in the design doc.
+# The five workloads (sizes, activations, losses and meta-parameters of each).
 # --------------------------------------------------------------------------------------
 C1 = Config(name="c1_linreg", cfg_id=1, widths=(64, 1), act=ACT_NONE, loss=LOSS_MSE,
             optimizer=OPT_SGD, meta=META_LOGLR_PER_PARAM, precision=PREC_FP32, has_bias=False,
