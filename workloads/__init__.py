@@ -156,6 +156,11 @@ SMALL: Dict[str, Config] = {
                          val_rows=96, T=4),
     "c5_small": C5.with_(name="c5_small", cfg_id=105, widths=(200, 300, 260, 37), rows=130,
                          val_rows=70, T=3),
+    # a tall first layer: its backward-weight product has more tile rows (65 of
+    # 64) than bias entries per tile column (24), so each tile sums at most one
+    # bias row and some none
+    "c5_tall": C5.with_(name="c5_tall", cfg_id=133, widths=(4104, 24, 10), rows=64, val_rows=40,
+                        T=2),
     # 50 steps: more operand sets (51 checkpoints + 2 tangents) than one launch of
     # the padding-zeroing kernel takes; the 37-wide output layer contracts over 40
     "c5_small_long": C5.with_(name="c5_small_long", cfg_id=132, widths=(200, 300, 260, 37),
