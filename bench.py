@@ -415,36 +415,6 @@ def cpu_baseline(cfg: W.Config, inp: dict, runs: int = 1):
                        f"{', '.join(f'{t:.2f}' for t in times)} s")}
 
 
-def cpu_baseline_sampled(cfg: W.Config, inp: dict):
-    """The float64 oracle on a bounded sample of a workload too slow to run whole
-    on the host: one forward inner step (with the validation loss), the
-    validation seed and one reverse step at full size, extrapolated to T."""
-    import torch
-    from oracle.metagrad import _Inputs, reverse_step, seed, unroll
-    T = len(inp["train_x"])
-    one = dict(inp)
-    one["train_x"], one["train_y"] = inp["train_x"][:1], inp["train_y"][:1]
-    if cfg.meta == W.META_EXAMPLE_WEIGHT_LOGITS:
-        one["eta"] = inp["eta"][:cfg.rows]
-    c1 = cfg.with_(T=1)
-    I = _Inputs(c1, one)
-    t0 = time.perf_counter()
-    thetas, opts, _, _ = unroll(c1, one)
-    t1 = time.perf_counter()
-    V, thbar = seed(c1, I, thetas[-1], False)
-    t2 = time.perf_counter()
-    reverse_step(c1, I, 0, thetas[0], opts[0], thbar,
-                 None if opts[-1] is None else torch.zeros_like(opts[-1]), False)
-    t3 = time.perf_counter()
-    per = T * ((t1 - t0) + (t3 - t2)) + (t2 - t1)
-    return {"value": 1.0 / per, "unit": "meta-gradients/s", "cores": torch.get_num_threads(),
-            "kind": "oracle", "measured": False, "cpu": cpu_model(),
-            "sample": (f"float64 oracle at full size: one inner step with the validation loss "
-                       f"({t1 - t0:.2f} s), the validation seed ({t2 - t1:.2f} s) and one "
-                       f"reverse step ({t3 - t2:.2f} s), extrapolated to T={T}: {per:.1f} s "
-                       f"per meta-gradient")}
-
-
 WORKLOADS = {
     "c1_linreg": "linear regression 64 features, 256 rows, per-parameter log learning rates, fp32",
     "c2_mlp_tanh_lossweights": ("MLP 784-256-10 tanh, CE, 128 rows, SGD lr 0.1, per-example loss "
@@ -503,12 +473,11 @@ def bench_config(name: str, args):
     cpu = None
     if not args.no_cpu_baseline and torch.cuda.is_available():
         inp = W.make_inputs(cfg)
-        if name in ("c1_linreg", "c2_mlp_tanh_lossweights", "c3_mlp_gelu_adam"):
-            log(f"[bench] {name}: cpu baseline, 3 whole float64 oracle meta-gradients")
-            cpu = cpu_baseline(cfg, inp, runs=3)
-        else:
-            log(f"[bench] {name}: cpu baseline, float64 oracle sample")
-            cpu = cpu_baseline_sampled(cfg, inp)
+        # three whole float64 oracle meta-gradients of the small workloads, one of
+        # the large ones (about a minute on 16 host cores)
+        runs = 3 if name in ("c1_linreg", "c2_mlp_tanh_lossweights", "c3_mlp_gelu_adam") else 1
+        log(f"[bench] {name}: cpu baseline, {runs} whole float64 oracle meta-gradient(s)")
+        cpu = cpu_baseline(cfg, inp, runs=runs)
     print(json.dumps({
         "metric": "meta-gradients/sec on 1 MI355X", "value": round(1e3 / ms, 4),
         "unit": "meta-gradients/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
