@@ -720,38 +720,54 @@ __device__ __forceinline__ float quad_sum(float v) {
 
 // r[n] = X[n] . w - y[n] (and rd[n] = X[n] . u when DU).  Staged batches: four
 // threads per row, thread q taking 16-byte groups q, q + 4, ... of the row (w
-// and u zero past d, like the row's padding); batches in global memory: one
+// and u zero past d, like the row's padding), and two rows (n and n + 128) per
+// thread at once, sharing the reads of w and u; batches in global memory: one
 // thread per row.  Returns this thread's share of sum_n r[n]^2.
 template <bool DU>
 __device__ float lr_rows_staged(const float* X, int P, const float* y, const float* w,
                                 const float* u, int rows, int d, float* r, float* rd) {
+  constexpr int RPP = LR_THREADS / 4;   // rows per pass and half
   const int q = threadIdx.x & 3;
   const int g4 = (d + 3) >> 2;
+  const float4* w4 = reinterpret_cast<const float4*>(w);
+  const float4* u4 = reinterpret_cast<const float4*>(u);
   float sq = 0.0f;
-  for (int nb = 0; nb < rows; nb += LR_THREADS / 4) {
-    const int n = nb + (threadIdx.x >> 2);
-    float s = 0.0f, sd = 0.0f;
-    if (n < rows) {
-      const float4* xr = reinterpret_cast<const float4*>(X + n * P);
-      const float4* w4 = reinterpret_cast<const float4*>(w);
-      const float4* u4 = reinterpret_cast<const float4*>(u);
+  for (int nb = 0; nb < rows; nb += 2 * RPP) {
+    const int n0 = nb + (threadIdx.x >> 2), n1 = n0 + RPP;
+    // rows past the end read the last row; their sums are not used
+    const float4* x0 = reinterpret_cast<const float4*>(X + min(n0, rows - 1) * P);
+    const float4* x1 = reinterpret_cast<const float4*>(X + min(n1, rows - 1) * P);
+    float s0 = 0.0f, s1 = 0.0f, sd0 = 0.0f, sd1 = 0.0f;
 #pragma unroll 2
-      for (int j = q; j < g4; j += 4) {
-        const float4 x = xr[j], ww = w4[j];
-        s += x.x * ww.x + x.y * ww.y + x.z * ww.z + x.w * ww.w;
-        if (DU) {
-          const float4 uu = u4[j];
-          sd += x.x * uu.x + x.y * uu.y + x.z * uu.z + x.w * uu.w;
-        }
+    for (int j = q; j < g4; j += 4) {
+      const float4 ww = w4[j], a = x0[j], b = x1[j];
+      s0 += a.x * ww.x + a.y * ww.y + a.z * ww.z + a.w * ww.w;
+      s1 += b.x * ww.x + b.y * ww.y + b.z * ww.z + b.w * ww.w;
+      if (DU) {
+        const float4 uu = u4[j];
+        sd0 += a.x * uu.x + a.y * uu.y + a.z * uu.z + a.w * uu.w;
+        sd1 += b.x * uu.x + b.y * uu.y + b.z * uu.z + b.w * uu.w;
       }
     }
-    s = quad_sum(s);
-    if (DU) sd = quad_sum(sd);
-    if (n < rows && q == 0) {
-      const float res = s - y[n];
-      r[n] = res;
-      if (DU) rd[n] = sd;
-      sq += res * res;
+    s0 = quad_sum(s0);
+    s1 = quad_sum(s1);
+    if (DU) {
+      sd0 = quad_sum(sd0);
+      sd1 = quad_sum(sd1);
+    }
+    if (q == 0) {
+      if (n0 < rows) {
+        const float res = s0 - y[n0];
+        r[n0] = res;
+        if (DU) rd[n0] = sd0;
+        sq += res * res;
+      }
+      if (n1 < rows) {
+        const float res = s1 - y[n1];
+        r[n1] = res;
+        if (DU) rd[n1] = sd1;
+        sq += res * res;
+      }
     }
   }
   __syncthreads();
