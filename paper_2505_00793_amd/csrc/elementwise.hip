@@ -648,11 +648,12 @@ struct LrRegs {
   float x[LR_PF];   // vec: group u in x[4u .. 4u + 3]
   float y[LR_YPT];
 };
-__device__ __forceinline__ void lr_load(const LrBatch& b, int d, bool vec, LrRegs& g) {
+template <bool VEC>
+__device__ __forceinline__ void lr_load(const LrBatch& b, int d, LrRegs& g) {
   const int tid = threadIdx.x;
   if (lr_staged(b.rows, d)) {
     const int n = b.rows * d;
-    if (vec) {
+    if constexpr (VEC) {
       const float4* X4 = reinterpret_cast<const float4*>(b.X);
 #pragma unroll
       for (int u = 0; u < LR_PF4; ++u) {
@@ -669,8 +670,9 @@ __device__ __forceinline__ void lr_load(const LrBatch& b, int d, bool vec, LrReg
 }
 // Registers -> LDS (padded rows; the padding columns stay zero).  Callers
 // synchronise before (the previous batch's readers are done) and after.
-__device__ __forceinline__ void lr_commit(const LrBatch& b, int d, bool vec, const LrRegs& g,
-                                          float* stage, float* ys) {
+template <bool VEC>
+__device__ __forceinline__ void lr_commit(const LrBatch& b, int d, const LrRegs& g, float* stage,
+                                          float* ys) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int v = 0; v < LR_YPT; ++v)
@@ -679,7 +681,7 @@ __device__ __forceinline__ void lr_commit(const LrBatch& b, int d, bool vec, con
   const int n = b.rows * d, P = lr_spitch(d);
   // element i = row * d + col goes to row * P + col; row and col advance by the
   // elements of one step without a division
-  if (vec) {
+  if constexpr (VEC) {
     const int st = 4 * LR_THREADS;
     const int qd = st / d, rd = st - qd * d;
     int row = 4 * tid / d, col = 4 * tid - row * d;
@@ -895,6 +897,11 @@ __device__ float lr_pass(const LrBatch& b, int d, const float* stage, const floa
   return sq;
 }
 
+// VEC: every batch 16-byte aligned and d % 4 == 0 (16-byte prefetch loads).  The
+// two forms are separate kernels so that the prefetch has one load site, whose
+// registers the compiler then carries across the phase without copying them
+// (a copy would wait for the loads it was meant to overlap).
+template <bool VEC>
 __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __shared__ __attribute__((aligned(16))) float stage[LR_STAGE];
   __shared__ float ck[LR_CKPT];
@@ -906,10 +913,9 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   __shared__ __attribute__((aligned(16))) float part[NPART], part2[NPART];
   __shared__ float red[LR_THREADS / 64];
   const int tid = threadIdx.x, d = a.d, T = a.T;
-  const bool vec = a.vec != 0;
   const bool ck_lds = (long)(T + 1) * d <= LR_CKPT;
   LrRegs g;
-  lr_load(lr_batch(a, 0), d, vec, g);
+  lr_load<VEC>(lr_batch(a, 0), d, g);
   {
     // the columns d .. (d rounded up to 4) - 1 of every row that can be staged
     // stay zero (the 16-byte groups of the residual pass read them)
@@ -937,8 +943,8 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
       }
     }
     __syncthreads();   // the previous batch's readers are done; th, vv published
-    lr_commit(b, d, vec, g, stage, ys);
-    if (k < 2 * T) lr_load(lr_batch(a, k + 1), d, vec, g);   // in flight during this phase
+    lr_commit<VEC>(b, d, g, stage, ys);
+    if (k < 2 * T) lr_load<VEC>(lr_batch(a, k + 1), d, g);   // in flight during this phase
     __syncthreads();
     const float inv = 2.0f / b.rows;
     if (k < T) {
@@ -1204,7 +1210,10 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   a.d_eta = d_eta;
   a.val_loss = val_loss;
   a.ckpt = scratch;
-  hipLaunchKernelGGL(linreg_kernel, dim3(1), dim3(LR_THREADS), 0, s, a);
+  if (a.vec)
+    hipLaunchKernelGGL(linreg_kernel<true>, dim3(1), dim3(LR_THREADS), 0, s, a);
+  else
+    hipLaunchKernelGGL(linreg_kernel<false>, dim3(1), dim3(LR_THREADS), 0, s, a);
   return hipGetLastError();
 }
 
