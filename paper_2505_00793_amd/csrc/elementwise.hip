@@ -982,6 +982,198 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_kernel(LinregArgs a) {
   for (int j = tid; j < d; j += LR_THREADS) a.d_eta[j] = eb[j];
 }
 
+// The same meta-gradient with each batch held in registers, for d <= 64 with
+// d % 4 == 0, at most 256 rows in every batch and 16-byte aligned batches.
+// Thread (q, c) = (tid / 16, tid % 16) holds the 16-byte group c of rows q,
+// q + 32, .., q + 224 (32 registers); the 16 groups of a row lie in one DPP row
+// of 16 lanes, which sums the row's dot products with rotations, so a residual
+// needs neither LDS nor a barrier and every lane of the row receives it.  X^T r
+// is summed over the thread's eight rows in registers, then over the 32 row
+// slots in LDS, in a fixed order.  The next batch is loaded into a second set
+// of registers one group per residual, between the residuals of the current
+// batch: a compute unit takes in only ~20 bytes per clock, and a whole batch
+// requested at once stalls every wave at the load instructions until most of
+// it has arrived, whereas spread out the loads run under the arithmetic.
+constexpr int LRR_RPT = 8;                          // rows per thread
+constexpr int LRR_SLOTS = LR_THREADS / 16;          // row slots (32)
+constexpr int LRR_MAXROWS = LRR_SLOTS * LRR_RPT;    // 256
+constexpr int LRR_MAXD = 64;
+
+struct LrrRegs {
+  float4 x[LRR_RPT];  // group c of rows q + 32 u
+  float y;            // y of row q + 32 (c % 8)
+};
+struct LrrSrc {
+  const float4* x;
+  const float* y;
+  int n4, rows;
+};
+template <bool B>
+struct LrrLoad {
+  static constexpr bool value = B;
+};
+
+__device__ __forceinline__ LrrSrc lrr_src(const LrBatch& b, int g4) {
+  return {reinterpret_cast<const float4*>(b.X), b.y, b.rows * g4, b.rows};
+}
+// Loads past the end read the last element (never cleared registers, see LrRegs).
+__device__ __forceinline__ float4 lrr_group(const LrrSrc& s, int g4, int q, int c, int u) {
+  return s.x[min((q + LRR_SLOTS * u) * g4 + c, s.n4 - 1)];
+}
+__device__ __forceinline__ float lrr_target(const LrrSrc& s, int q, int c) {
+  return s.y[min(q + LRR_SLOTS * (c & 7), s.rows - 1)];
+}
+__device__ __forceinline__ float dot4(const float4& a, const float4& b) {
+  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+}
+// Sum over the 16 lanes of a DPP row.  Every lane gets the same bits: each step
+// adds two values that the partner lane adds in the other order.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, true));  // row_ror:8
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, true));  // row_ror:4
+  return quad_sum(v);
+}
+
+// CKL: the checkpoints fit in LDS ((T + 1) d <= 4096).  A compile-time choice,
+// since a runtime one merges the two checkpoint reads into one flat load, which
+// waits for every global load in flight, the next batch's included.
+template <bool CKL>
+__global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
+  __shared__ float ck[CKL ? LR_CKPT : 1];
+  __shared__ __attribute__((aligned(16))) float th[LRR_MAXD], vv[LRR_MAXD];
+  __shared__ float tb[LRR_MAXD], lam[LRR_MAXD], eb[LRR_MAXD];
+  __shared__ __attribute__((aligned(16))) float part[LRR_SLOTS * LRR_MAXD];
+  __shared__ __attribute__((aligned(16))) float part2[LRR_SLOTS * LRR_MAXD];
+  __shared__ float red[LR_THREADS / 64];
+  const int tid = threadIdx.x, d = a.d, T = a.T, g4 = d >> 2;
+  const int c = tid & 15, q = tid >> 4;
+  // theta_0 and eta, then the first batch; the set-up waits for the former only
+  const float th0 = a.theta0[min(tid, d - 1)], et = a.eta[min(tid, d - 1)];
+  LrrRegs A, B;
+  {
+    const LrrSrc s0 = lrr_src(lr_batch(a, 0), g4);
+    A.y = lrr_target(s0, q, c);
+#pragma unroll
+    for (int u = 0; u < LRR_RPT; ++u) A.x[u] = lrr_group(s0, g4, q, c, u);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < LRR_MAXD) {
+    const bool in = tid < d;
+    th[tid] = in ? th0 : 0.0f;   // zero past d, like vv: the groups past d add nothing
+    vv[tid] = 0.0f;
+    lam[tid] = in ? expf(et) : 0.0f;
+    eb[tid] = 0.0f;
+    if (in) {
+      if constexpr (CKL) ck[tid] = th0;
+      else a.ckpt[tid] = th0;
+    }
+  }
+  __syncthreads();
+
+  // Phase k of the sweep on the batch in cur; with LOAD, batch k + 1 into nxt.
+  auto phase = [&](int k, const LrrRegs& cur, LrrRegs& nxt, auto load) {
+    constexpr bool LOAD = decltype(load)::value;
+    const LrBatch b = lr_batch(a, k);
+    const bool du = k > T;
+    const float4 w4 = reinterpret_cast<const float4*>(th)[c];
+    const float4 u4 = reinterpret_cast<const float4*>(vv)[c];
+    LrrSrc ns{};
+    if constexpr (LOAD) {
+      ns = lrr_src(lr_batch(a, k + 1), g4);
+      nxt.y = lrr_target(ns, q, c);
+    }
+    // residuals r = X th - y (and rd = X vv); lane u of the row holds y of row u
+    float r[LRR_RPT], rd[LRR_RPT], sq = 0.0f;
+    const bool in = c < g4;
+#pragma unroll
+    for (int u = 0; u < LRR_RPT; ++u) {
+      if constexpr (LOAD) nxt.x[u] = lrr_group(ns, g4, q, c, u);
+      const float4 x = cur.x[u];
+      const bool valid = q + LRR_SLOTS * u < b.rows;
+      float s = in ? dot4(x, w4) : 0.0f;
+      s -= c == u ? cur.y : 0.0f;
+      s = row16_sum(s);
+      r[u] = valid ? s : 0.0f;
+      sq += r[u] * r[u];
+      if (du) {
+        const float sd = row16_sum(in ? dot4(x, u4) : 0.0f);
+        rd[u] = valid ? sd : 0.0f;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // X^T r (and X^T rd) over this thread's rows, then over the row slots
+    float4 ga = make_float4(0.f, 0.f, 0.f, 0.f), ha = ga;
+#pragma unroll
+    for (int u = 0; u < LRR_RPT; ++u) {
+      const float4 x = cur.x[u];
+      ga.x += x.x * r[u]; ga.y += x.y * r[u]; ga.z += x.z * r[u]; ga.w += x.w * r[u];
+      if (du) {
+        ha.x += x.x * rd[u]; ha.y += x.y * rd[u]; ha.z += x.z * rd[u]; ha.w += x.w * rd[u];
+      }
+    }
+    reinterpret_cast<float4*>(part)[q * 16 + c] = ga;
+    if (du) reinterpret_cast<float4*>(part2)[q * 16 + c] = ha;
+    if (k == T) {
+      const float v = wave_sum(c == 0 ? sq : 0.0f);
+      if ((tid & 63) == 0) red[tid >> 6] = v;
+    }
+    __syncthreads();
+    if (tid < 4 * LRR_MAXD) {
+      // column j, row slots 8h .. 8h + 7 in order, then across the quad
+      const int j = tid >> 2, h = tid & 3;
+      float g = 0.0f, hv = 0.0f;
+#pragma unroll
+      for (int i = 0; i < LRR_SLOTS / 4; ++i) {
+        g += part[(h * (LRR_SLOTS / 4) + i) * LRR_MAXD + j];
+        if (du) hv += part2[(h * (LRR_SLOTS / 4) + i) * LRR_MAXD + j];
+      }
+      g = quad_sum(g);
+      if (du) hv = quad_sum(hv);
+      const float inv = 2.0f / b.rows;
+      if (h == 0 && j < d) {
+        if (k < T) {
+          // forward step k: theta_{k+1}
+          const float t = th[j] - lam[j] * inv * g;
+          th[j] = t;
+          if constexpr (CKL) ck[(k + 1) * d + j] = t;
+          else a.ckpt[(long)(k + 1) * d + j] = t;
+        } else {
+          // validation: bar theta_T = dV/dtheta_T; reverse step i = 2T - k:
+          // bar eta += -exp(eta) g_i bar theta_{i+1}; bar theta_i = bar theta_{i+1} + H v
+          float t;
+          if (k == T) {
+            t = inv * g;
+          } else {
+            t = tb[j];
+            eb[j] += -lam[j] * inv * g * t;
+            t += inv * hv;
+          }
+          tb[j] = t;
+          const int i = 2 * T - k;
+          if (i >= 1) {   // the next reverse step's theta_{i-1} and v = -exp(eta) bar theta_i
+            if constexpr (CKL) th[j] = ck[(i - 1) * d + j];
+            else th[j] = a.ckpt[(long)(i - 1) * d + j];
+            vv[j] = -lam[j] * t;
+          }
+        }
+      }
+      if (k == T && tid == 0 && a.val_loss) {
+        float ls = 0.0f;
+        for (int w = 0; w < LR_THREADS / 64; ++w) ls += red[w];
+        *a.val_loss = ls / b.rows;
+      }
+    }
+    __syncthreads();
+  };
+
+  for (int k = 0; k < 2 * T; k += 2) {
+    phase(k, A, B, LrrLoad<true>{});
+    phase(k + 1, B, A, LrrLoad<true>{});
+  }
+  phase(2 * T, A, B, LrrLoad<false>{});
+  if (tid < d) a.d_eta[tid] = eb[tid];
+}
+
 // Columns c0 .. c1 - 1 of rows 0 .. rows - 1 of each job's bf16 matrix set to
 // zero; one workgroup per job and 256 rows.
 __global__ void zero_cols_kernel(ZeroColJobs J) {
@@ -1210,7 +1402,12 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   a.d_eta = d_eta;
   a.val_loss = val_loss;
   a.ckpt = scratch;
-  if (a.vec)
+  if (a.vec && d <= LRR_MAXD && rows <= LRR_MAXROWS && vrows <= LRR_MAXROWS) {
+    if ((T + 1) * d <= LR_CKPT)
+      hipLaunchKernelGGL(linreg_reg_kernel<true>, dim3(1), dim3(LR_THREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL(linreg_reg_kernel<false>, dim3(1), dim3(LR_THREADS), 0, s, a);
+  } else if (a.vec)
     hipLaunchKernelGGL(linreg_kernel<true>, dim3(1), dim3(LR_THREADS), 0, s, a);
   else
     hipLaunchKernelGGL(linreg_kernel<false>, dim3(1), dim3(LR_THREADS), 0, s, a);

@@ -53,10 +53,10 @@ def run_meta(cfg, inp):
     return d.cpu().numpy().astype(np.float64), float(vl.item()), peak
 
 
-META_CASES = ["c1_small", "c1_wide", "c1_long", "c1_vec", "c2_small", "c2_splitk", "c3_fp32",
-              "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c5_small_long", "c5_tall", "c3_small",
-              "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml", "c5_maml_r8_fp32",
-              "toy_small", "toy_mid", "c1_linreg", "c2_mlp_tanh_lossweights"]
+META_CASES = ["c1_small", "c1_wide", "c1_long", "c1_vec", "c1_reg", "c1_reg_long", "c2_small",
+              "c2_splitk", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c5_small_long",
+              "c5_tall", "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml",
+              "c5_maml_r8_fp32", "toy_small", "toy_mid", "c1_linreg", "c2_mlp_tanh_lossweights"]
 
 
 def start_of(cfg, inp):

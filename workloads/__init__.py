@@ -146,6 +146,12 @@ SMALL: Dict[str, Config] = {
     "c1_long": C1.with_(name="c1_long", cfg_id=128, rows=120, val_rows=128, T=33, widths=(131, 1)),
     # 16-byte loads (d % 4 == 0) whose steps wrap rows; the validation batch is unstaged
     "c1_vec": C1.with_(name="c1_vec", cfg_id=129, rows=150, val_rows=200, T=4, widths=(100, 1)),
+    # batches held in registers (d <= 64, d % 4 == 0, at most 256 rows): partial
+    # 16-lane rows (9 of 16 groups) and partial row slots in training and validation
+    "c1_reg": C1.with_(name="c1_reg", cfg_id=134, rows=200, val_rows=250, T=5, widths=(36, 1)),
+    # registers with the checkpoints in global memory ((T + 1) d > 4096)
+    "c1_reg_long": C1.with_(name="c1_reg_long", cfg_id=135, rows=40, val_rows=24, T=64,
+                            widths=(64, 1)),
     "c2_small": C2.with_(name="c2_small", cfg_id=102, widths=(150, 70, 13), rows=70, val_rows=90, T=3),
     # a float32 first layer with a long contraction and few output tiles: the
     # training forward products run split-K (8 slices of 76), the validation
