@@ -74,22 +74,40 @@ template <typename T> struct Frag;
 template <> struct Frag<bf16_t> { typedef bf16x8 type; };
 template <> struct Frag<float> { typedef f32x4 type; };
 
-// 16 bytes of row gr starting at column gk, zero outside [0,M) x [0,K).
-template <typename T>
+// 16 bytes of row gr starting at column gk of an operand with M >= 1 rows of
+// K >= 1 elements.  Every lane loads, from indices clamped into the operand:
+// with KVEC (K a multiple of the chunk width, so that a chunk lies wholly
+// inside or outside K) one 16-byte load, else single elements; the parts
+// outside [0,M) x [0,K) are zeroed by mask_chunk when the chunk is stored.
+// With no branch around a load the compiler never waits for all loads in
+// flight to merge the registers of two paths, and with the form a template
+// parameter it cannot fold the 16-byte load into the element loads.
+template <typename T, bool KVEC>
 __device__ __forceinline__ uint4 load_chunk(const T* __restrict__ src, int gr, int gk, int M,
                                             int K, int ld) {
   constexpr int VE = Elem<T>::VE;
-  if (gr < M && gk + VE <= K) return *reinterpret_cast<const uint4*>(src + (long)gr * ld + gk);
+  const long row = (long)min(gr, M - 1) * ld;
+  if constexpr (KVEC) return *reinterpret_cast<const uint4*>(src + row + min(gk, K - VE));
   union {
     uint4 v;
     T e[VE];
   } u;
-  u.v = make_uint4(0, 0, 0, 0);
-  if (gr < M) {
 #pragma unroll
-    for (int e = 0; e < VE; ++e)
-      if (gk + e < K) u.e[e] = src[(long)gr * ld + gk + e];
-  }
+  for (int e = 0; e < VE; ++e) u.e[e] = src[row + min(gk + e, K - 1)];
+  return u.v;
+}
+template <typename T, bool KVEC>
+__device__ __forceinline__ uint4 mask_chunk(const uint4& v, int gr, int gk, int M, int K) {
+  constexpr int VE = Elem<T>::VE;
+  if constexpr (KVEC) return gr < M && gk < K ? v : make_uint4(0, 0, 0, 0);
+  union {
+    uint4 v;
+    T e[VE];
+  } u;
+  u.v = v;
+  const T z = T(0);
+#pragma unroll
+  for (int e = 0; e < VE; ++e) u.e[e] = gr < M && gk + e < K ? u.e[e] : z;
   return u.v;
 }
 
@@ -595,7 +613,8 @@ __device__ __forceinline__ void run_epilogue(const f32x4 (&acc1)[BM / 32][BN / 3
 // k step into registers while the current one is multiplied, then stores them
 // to the other LDS buffer.  Handles any K, leading dimension and element type.
 // ------------------------------------------------------------------------------------
-template <typename T, int FLAGS, int BM, int BN, int BK, class Epi>
+// KVEC: K is a multiple of the 16-byte chunk width (see load_chunk).
+template <typename T, int FLAGS, int BM, int BN, int BK, class Epi, bool KVEC>
 __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   typedef Smem<T, FLAGS, BM, BN, BK> SM;
   constexpr int VE = Elem<T>::VE;
@@ -641,7 +660,8 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
         int ch = tid + c * 256;
-        ra[s][c] = load_chunk<T>(src, m0 + ch / CPR, k0 + (ch % CPR) * VE, op.M, op.K, op.lda);
+        ra[s][c] = load_chunk<T, KVEC>(src, m0 + ch / CPR, k0 + (ch % CPR) * VE, op.M, op.K,
+                                       op.lda);
       }
     }
 #pragma unroll
@@ -650,18 +670,20 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 #pragma unroll
       for (int c = 0; c < BCH; ++c) {
         int ch = tid + c * 256;
-        rb[s][c] = load_chunk<T>(src, n0 + ch / CPR, k0 + (ch % CPR) * VE, op.N, op.K, op.ldb);
+        rb[s][c] = load_chunk<T, KVEC>(src, n0 + ch / CPR, k0 + (ch % CPR) * VE, op.N, op.K,
+                                       op.ldb);
       }
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int buf, int k0) {
     T* base = smem + buf * STAGE;
 #pragma unroll
     for (int s = 0; s < NAS; ++s)
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
         int ch = tid + c * 256;
-        *reinterpret_cast<uint4*>(base + (s * BM + ch / CPR) * LDL + (ch % CPR) * VE) = ra[s][c];
+        *reinterpret_cast<uint4*>(base + (s * BM + ch / CPR) * LDL + (ch % CPR) * VE) =
+            mask_chunk<T, KVEC>(ra[s][c], m0 + ch / CPR, k0 + (ch % CPR) * VE, op.M, op.K);
       }
 #pragma unroll
     for (int s = 0; s < NBS; ++s)
@@ -669,7 +691,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
       for (int c = 0; c < BCH; ++c) {
         int ch = tid + c * 256;
         *reinterpret_cast<uint4*>(base + (NAS * BM + s * BN + ch / CPR) * LDL + (ch % CPR) * VE) =
-            rb[s][c];
+            mask_chunk<T, KVEC>(rb[s][c], n0 + ch / CPR, k0 + (ch % CPR) * VE, op.N, op.K);
       }
   };
 
@@ -683,8 +705,8 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
     }
 
   const int nk = (op.K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
+  if (op.K > 0) gload(0);   // with K = 0 every chunk is masked to zero
+  sstore(0, 0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
@@ -718,7 +740,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
           if constexpr (HBD) mma(acc2[i][j], a[i], bd[j]);
         }
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+    if (kt + 1 < nk) sstore(buf ^ 1, (kt + 1) * BK);
     __syncthreads();
   }
   run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem_raw, m0, n0, bz, epi);
@@ -1129,8 +1151,12 @@ hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
   }
   if constexpr (BN >= 64) {
     constexpr int BK = KDepth<FLAGS, Epi>::value;
-    hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi>), dim3(tiles, op.batch), dim3(256), 0, s,
-                       op, epi);
+    if (op.K % Elem<T>::VE == 0)
+      hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi, true>), dim3(tiles, op.batch),
+                         dim3(256), 0, s, op, epi);
+    else
+      hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi, false>), dim3(tiles, op.batch),
+                         dim3(256), 0, s, op, epi);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;
