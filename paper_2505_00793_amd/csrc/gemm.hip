@@ -206,6 +206,43 @@ struct ActBwdOp {
       for (int it = 0; it < NIT; ++it) ld4v(e.Zdp, (long)(m + it * dm) * e.N + n, in[it].zd);
     }
   }
+  // Any tile: indices clamped into the M x N output (the values past its edges
+  // are loaded but never used); 16-byte loads when N is a multiple of 4.
+  template <int NIT>
+  __device__ __forceinline__ void load_rows_clamped(int bz, int m, int dm, int n,
+                                                    In (&in)[NIT]) const {
+    if (aligned() && (N & 3) == 0) {
+      const int nc = min(n, N - 4);
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const long r = min(m + it * dm, M - 1);
+        if (!e.Zp) {
+          ld_act4(r * e.ldAp + nc, in[it].z);
+          in[it].zd[0] = in[it].zd[1] = in[it].zd[2] = in[it].zd[3] = 0.f;
+        } else {
+          ld4v(e.Zp, r * e.N + nc, in[it].z);
+          if (e.dual) ld4v(e.Zdp, r * e.N + nc, in[it].zd);
+          else in[it].zd[0] = in[it].zd[1] = in[it].zd[2] = in[it].zd[3] = 0.f;
+        }
+      }
+      return;
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const long r = min(m + it * dm, M - 1);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int nk = min(n + k, N - 1);
+        if (!e.Zp) {   // ReLU: the sign of the activation
+          in[it].z[k] = Elem<T>::to_float(e.Ap[r * e.ldAp + nk]);
+          in[it].zd[k] = 0.f;
+        } else {
+          in[it].z[k] = e.Zp[r * e.N + nk];
+          in[it].zd[k] = e.dual ? e.Zdp[r * e.N + nk] : 0.f;
+        }
+      }
+    }
+  }
   __device__ __forceinline__ void row_in(int bz, int m, int n, int cnt, const In& in,
                                          const float* c1, const float* c2, float* t1,
                                          float* t2) const {
@@ -259,6 +296,28 @@ struct ParamOp {
 #pragma unroll
         for (int it = 0; it < NIT; ++it)
           ld4v(src[s], P.w_off + (long)(m + it * dm) * P.nout + n, in[it].x[s]);
+      }
+  }
+  template <int NIT>
+  __device__ __forceinline__ void load_rows_clamped(int bz, int m, int dm, int n,
+                                                    ParamIn (&in)[NIT]) const {
+    const float* src[3];
+    param_sources(P, src);
+    const bool al = aligned() && (N & 3) == 0;
+    const int nc = min(n, N - 4);
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+      if (src[s]) {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+          const long r = P.w_off + (long)min(m + it * dm, M - 1) * P.nout;
+          if (al) {
+            ld4v(src[s], r + nc, in[it].x[s]);
+          } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) in[it].x[s][k] = src[s][r + min(n + k, N - 1)];
+          }
+        }
       }
   }
   __device__ __forceinline__ void load(int bz, int m, int n, int cnt, ParamIn& in) const {
@@ -538,6 +597,39 @@ __device__ __forceinline__ void walk_tile(float* S1, float* S2, int mr0, int n0,
       }
       walked = true;
     }
+  }
+  if constexpr (Epi::PRELOAD && NT == 256) {
+    // Any tile: every row's inputs first (single elements from clamped indices,
+    // no branch around a load), then the rows inside the output.
+    constexpr int TPR = BN / 4;
+    constexpr int RPI = NT / TPR;
+    constexpr int NIT = RP / RPI;
+    static_assert(RP % RPI == 0, "rows per thread");
+    const int c = (tid % TPR) * 4;
+    const int n = n0 + c;
+    typename Epi::In in[NIT];
+    epi.template load_rows_clamped<NIT>(bz, mr0 + tid / TPR, RPI, n, in);
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int rr = tid / TPR + it * RPI;
+      const int m = mr0 + rr;
+      if (m < epi.M && n < epi.N) {
+        float c1[4], c2[4], t1[4], t2[4];
+        const int si = stage_idx<SLD>(rr, c);
+        const float4 x1 = *reinterpret_cast<const float4*>(S1 + si);
+        c1[0] = x1.x; c1[1] = x1.y; c1[2] = x1.z; c1[3] = x1.w;
+        if constexpr (HC2) {
+          const float4 x2 = *reinterpret_cast<const float4*>(S2 + si);
+          c2[0] = x2.x; c2[1] = x2.y; c2[2] = x2.z; c2[3] = x2.w;
+        } else {
+          c2[0] = c2[1] = c2[2] = c2[3] = 0.0f;
+        }
+        epi.row_in(bz, m, n, min(4, epi.N - n), in[it], c1, c2, t1, t2);
+        if (nT > 0) *reinterpret_cast<float4*>(S1 + si) = make_float4(t1[0], t1[1], t1[2], t1[3]);
+        if (nT > 1) *reinterpret_cast<float4*>(S2 + si) = make_float4(t2[0], t2[1], t2[2], t2[3]);
+      }
+    }
+    walked = true;
   }
   if (!walked) {
     constexpr int TPR = BN / 4;        // threads per row, 4 columns each
