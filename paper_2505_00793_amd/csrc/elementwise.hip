@@ -256,6 +256,15 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
   }
   const float* z = a.Z + (long)row * C;
   const float* zd = a.dual ? a.Zd + (long)row * C : nullptr;
+  // dL/dz (and its tangent) of class c in both layouts
+  auto put = [&](int c, float v, float vd) {
+    a.d[(long)row * a.ld + c] = Elem<T>::from_float(v);
+    if (a.direct_t) a.dT[(long)c * a.ldT + row] = Elem<T>::from_float(v);
+    if (a.dual) {
+      a.dd[(long)row * a.ld + c] = Elem<T>::from_float(vd);
+      if (a.direct_t) a.ddT[(long)c * a.ldT + row] = Elem<T>::from_float(vd);
+    }
+  };
   float w = 1.0f;
   if (a.alpha_logits) w = 1.0f / (1.0f + expf(-a.alpha_logits[row]));
   const float scale = w * a.inv_n;
@@ -315,6 +324,13 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
       }
       store4(a.d + (long)row * a.ld + c, dv[0], dv[1], dv[2], dv[3]);
       if (a.dual) store4(a.dd + (long)row * a.ld + c, ddv[0], ddv[1], ddv[2], ddv[3]);
+      if (a.direct_t) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          a.dT[(long)(c + k) * a.ldT + row] = Elem<T>::from_float(dv[k]);
+          if (a.dual) a.ddT[(long)(c + k) * a.ldT + row] = Elem<T>::from_float(ddv[k]);
+        }
+      }
     }
   } else if (a.loss == 2) {
     // Squared error after the M-step map y_i = i (2 + sin y_{i-1})^cos y_{i-1},
@@ -340,13 +356,13 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
       }
       const float r = g - t[c];
       loss += r * r * invC;
-      a.d[(long)row * a.ld + c] = Elem<T>::from_float(2.0f * scale * invC * r * g1);
+      float vd = 0.0f;
       if (a.dual) {
         const float zdc = zd[c];
         ldot += 2.0f * invC * r * g1 * zdc;
-        a.dd[(long)row * a.ld + c] =
-            Elem<T>::from_float(2.0f * scale * invC * zdc * (g1 * g1 + r * g2));
+        vd = 2.0f * scale * invC * zdc * (g1 * g1 + r * g2);
       }
+      put(c, 2.0f * scale * invC * r * g1, vd);
     }
     loss = wave_sum(loss);
     ldot = wave_sum(ldot);
@@ -373,25 +389,15 @@ __global__ void __launch_bounds__(256) loss_kernel(LossArgs<T> a) {
     }
     for (int c = lane; c < C; c += 64) {
       const float p = expf(z[c] - lse);
-      const float d = scale * (p - (c == y ? 1.0f : 0.0f));
-      a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
-      if (a.dual) {
-        const float dd = scale * p * (zd[c] - s);
-        a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
-      }
+      put(c, scale * (p - (c == y ? 1.0f : 0.0f)), a.dual ? scale * p * (zd[c] - s) : 0.0f);
     }
   } else {
     const float* t = a.targets + (long)row * C;
     for (int c = lane; c < C; c += 64) {
       const float r = z[c] - t[c];
       loss += r * r;
-      const float d = 2.0f * scale * r;
-      a.d[(long)row * a.ld + c] = Elem<T>::from_float(d);
-      if (a.dual) {
-        ldot += 2.0f * r * zd[c];
-        const float dd = 2.0f * scale * zd[c];
-        a.dd[(long)row * a.ld + c] = Elem<T>::from_float(dd);
-      }
+      if (a.dual) ldot += 2.0f * r * zd[c];
+      put(c, 2.0f * scale * r, a.dual ? 2.0f * scale * zd[c] : 0.0f);
     }
     loss = wave_sum(loss);
     ldot = wave_sum(ldot);
@@ -1320,10 +1326,15 @@ hipError_t bias_reduce(const T* dZT, const T* dZdT, int ld, int rows, const Para
 }
 
 template <typename T>
-hipError_t loss_head(const LossArgs<T>& a, hipStream_t s) {
+hipError_t loss_head(const LossArgs<T>& args, hipStream_t s) {
+  // Up to 128 classes the loss kernel writes the transposed copies itself (a
+  // wave's C strided stores per row cost less than a transpose launch); wider
+  // heads are transposed through LDS tiles afterwards.
+  LossArgs<T> a = args;
+  a.direct_t = a.C <= 128 ? 1 : 0;
   hipLaunchKernelGGL(loss_kernel<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.direct_t) return e;
   // transposed copies of dL/dz (and its tangent), coalesced through LDS
   const dim3 tg(cdiv(a.C, 64), cdiv(a.rows, 64), 2);
   if constexpr (sizeof(T) == 2) {

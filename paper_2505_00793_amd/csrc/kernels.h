@@ -184,6 +184,7 @@ struct LossArgs {
   T* dd; T* ddT;            // its tangent (dual)
   int ld, ldT;
   int pad_to;               // columns C .. pad_to - 1 of d (dd) are written as zero
+  int direct_t;             // set by loss_head: the kernel also writes dT (ddT) itself
   float* loss_rows;         // l_n (unweighted), or null
   float* mvp_rows;          // (1/N) ldot_n, or null
   float* deta_rows;         // sigmoid'(eta_n) (1/N) ldot_n, or null
