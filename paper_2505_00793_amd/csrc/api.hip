@@ -489,8 +489,8 @@ struct Eng {
         e.ld = (int)p->ld(nin);
         e.ldT = (int)p->ld(R);
       }
-      // the bias entries: summed by the backward-weight GEMM on its
-      // direct-to-LDS path, else by a reduction over dZ^T
+      // the bias entries: summed by the backward-weight GEMM itself unless it
+      // runs split-K, else by a reduction over dZ^T
       P.fuse_bias = p->d.has_bias && gemm_fuses_bias<T>(opw, flags_w) ? 1 : 0;
       // the two products are independent: small ones share one launch
       const bool paired = l > 0 && gemm_pairs<T>(opw, flags_w, opd, flags_d);

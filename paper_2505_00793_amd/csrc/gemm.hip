@@ -110,6 +110,20 @@ __device__ __forceinline__ uint4 mask_chunk(const uint4& v, int gr, int gk, int 
   for (int e = 0; e < VE; ++e) u.e[e] = gr < M && gk + e < K ? u.e[e] : z;
   return u.v;
 }
+// Sum of a chunk's elements, in order.
+template <typename T>
+__device__ __forceinline__ float chunk_sum(const uint4& v) {
+  constexpr int VE = Elem<T>::VE;
+  union {
+    uint4 v;
+    T e[VE];
+  } u;
+  u.v = v;
+  float s = 0.0f;
+#pragma unroll
+  for (int e = 0; e < VE; ++e) s += Elem<T>::to_float(u.e[e]);
+  return s;
+}
 
 // ------------------------------------------------------------------------------------
 // Epilogues.  row(m, n, cnt, c1, c2, t1, t2): cnt (1..4) consecutive columns
@@ -745,6 +759,30 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 
   uint4 ra[NAS][ACH], rb[NBS][BCH];
 
+  // Parameter epilogues with fused bias: as in the direct-to-LDS kernel, the
+  // tiles of a tile column share out its BN bias entries; each B (and Bd) chunk
+  // of a row in this tile's share is added up as it is stored to LDS, in k
+  // order, and the CPR threads of a row then combine their sums in lane order.
+  constexpr bool BIAS = IsParamOp<Epi>::value;
+  int br0 = 0, bnr = 0;
+  float bsum[BCH], bdsum[BCH];
+  ParamIn bin[BCH];
+  if constexpr (BIAS) {
+    if (bz == 0 && epi.fuse_bias()) {
+      const int tiles_m = (op.M + BM - 1) / BM;
+      const int rpt = (BN + tiles_m - 1) / tiles_m;   // bias rows per tile
+      br0 = (m0 / BM) * rpt;
+      bnr = max(0, min(BN, br0 + rpt) - br0);
+    }
+#pragma unroll
+    for (int c = 0; c < BCH; ++c) {
+      bsum[c] = bdsum[c] = 0.0f;
+      const int rr = (tid + c * 256) / CPR;
+      if (rr >= br0 && rr < br0 + bnr && tid % CPR == 0 && n0 + rr < op.N)
+        epi.bias_load(n0 + rr, bin[c]);
+    }
+  }
+
   auto gload = [&](int k0) {
 #pragma unroll
     for (int s = 0; s < NAS; ++s) {
@@ -782,8 +820,16 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
 #pragma unroll
       for (int c = 0; c < BCH; ++c) {
         int ch = tid + c * 256;
-        *reinterpret_cast<uint4*>(base + (NAS * BM + s * BN + ch / CPR) * LDL + (ch % CPR) * VE) =
+        const uint4 v =
             mask_chunk<T, KVEC>(rb[s][c], n0 + ch / CPR, k0 + (ch % CPR) * VE, op.N, op.K);
+        *reinterpret_cast<uint4*>(base + (NAS * BM + s * BN + ch / CPR) * LDL + (ch % CPR) * VE) =
+            v;
+        if constexpr (BIAS) {
+          if (bnr > 0) {
+            if (s == 0) bsum[c] += chunk_sum<T>(v);
+            else bdsum[c] += chunk_sum<T>(v);
+          }
+        }
       }
   };
 
@@ -834,6 +880,20 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
     }
     if (kt + 1 < nk) sstore(buf ^ 1, (kt + 1) * BK);
     __syncthreads();
+  }
+  if constexpr (BIAS) {
+    if (bnr > 0) {   // uniform: every lane of the block takes part in the shuffles
+#pragma unroll
+      for (int c = 0; c < BCH; ++c) {
+        for (int o = 1; o < CPR; o <<= 1) {
+          bsum[c] += __shfl_xor(bsum[c], o, 64);
+          bdsum[c] += __shfl_xor(bdsum[c], o, 64);
+        }
+        const int rr = (tid + c * 256) / CPR;
+        if (rr >= br0 && rr < br0 + bnr && tid % CPR == 0 && n0 + rr < op.N)
+          epi.bias_finish(n0 + rr, bin[c], bsum[c], bdsum[c]);
+      }
+    }
   }
   run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem_raw, m0, n0, bz, epi);
 }
@@ -1498,9 +1558,12 @@ hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const
   return gemm_act_bwd<T>(opd, flags_d, e, s);
 }
 
+// Both tile kernels sum the bias entries of a parameter epilogue; split-K
+// launches and batched products do not.
 template <typename T>
 bool gemm_fuses_bias(const GemmOperands<T>& op, int flags) {
-  return dma_tile_kind(op) >= 0 && (flags & (G_C1 | G_AD)) != 0;
+  if ((flags & (G_C1 | G_AD)) == 0 || op.batch != 1 || op.M <= 0 || op.N <= 0) return false;
+  return !(op.ws && splitk_count(op.M, op.N, op.K) > 1);
 }
 template bool gemm_fuses_bias<bf16_t>(const GemmOperands<bf16_t>&, int);
 template bool gemm_fuses_bias<float>(const GemmOperands<float>&, int);

@@ -42,8 +42,9 @@ long gemm_splitk_floats(int M, int N, int K);
 // M x N output over K uses for split-K when given it (few output tiles, long k);
 // 0 when it runs without.
 long gemm_splitk_fwd_f32_floats(int M, int N, int K);
-// Whether the parameter GEMM of op / flags (B = dZ^T, Bd = its tangent) runs on
-// the direct-to-LDS path that can sum the bias gradients of P.fuse_bias.
+// Whether the parameter GEMM of op / flags (B = dZ^T, Bd = its tangent) sums the
+// bias gradients of P.fuse_bias itself (either tile kernel; not split-K or
+// batched launches).
 template <typename T>
 bool gemm_fuses_bias(const GemmOperands<T>& op, int flags);
 
@@ -164,8 +165,9 @@ struct ParamArgs {
   T* outW; T* outWT; float* outb;
   int ldW, ldWT;
   // set by the host when the backward-weight GEMM also finishes the bias
-  // entries (its first row of tiles sums the rows of dZ^T it stages; see
-  // gemm_fuses_bias), so that no separate reduction runs
+  // entries (the tiles of each tile column share out the column's entries and
+  // sum the rows of dZ^T they stage; see gemm_fuses_bias), so that no separate
+  // reduction runs
   int fuse_bias;
 };
 
