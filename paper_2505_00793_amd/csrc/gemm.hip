@@ -1334,10 +1334,11 @@ int splitk_count(int M, int N, int K) {
 
 // Float32 products with at most 8 output tiles of 64 x 64 and a long k (say a
 // 784-deep first layer with 128 x 256 outputs: 8 workgroups would each walk all
-// of k): up to 8 k slices, each at least 64 deep and a multiple of 4.
+// of k), or at most 2 tiles and k >= 256 (a 10-wide output layer over 128 rows):
+// up to 8 k slices, each at least 64 deep and a multiple of 4.
 int splitk_count_small(int M, int N, int K) {
   const int tiles = cdiv(M, 64) * cdiv(N, 64);
-  if (M <= 0 || N <= 0 || tiles > 8 || K < 512) return 1;
+  if (M <= 0 || N <= 0 || tiles > 8 || K < (tiles <= 2 ? 256 : 512)) return 1;
   int S = 8;
   while (S > 1 && (K % S != 0 || (K / S) % 4 != 0 || K / S < 64)) --S;
   return S;
