@@ -78,24 +78,44 @@ __global__ void __launch_bounds__(256) convert_vec_kernel(ConvJobs<T> J, int bat
   T* dstT = P.dstT;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int c = c0 + tx * 4;
-  for (int i = ty; i < 64; i += 16) {
-    const int r = r0 + i;
-    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (r < rows) {
-      if (c + 4 <= cols) {
-        const float4 x = *reinterpret_cast<const float4*>(src + (long)r * lds + c);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-        if (dst) store4(dst + (long)r * ldd + c, v[0], v[1], v[2], v[3]);
-      } else {
+  if ((cols & 3) == 0) {
+    // every 16-byte chunk lies wholly inside or outside the matrix: the thread's
+    // four rows are requested at once, from indices clamped into it, and the
+    // chunks outside are zeroed on their way to LDS
+    const int cl = min(c, cols - 4);
+    float4 x[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          if (c + k < cols) {
-            v[k] = src[(long)r * lds + c + k];
-            if (dst) dst[(long)r * ldd + c + k] = Elem<T>::from_float(v[k]);
-          }
-      }
+    for (int it = 0; it < 4; ++it)
+      x[it] = *reinterpret_cast<const float4*>(src + (long)min(r0 + ty + 16 * it, rows - 1) * lds +
+                                               cl);
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int i = ty + 16 * it, r = r0 + i;
+      const bool in = r < rows && c < cols;
+      const float4 v = in ? x[it] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (in && dst) store4(dst + (long)r * ldd + c, v.x, v.y, v.z, v.w);
+      *reinterpret_cast<float4*>(&tile[i][tx * 4]) = v;
     }
-    *reinterpret_cast<float4*>(&tile[i][tx * 4]) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    for (int i = ty; i < 64; i += 16) {
+      const int r = r0 + i;
+      float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (r < rows) {
+        if (c + 4 <= cols) {
+          const float4 x = *reinterpret_cast<const float4*>(src + (long)r * lds + c);
+          v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+          if (dst) store4(dst + (long)r * ldd + c, v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (c + k < cols) {
+              v[k] = src[(long)r * lds + c + k];
+              if (dst) dst[(long)r * ldd + c + k] = Elem<T>::from_float(v[k]);
+            }
+        }
+      }
+      *reinterpret_cast<float4*>(&tile[i][tx * 4]) = make_float4(v[0], v[1], v[2], v[3]);
+    }
   }
   if (!dstT) return;
   __syncthreads();
