@@ -1433,6 +1433,8 @@ hipError_t linreg_meta_grad(const float* theta0, const float* eta, const float* 
   a.d_eta = d_eta;
   a.val_loss = val_loss;
   a.ckpt = scratch;
+  // batches that fit one register set per thread: the register-resident kernel;
+  // else batches staged in LDS (16-byte or 4-byte loads) or read from global memory
   if (a.vec && d <= LRR_MAXD && rows <= LRR_MAXROWS && vrows <= LRR_MAXROWS) {
     if ((T + 1) * d <= LR_CKPT)
       hipLaunchKernelGGL(linreg_reg_kernel<true>, dim3(1), dim3(LR_THREADS), 0, s, a);
