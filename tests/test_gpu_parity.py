@@ -54,9 +54,10 @@ def run_meta(cfg, inp):
 
 
 META_CASES = ["c1_small", "c1_wide", "c1_long", "c1_vec", "c1_reg", "c1_reg_long", "c2_small",
-              "c2_splitk", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small", "c5_small_long",
-              "c5_tall", "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32", "c5_maml",
-              "c5_maml_r8_fp32", "toy_small", "toy_mid", "c1_linreg", "c2_mlp_tanh_lossweights"]
+              "c2_splitk", "c2_narrow", "c3_fp32", "c5_tanh_fp32", "c5_gelu_fp32", "c5_small",
+              "c5_small_long", "c5_tall", "c3_small", "c5_mid", "c5_r8", "c5_rag2", "c5_maml_fp32",
+              "c5_maml", "c5_maml_r8_fp32", "toy_small", "toy_mid", "c1_linreg",
+              "c2_mlp_tanh_lossweights"]
 
 
 def start_of(cfg, inp):
@@ -105,8 +106,9 @@ def test_segment_checkpoints_full_size(name, T, k):
     assert p1 < p0
 
 
-INNER_CASES = ["c1_small", "c2_small", "c2_splitk", "c3_fp32", "c5_tanh_fp32", "c5_small",
-               "c5_tall", "c3_small", "c5_r8", "c5_mid_r8", "toy_small", "c5_slice2", "c5_slice3"]
+INNER_CASES = ["c1_small", "c2_small", "c2_splitk", "c2_narrow", "c3_fp32", "c5_tanh_fp32",
+               "c5_small", "c5_tall", "c3_small", "c5_r8", "c5_mid_r8", "toy_small", "c5_slice2",
+               "c5_slice3"]
 
 
 @pytest.mark.parametrize("name,k", [("c5_small", 1), ("c5_small", 3), ("c5_r8", 2),
@@ -187,9 +189,9 @@ def test_inner_step_parity(name):
         assert relerr(opt1.cpu().numpy()[n:], opt1_ref[n:]) <= tol
 
 
-HVP_CASES = ["toy_small", "c1_small", "c2_small", "c2_splitk", "c5_tanh_fp32", "c5_gelu_fp32",
-             "c5_small", "c5_tall", "c3_small", "c5_mid", "c5_r8", "c5_mid_r8", "c5_slice2",
-             "c5_slice3"]
+HVP_CASES = ["toy_small", "c1_small", "c2_small", "c2_splitk", "c2_narrow", "c5_tanh_fp32",
+             "c5_gelu_fp32", "c5_small", "c5_tall", "c3_small", "c5_mid", "c5_r8", "c5_mid_r8",
+             "c5_slice2", "c5_slice3"]
 
 
 @pytest.mark.parametrize("name", HVP_CASES)
