@@ -503,7 +503,7 @@ struct Smem {
   static constexpr int NBS = (FLAGS & G_BD) ? 2 : 1;
   static constexpr int STAGE = (NAS * BM + NBS * BN) * LDL;  // elements
   static constexpr int PIPE_BYTES = 2 * STAGE * (int)sizeof(T);
-  static constexpr int EPI_BYTES = EpiSmem<FLAGS, BM, BN, 2>::BYTES;
+  static constexpr int EPI_BYTES = EpiSmem<FLAGS, BM, BN, BM == 64 ? 1 : 2>::BYTES;
   static constexpr int BYTES = PIPE_BYTES > EPI_BYTES ? PIPE_BYTES : EPI_BYTES;
 };
 
@@ -694,18 +694,28 @@ __device__ __forceinline__ void walk_tile(float* S1, float* S2, int mr0, int n0,
   __syncthreads();
 }
 
-// Two-slab epilogue of the 256-thread kernels: one wave row (BM / 2 rows) at a
-// time in half the LDS.  The caller guarantees that no wave still reads or
-// writes smem.
+// Epilogue of the 256-thread kernels.  A 64-row tile is staged whole (it fits in
+// the LDS of the main loop) and walked in one pass, so a thread requests the
+// epilogue inputs of all its rows at once; a 128-row tile goes one wave row
+// (BM / 2 rows) at a time in half the LDS.  The caller guarantees that no wave
+// still reads or writes smem.
 template <int FLAGS, int BM, int BN, class Epi>
 __device__ __forceinline__ void run_epilogue(const f32x4 (&acc1)[BM / 32][BN / 32],
                                              const f32x4 (&acc2)[BM / 32][BN / 32],
                                              char* smem_raw, int m0, int n0, int bz,
                                              const Epi& epi) {
+  const int wm = threadIdx.x >> 7;
+  if constexpr (BM == 64) {
+    float* S1 = reinterpret_cast<float*>(smem_raw);
+    float* S2 = S1 + BM * Stage<BN>::SLD;
+    stage_tile<FLAGS, BM, BN, BM>(acc1, acc2, S1, S2, wm * (BM / 2));
+    __syncthreads();
+    walk_tile<FLAGS, BN, BM, 256>(S1, S2, m0, n0, bz, epi);
+    return;
+  }
   constexpr int RP = BM / 2;
   float* S1 = reinterpret_cast<float*>(smem_raw);
   float* S2 = S1 + RP * Stage<BN>::SLD;
-  const int wm = threadIdx.x >> 7;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
     if (wm == pass) stage_tile<FLAGS, BM, BN, RP>(acc1, acc2, S1, S2, 0);
