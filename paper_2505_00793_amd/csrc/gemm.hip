@@ -1370,17 +1370,29 @@ __global__ void __launch_bounds__(256) splitk_epilogue(const float* __restrict__
   float c1[4] = {0.f, 0.f, 0.f, 0.f}, c2[4] = {0.f, 0.f, 0.f, 0.f};
   float t1[4] = {0.f, 0.f, 0.f, 0.f}, t2[4] = {0.f, 0.f, 0.f, 0.f};
   if (m < M && cn > 0) {
-    const bool vec = cn == 4 && (N & 3) == 0;
-    for (int sp = 0; sp < S; ++sp) {
-      const long off = sp * MN + (long)m * N + n;
-      if (vec) {
-        const float4 x = *reinterpret_cast<const float4*>(P1 + off);
-        c1[0] += x.x; c1[1] += x.y; c1[2] += x.z; c1[3] += x.w;
-        if (P2) {
-          const float4 y = *reinterpret_cast<const float4*>(P2 + off);
-          c2[0] += y.x; c2[1] += y.y; c2[2] += y.z; c2[3] += y.w;
+    constexpr int SMAX = 8;   // the most slices a split-K launch makes
+    if (cn == 4 && (N & 3) == 0 && S <= SMAX) {
+      // every slice's 16 bytes requested before the first is added; the sum
+      // keeps the slice order
+      float4 x[SMAX], y[SMAX];
+#pragma unroll
+      for (int sp = 0; sp < SMAX; ++sp)
+        if (sp < S) {
+          const long off = sp * MN + (long)m * N + n;
+          x[sp] = *reinterpret_cast<const float4*>(P1 + off);
+          if (P2) y[sp] = *reinterpret_cast<const float4*>(P2 + off);
         }
-      } else {
+#pragma unroll
+      for (int sp = 0; sp < SMAX; ++sp)
+        if (sp < S) {
+          c1[0] += x[sp].x; c1[1] += x[sp].y; c1[2] += x[sp].z; c1[3] += x[sp].w;
+          if (P2) {
+            c2[0] += y[sp].x; c2[1] += y[sp].y; c2[2] += y[sp].z; c2[3] += y[sp].w;
+          }
+        }
+    } else {
+      for (int sp = 0; sp < S; ++sp) {
+        const long off = sp * MN + (long)m * N + n;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           if (k < cn) {
