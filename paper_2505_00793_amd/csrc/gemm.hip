@@ -1066,7 +1066,7 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
     // of the B and Bd rows, btpr threads per row, each over its 16-byte chunks
     // in their order in LDS; the btpr partial sums of a row are then combined in
     // lane order.  The entries' epilogue inputs are loaded before the loop.
-    constexpr bool BIAS = IsParamOp<Epi>::value && SM::LB;
+    constexpr bool BIAS = IsParamOp<Epi>::value && (SM::LB || SM::LBD);
     const int lt = tid - 256;
     bool bias_w = false;
     int brow = 0, btpr = 1, bcpt = CPR;
@@ -1101,11 +1101,13 @@ __device__ __forceinline__ void gemm_ws_tile(const GemmOperands<bf16_t>& op, con
           const int c0 = (lt % btpr) * bcpt;
           for (int c = 0; c < bcpt; ++c) {
             const int off = brow * ROWB + (c0 + c) * 16;
-            const u32x4 u = lds_read16(st + SM::OFF_B + off);
-            u32x4 ud = u;
+            // a product without a B tile (tangent only: an Adam reverse, whose
+            // epilogue reads no gradient) sums Bd alone
+            u32x4 u = {0u, 0u, 0u, 0u}, ud = {0u, 0u, 0u, 0u};
+            if constexpr (SM::LB) u = lds_read16(st + SM::OFF_B + off);
             if constexpr (SM::LBD) ud = lds_read16(st + SM::OFF_BD + off);
             lds_read_wait();
-            bsum += sum8(u);
+            if constexpr (SM::LB) bsum += sum8(u);
             if constexpr (SM::LBD) bdsum += sum8(ud);
           }
         }
@@ -1585,7 +1587,7 @@ hipError_t gemm_param_and_act_bwd(const GemmOperands<T>& opw, int flags_w, const
 // launches and batched products do not.
 template <typename T>
 bool gemm_fuses_bias(const GemmOperands<T>& op, int flags) {
-  if ((flags & (G_C1 | G_AD)) == 0 || op.batch != 1 || op.M <= 0 || op.N <= 0) return false;
+  if (flags == 0 || op.batch != 1 || op.M <= 0 || op.N <= 0) return false;
   return !(op.ws && splitk_count(op.M, op.N, op.K) > 1);
 }
 template bool gemm_fuses_bias<bf16_t>(const GemmOperands<bf16_t>&, int);
