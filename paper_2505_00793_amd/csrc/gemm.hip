@@ -538,21 +538,22 @@ __device__ __forceinline__ int stage_idx(int row, int col) {
   return row * SLD + (col ^ (((row >> 4) & 3) << 2));
 }
 
-// Accumulators of the four computing waves (2 x 2 arrangement, each TM x TN
-// tiles of 16 x 16) -> LDS staging buffer, rows [row0, row0 + RP) of the tile.
-// C layout of a 16x16 MFMA tile: lane holds rows 4*(lane/16) + 0..3 of column
-// lane%16.  Called by the waves whose rows fall in the slab.
-template <int FLAGS, int BM, int BN, int RP>
-__device__ __forceinline__ void stage_tile(const f32x4 (&acc1)[BM / 32][BN / 32],
-                                           const f32x4 (&acc2)[BM / 32][BN / 32], float* S1,
-                                           float* S2, int rbase) {
+// Accumulators of the four computing waves (WN = 2: a 2 x 2 arrangement; WN = 1:
+// four waves stacked along m, for 16-column tiles; each TM x TN tiles of 16 x 16)
+// -> LDS staging buffer, the wave's rows from rbase.  C layout of a 16x16 MFMA
+// tile: lane holds rows 4*(lane/16) + 0..3 of column lane%16.  Called by the
+// waves whose rows fall in the slab.
+template <int FLAGS, int BM, int BN, int RP, int WN = 2>
+__device__ __forceinline__ void stage_tile(const f32x4 (&acc1)[BM * WN / 64][BN / (16 * WN)],
+                                           const f32x4 (&acc2)[BM * WN / 64][BN / (16 * WN)],
+                                           float* S1, float* S2, int rbase) {
   constexpr bool HC1 = (FLAGS & G_C1) != 0;
   constexpr bool HC2 = (FLAGS & (G_AD | G_BD)) != 0;
-  constexpr int WTN = BN / 2;
-  constexpr int TM = BM / 32, TN = BN / 32;
+  constexpr int WTN = BN / WN;
+  constexpr int TM = BM * WN / 64, TN = BN / (16 * WN);
   constexpr int SLD = Stage<BN>::SLD;
   const int lane = threadIdx.x & 63;
-  const int wn = (threadIdx.x >> 6) & 1;
+  const int wn = (threadIdx.x >> 6) % WN;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -699,28 +700,28 @@ __device__ __forceinline__ void walk_tile(float* S1, float* S2, int mr0, int n0,
 // epilogue inputs of all its rows at once; a 128-row tile goes one wave row
 // (BM / 2 rows) at a time in half the LDS.  The caller guarantees that no wave
 // still reads or writes smem.
-template <int FLAGS, int BM, int BN, class Epi>
-__device__ __forceinline__ void run_epilogue(const f32x4 (&acc1)[BM / 32][BN / 32],
-                                             const f32x4 (&acc2)[BM / 32][BN / 32],
+template <int FLAGS, int BM, int BN, int WN, class Epi>
+__device__ __forceinline__ void run_epilogue(const f32x4 (&acc1)[BM * WN / 64][BN / (16 * WN)],
+                                             const f32x4 (&acc2)[BM * WN / 64][BN / (16 * WN)],
                                              char* smem_raw, int m0, int n0, int bz,
                                              const Epi& epi) {
-  const int wm = threadIdx.x >> 7;
+  const int wm = (threadIdx.x >> 6) / WN;
   if constexpr (BM == 64) {
     float* S1 = reinterpret_cast<float*>(smem_raw);
     float* S2 = S1 + BM * Stage<BN>::SLD;
-    stage_tile<FLAGS, BM, BN, BM>(acc1, acc2, S1, S2, wm * (BM / 2));
+    stage_tile<FLAGS, BM, BN, BM, WN>(acc1, acc2, S1, S2, wm * (BM * WN / 4));
     __syncthreads();
     walk_tile<FLAGS, BN, BM, 256>(S1, S2, m0, n0, bz, epi);
-    return;
-  }
-  constexpr int RP = BM / 2;
-  float* S1 = reinterpret_cast<float*>(smem_raw);
-  float* S2 = S1 + RP * Stage<BN>::SLD;
+  } else {
+    constexpr int RP = BM / 2;
+    float* S1 = reinterpret_cast<float*>(smem_raw);
+    float* S2 = S1 + RP * Stage<BN>::SLD;
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    if (wm == pass) stage_tile<FLAGS, BM, BN, RP>(acc1, acc2, S1, S2, 0);
-    __syncthreads();
-    walk_tile<FLAGS, BN, RP, 256>(S1, S2, m0 + pass * RP, n0, bz, epi);
+    for (int pass = 0; pass < 2; ++pass) {
+      if (wm == pass) stage_tile<FLAGS, BM, BN, RP, WN>(acc1, acc2, S1, S2, 0);
+      __syncthreads();
+      walk_tile<FLAGS, BN, RP, 256>(S1, S2, m0 + pass * RP, n0, bz, epi);
+    }
   }
 }
 
@@ -741,7 +742,9 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   constexpr int NAS = SM::NAS;
   constexpr int NBS = SM::NBS;
   constexpr int STAGE = SM::STAGE;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
+  // 2 x 2 waves over the tile, or 4 x 1 (stacked along m) for 16-column tiles
+  constexpr int WN = BN >= 32 ? 2 : 1, WM = 4 / WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
   constexpr int CPR = BK / VE;           // 16-byte chunks per tile row
   constexpr int ACH = BM * CPR / 256;    // chunks per thread, A-side tile
@@ -756,7 +759,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   int m0, n0;
   tile_origin<BM, BN>(op.M, op.N, m0, n0);
   const int bz = blockIdx.y;
@@ -905,7 +908,7 @@ __global__ void __launch_bounds__(256) gemm_nt(GemmOperands<T> op, Epi epi) {
       }
     }
   }
-  run_epilogue<FLAGS, BM, BN>(acc1, acc2, smem_raw, m0, n0, bz, epi);
+  run_epilogue<FLAGS, BM, BN, WN>(acc1, acc2, smem_raw, m0, n0, bz, epi);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1313,8 +1316,8 @@ hipError_t launch(const GemmOperands<T>& op, const Epi& epi, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  if constexpr (BN >= 64) {
-    constexpr int BK = KDepth<FLAGS, Epi>::value;
+  if constexpr (BN >= 64 || BN == 16) {
+    constexpr int BK = BN == 16 ? 64 : KDepth<FLAGS, Epi>::value;
     if (op.K % Elem<T>::VE == 0)
       hipLaunchKernelGGL((gemm_nt<T, FLAGS, BM, BN, BK, Epi, true>), dim3(tiles, op.batch),
                          dim3(256), 0, s, op, epi);
@@ -1351,6 +1354,7 @@ int splitk_count(int M, int N, int K) {
 int splitk_count_small(int M, int N, int K) {
   const int tiles = cdiv(M, 64) * cdiv(N, 64);
   if (M <= 0 || N <= 0 || tiles > 8 || K < (tiles <= 2 ? 256 : 512)) return 1;
+  if (N <= 16 && K <= 4096) return 1;   // 64 x 16 tiles instead (launch_sized)
   int S = 8;
   while (S > 1 && (K % S != 0 || (K / S) % 4 != 0 || K / S < 64)) --S;
   return S;
@@ -1464,6 +1468,11 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
       if (S > 1 && op.ws_floats >= 2L * S * op.M * op.N)
         return launch_splitk<T, FLAGS>(op, epi, S, s);
     }
+  }
+  if constexpr (sizeof(T) == 4) {
+    // at most 16 output columns: 64 x 16 tiles, a quarter of a 64 x 64 tile's
+    // MFMA work (k at most 4096; longer narrow products split k above)
+    if (op.N <= 16 && op.K <= 4096) return launch<T, FLAGS, 64, 16>(op, epi, s);
   }
   if constexpr (sizeof(T) == 4 && IsActFwdOp<Epi>::value) {
     if (op.ws && op.batch == 1) {
