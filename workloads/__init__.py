@@ -158,9 +158,10 @@ SMALL: Dict[str, Config] = {
     # ones (more tiles) do not
     "c2_splitk": C2.with_(name="c2_splitk", cfg_id=126, widths=(608, 72, 10), rows=36,
                           val_rows=300, T=3),
-    # a narrow float32 output layer over few rows: 90 x 7 outputs (2 tiles) contracting
-    # over 320, split into 5 k slices of 64 (ragged rows in the last tile)
-    "c2_narrow": C2.with_(name="c2_narrow", cfg_id=136, widths=(96, 320, 7), rows=90,
+    # a float32 output layer over few rows: 90 x 20 outputs (2 tiles of 64 x 64; wider
+    # than the 16 columns of the narrow tiles) contracting over 320, split into 5 k
+    # slices of 64 (ragged rows in the last tile)
+    "c2_narrow": C2.with_(name="c2_narrow", cfg_id=136, widths=(96, 320, 20), rows=90,
                           val_rows=70, T=3),
     "c3_small": C3.with_(name="c3_small", cfg_id=103, widths=(136, 200, 72, 10), rows=150,
                          val_rows=96, T=4),
