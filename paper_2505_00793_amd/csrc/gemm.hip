@@ -1471,8 +1471,12 @@ hipError_t launch_sized(const GemmOperands<T>& op, const Epi& epi, hipStream_t s
   }
   if constexpr (sizeof(T) == 4) {
     // at most 16 output columns: 64 x 16 tiles, a quarter of a 64 x 64 tile's
-    // MFMA work (k at most 4096; longer narrow products split k above)
+    // MFMA work (k at most 4096; longer narrow products split k above); also
+    // short-k products with few 64 x 64 tiles, whose time is their epilogue:
+    // four times the workgroups, each with a quarter of the outputs
     if (op.N <= 16 && op.K <= 4096) return launch<T, FLAGS, 64, 16>(op, epi, s);
+    if (op.K <= 128 && cdiv(op.M, 64) * cdiv(op.N, 64) * op.batch < 64)
+      return launch<T, FLAGS, 64, 16>(op, epi, s);
   }
   if constexpr (sizeof(T) == 4 && IsActFwdOp<Epi>::value) {
     if (op.ws && op.batch == 1) {
