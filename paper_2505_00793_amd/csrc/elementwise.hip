@@ -1067,14 +1067,17 @@ template <bool CKL>
 __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
   __shared__ float ck[CKL ? LR_CKPT : 1];
   __shared__ __attribute__((aligned(16))) float th[LRR_MAXD], vv[LRR_MAXD];
-  __shared__ float tb[LRR_MAXD], lam[LRR_MAXD], eb[LRR_MAXD];
   __shared__ __attribute__((aligned(16))) float part[LRR_SLOTS * LRR_MAXD];
   __shared__ __attribute__((aligned(16))) float part2[LRR_SLOTS * LRR_MAXD];
   __shared__ float red[LR_THREADS / 64];
   const int tid = threadIdx.x, d = a.d, T = a.T, g4 = d >> 2;
   const int c = tid & 15, q = tid >> 4;
+  // Column j < d is owned by thread 4 j (the first of the four that sum its
+  // partials), which keeps exp(eta_j), theta_j, bar theta_j and bar eta_j in
+  // registers through the sweep.
+  const int jc = min(tid >> 2, d - 1);
   // theta_0 and eta, then the first batch; the set-up waits for the former only
-  const float th0 = a.theta0[min(tid, d - 1)], et = a.eta[min(tid, d - 1)];
+  const float th0 = a.theta0[min(tid, d - 1)], etc = a.eta[jc], thc0 = a.theta0[jc];
   LrrRegs A, B;
   {
     const LrrSrc s0 = lrr_src(lr_batch(a, 0), g4);
@@ -1083,12 +1086,12 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
     for (int u = 0; u < LRR_RPT; ++u) A.x[u] = lrr_group(s0, g4, q, c, u);
   }
   __builtin_amdgcn_sched_barrier(0);
+  const float lamr = expf(etc);
+  float thr = thc0, tbr = 0.0f, ebr = 0.0f;
   if (tid < LRR_MAXD) {
     const bool in = tid < d;
     th[tid] = in ? th0 : 0.0f;   // zero past d, like vv: the groups past d add nothing
     vv[tid] = 0.0f;
-    lam[tid] = in ? expf(et) : 0.0f;
-    eb[tid] = 0.0f;
     if (in) {
       if constexpr (CKL) ck[tid] = th0;
       else a.ckpt[tid] = th0;
@@ -1125,7 +1128,9 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
         const float sd = row16_sum(in ? dot4(x, u4) : 0.0f);
         rd[u] = valid ? sd : 0.0f;
       }
-      __builtin_amdgcn_sched_barrier(0);
+      // two rows per scheduling group: their dependent sums interleave, and
+      // the loads still go out spread over the residuals
+      if (u & 1) __builtin_amdgcn_sched_barrier(0);
     }
     // X^T r (and X^T rd) over this thread's rows, then over the row slots
     float4 ga = make_float4(0.f, 0.f, 0.f, 0.f), ha = ga;
@@ -1135,6 +1140,15 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
       ga.x += x.x * r[u]; ga.y += x.y * r[u]; ga.z += x.z * r[u]; ga.w += x.w * r[u];
       if (du) {
         ha.x += x.x * rd[u]; ha.y += x.y * rd[u]; ha.z += x.z * rd[u]; ha.w += x.w * rd[u];
+      }
+    }
+    // the column owner's theta for the next reverse step, read ahead
+    float thn = 0.0f;
+    {
+      const int i = 2 * T - k;
+      if (k >= T && i >= 1 && (tid & 3) == 0 && tid < 4 * d) {
+        if constexpr (CKL) thn = ck[(i - 1) * d + (tid >> 2)];
+        else thn = a.ckpt[(long)(i - 1) * d + (tid >> 2)];
       }
     }
     reinterpret_cast<float4*>(part)[q * 16 + c] = ga;
@@ -1159,7 +1173,8 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
       if (h == 0 && j < d) {
         if (k < T) {
           // forward step k: theta_{k+1}
-          const float t = th[j] - lam[j] * inv * g;
+          const float t = thr - lamr * inv * g;
+          thr = t;
           th[j] = t;
           if constexpr (CKL) ck[(k + 1) * d + j] = t;
           else a.ckpt[(long)(k + 1) * d + j] = t;
@@ -1170,16 +1185,14 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
           if (k == T) {
             t = inv * g;
           } else {
-            t = tb[j];
-            eb[j] += -lam[j] * inv * g * t;
+            t = tbr;
+            ebr += -lamr * inv * g * t;
             t += inv * hv;
           }
-          tb[j] = t;
-          const int i = 2 * T - k;
-          if (i >= 1) {   // the next reverse step's theta_{i-1} and v = -exp(eta) bar theta_i
-            if constexpr (CKL) th[j] = ck[(i - 1) * d + j];
-            else th[j] = a.ckpt[(long)(i - 1) * d + j];
-            vv[j] = -lam[j] * t;
+          tbr = t;
+          if (2 * T - k >= 1) {   // the next reverse step's theta_{i-1}, v = -exp(eta) bar theta_i
+            th[j] = thn;
+            vv[j] = -lamr * t;
           }
         }
       }
@@ -1197,7 +1210,7 @@ __global__ void __launch_bounds__(LR_THREADS) linreg_reg_kernel(LinregArgs a) {
     phase(k + 1, B, A, LrrLoad<true>{});
   }
   phase(2 * T, A, B, LrrLoad<false>{});
-  if (tid < d) a.d_eta[tid] = eb[tid];
+  if ((tid & 3) == 0 && tid < 4 * d) a.d_eta[tid >> 2] = ebr;
 }
 
 // Columns c0 .. c1 - 1 of rows 0 .. rows - 1 of each job's bf16 matrix set to
